@@ -1,0 +1,149 @@
+/*
+ * vc_jointattn.h -- C ABI of the joint text-video attention library (gfx950).
+ *
+ * The operation is the full-sequence branch of the multimodal diffusion block
+ * of Vchitect-2.0 (Sec. III-B, "Parallel Transformer Architecture", and the
+ * method-overview figure): multi-head self-attention across the concatenation
+ * of text tokens and spatio-temporal video tokens (Sec. V-A, "3D and
+ * multi-modal nature": attention runs over the concatenated visual and text
+ * sequence while other operators treat the two separately). Q, K and V arrive
+ * already projected per modality. The paper gives no formula; the library
+ * computes exact scaled dot-product softmax attention:
+ *
+ *   s_ij = c <q_i, k_j>,  LSE_i = ln sum_{valid j} exp(s_ij),
+ *   P_ij = exp(s_ij - LSE_i) (exactly 0 for invalid j),  O_i = sum_j P_ij v_j,
+ *
+ * and, for the backward, dV = P^T dO, dS = P o (dO V^T - D) with
+ * D_i = <dO_i, O_i>, dQ = c dS K, dK = c dS^T Q. The backward recomputes P
+ * from the stored log-sum-exp instead of keeping it, the recomputation the
+ * paper adopts for long sequences (Sec. V-B) in the manner of the attention
+ * kernels it cites (Sec. II-C).
+ *
+ * Joint sequence of sample b (N = T + F*Hp*Wp tokens):
+ *   positions [0, T)      text slot; the first clamp(text_len[b], 0, T) are
+ *                         real caption tokens, the rest padding;
+ *   positions [T, N)      video tokens, frame-major (frame, row, column).
+ * Key j of sample b is valid iff
+ *   (j >= T || j < clamp(text_len[b],0,T)) && (key_mask == NULL || key_mask[b*N+j] != 0).
+ * Every token is a query, padded ones included. A query with no valid key gets
+ * O = 0, LSE = -inf and dQ = 0. The token order inside the sequence does not
+ * change any result (attention is equivariant in queries and invariant under
+ * a joint permutation of keys and values), so the paper's interleaving of text
+ * and visual embeddings is an ordering choice the caller may make freely.
+ *
+ * Conventions for every entry point
+ *  - Tensors q, k, v, o, dout, dq, dk, dv: bf16, contiguous [B, N, H, D]
+ *    (head_dim fastest), device memory, 16-byte aligned.
+ *  - lse: fp32 [B, H, N], device memory, 16-byte aligned.
+ *  - text_len: device int32 [B] or NULL (NULL means every text token is real).
+ *  - key_mask: device uint8 [B, N] or NULL (NULL means no extra mask).
+ *  - All memory is owned by the caller. The library never allocates, frees or
+ *    synchronises, keeps no per-call state, and only launches kernels on
+ *    `stream` (a hipStream_t; NULL = the null stream). Outputs are
+ *    overwritten, never accumulated into, and must not alias inputs.
+ *  - Argument errors are reported synchronously, before anything is launched.
+ *    Faults inside kernels surface at the caller's next synchronisation with
+ *    the stream, as for any HIP kernel.
+ *  - Thread-safe: the only shared state is a per-device property cache filled
+ *    once.
+ */
+#ifndef VC_JOINTATTN_H
+#define VC_JOINTATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define VC_JOINTATTN_ABI_VERSION 1
+
+typedef enum vc_status {
+  VC_OK = 0,
+  VC_ERR_NULL = -1,        /* a required pointer is NULL                       */
+  VC_ERR_SHAPE = -2,       /* a size is out of range or N overflows            */
+  VC_ERR_HEAD_DIM = -3,    /* head_dim is not 64 or 128                        */
+  VC_ERR_ALIGN = -4,       /* a tensor pointer is not 16-byte aligned          */
+  VC_ERR_WORKSPACE = -5,   /* workspace NULL or smaller than required          */
+  VC_ERR_DEVICE = -6,      /* no current HIP device, or it is not gfx950       */
+  VC_ERR_HIP = -7,         /* a HIP launch reported an error                   */
+  VC_ERR_UNSUPPORTED = -8  /* a requested mode is not available                */
+} vc_status;
+
+/* Problem descriptor (passed by pointer, read only during the call). */
+typedef struct vc_jointattn_desc {
+  int32_t batch;          /* B >= 1                                             */
+  int32_t heads;          /* H >= 1                                             */
+  int32_t head_dim;       /* D, 64 or 128                                       */
+  int32_t text_slot;      /* T >= 0: text tokens (padded) placed first          */
+  int32_t frames;         /* F >= 1                                             */
+  int32_t grid_h;         /* Hp >= 1: patch rows per frame                      */
+  int32_t grid_w;         /* Wp >= 1: patch columns per frame                   */
+  float softmax_scale;    /* c; <= 0 selects 1/sqrt(D)                          */
+  int32_t deterministic;  /* backward only: 0 = dQ summed with fp32 atomics
+                             (fast; last bits may vary run to run);
+                             1 = dQ from a separate query-stationary pass
+                             (bitwise reproducible)                             */
+} vc_jointattn_desc;
+
+/* Version of this ABI (VC_JOINTATTN_ABI_VERSION). */
+int vc_jointattn_abi_version(void);
+
+/* Static text for a status code; never NULL. */
+const char* vc_status_string(int status);
+
+/* Joint sequence length N = T + F*Hp*Wp of a descriptor, or a negative
+ * vc_status if the descriptor is invalid. Host only; touches no device. */
+int64_t vc_jointattn_tokens(const vc_jointattn_desc* desc);
+
+/* Forward: o = softmax(c q k^T, masked) v and lse, as defined above.
+ * Reads q, k, v, text_len, key_mask; writes o [B,N,H,D] bf16 and
+ * lse [B,H,N] fp32 (natural log, scale included). Deterministic. */
+vc_status vc_jointattn_fwd(const vc_jointattn_desc* desc,
+                           const void* q, const void* k, const void* v,
+                           const int32_t* text_len, const uint8_t* key_mask,
+                           void* o, float* lse, void* stream);
+
+/* Bytes of device workspace the backward needs for this descriptor: fp32
+ * D = rowsum(dO o O) [B,H,N] and an fp32 dQ accumulator [B,N,H,D]. Returns 0
+ * for an invalid descriptor. Host only. */
+size_t vc_jointattn_bwd_workspace_bytes(const vc_jointattn_desc* desc);
+
+/* Backward: dq, dk, dv (bf16 [B,N,H,D]) from q, k, v, the forward's o and lse,
+ * and the upstream gradient dout. Equivalent to the three stage calls below in
+ * order. `workspace` is caller-owned device memory of at least
+ * vc_jointattn_bwd_workspace_bytes(desc) bytes, 256-byte aligned; its contents
+ * on entry do not matter. Masked keys get dk = dv = 0 exactly. */
+vc_status vc_jointattn_bwd(const vc_jointattn_desc* desc,
+                           const void* q, const void* k, const void* v,
+                           const void* o, const float* lse, const void* dout,
+                           const int32_t* text_len, const uint8_t* key_mask,
+                           void* dq, void* dk, void* dv,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
+/* Backward stage 1: D_i = sum_d dO_id O_id (fp32, into the workspace) and a
+ * zeroed dQ accumulator. Memory-bound; one pass over o and dout. */
+vc_status vc_jointattn_bwd_prepare(const vc_jointattn_desc* desc,
+                                   const void* o, const void* dout,
+                                   void* workspace, size_t workspace_bytes, void* stream);
+
+/* Backward stage 2: recompute P from lse, write dk and dv, and accumulate dQ
+ * into the workspace (fp32 atomics, or the query-stationary pass when
+ * desc->deterministic = 1). Needs stage 1 to have run on the same workspace. */
+vc_status vc_jointattn_bwd_main(const vc_jointattn_desc* desc,
+                                const void* q, const void* k, const void* v,
+                                const float* lse, const void* dout,
+                                const int32_t* text_len, const uint8_t* key_mask,
+                                void* dk, void* dv,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
+/* Backward stage 3: convert the fp32 dQ accumulator to bf16 dq (RNE). */
+vc_status vc_jointattn_bwd_finish(const vc_jointattn_desc* desc, void* dq,
+                                  void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* VC_JOINTATTN_H */

@@ -1,0 +1,253 @@
+"""Joint text-video attention for MI355X (gfx950): Python binding.
+
+Thin ctypes binding over libvc_jointattn.so (include/vc_jointattn.h). It only
+marshals arguments: every step of the computation runs in the library's HIP
+kernels. PyTorch supplies device memory and the stream. If the library is
+not built, every call raises; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+PKG_DIR = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG_DIR, "libvc_jointattn.so")
+HEADER = os.path.join(os.path.dirname(PKG_DIR), "include", "vc_jointattn.h")
+
+VC_OK = 0
+STATUS = {
+    0: "VC_OK", -1: "VC_ERR_NULL", -2: "VC_ERR_SHAPE", -3: "VC_ERR_HEAD_DIM", -4: "VC_ERR_ALIGN",
+    -5: "VC_ERR_WORKSPACE", -6: "VC_ERR_DEVICE", -7: "VC_ERR_HIP", -8: "VC_ERR_UNSUPPORTED",
+}
+
+
+class JointAttnError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        msg = _lib().vc_status_string(status).decode() if _LIB is not None else STATUS.get(status, "?")
+        super().__init__("%s failed: %s (%s)" % (where, STATUS.get(status, status), msg))
+
+
+class vc_jointattn_desc(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int32),
+        ("heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("text_slot", ctypes.c_int32),
+        ("frames", ctypes.c_int32),
+        ("grid_h", ctypes.c_int32),
+        ("grid_w", ctypes.c_int32),
+        ("softmax_scale", ctypes.c_float),
+        ("deterministic", ctypes.c_int32),
+    ]
+
+
+_LIB = None
+_P = ctypes.c_void_p
+_DP = ctypes.POINTER(vc_jointattn_desc)
+_SIGS = {
+    "vc_jointattn_abi_version": (ctypes.c_int, []),
+    "vc_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "vc_jointattn_tokens": (ctypes.c_int64, [_DP]),
+    "vc_jointattn_fwd": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P]),
+    "vc_jointattn_bwd_workspace_bytes": (ctypes.c_size_t, [_DP]),
+    "vc_jointattn_bwd": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "vc_jointattn_bwd_prepare": (ctypes.c_int, [_DP, _P, _P, _P, ctypes.c_size_t, _P]),
+    "vc_jointattn_bwd_main": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "vc_jointattn_bwd_finish": (ctypes.c_int, [_DP, _P, _P, ctypes.c_size_t, _P]),
+}
+
+
+def library_path() -> str:
+    return LIB_PATH
+
+
+def _lib() -> ctypes.CDLL:
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libvc_jointattn.so is not built (%s); run __graft_entry__.build()" % LIB_PATH)
+        lib = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _LIB = lib
+    return _LIB
+
+
+def header_functions() -> list:
+    """Names of the functions include/vc_jointattn.h declares."""
+    with open(HEADER) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\**\s+\**(vc_[a-z_0-9]+)\s*\(", text, re.M)))
+
+
+def make_desc(batch, heads, head_dim, text_slot, frames, grid_h, grid_w, scale=None, deterministic=False):
+    return vc_jointattn_desc(int(batch), int(heads), int(head_dim), int(text_slot), int(frames), int(grid_h),
+                             int(grid_w), float(scale) if scale else 0.0, 1 if deterministic else 0)
+
+
+def desc_for(workload, scale=None, deterministic=False):
+    w = workload
+    return make_desc(w.batch, w.heads, w.head_dim, w.text_slot, w.frames, w.grid_h, w.grid_w, scale, deterministic)
+
+
+# --------------------------------------------------------------------------
+# Raw entry points with the C names (pointers are ints or torch tensors).
+# --------------------------------------------------------------------------
+
+def _ptr(x):
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _call(name, *args):
+    st = getattr(_lib(), name)(*args)
+    if st != VC_OK:
+        raise JointAttnError(st, name)
+
+
+def vc_jointattn_abi_version() -> int:
+    return _lib().vc_jointattn_abi_version()
+
+
+def vc_status_string(status: int) -> str:
+    return _lib().vc_status_string(status).decode()
+
+
+def vc_jointattn_tokens(desc) -> int:
+    return _lib().vc_jointattn_tokens(ctypes.byref(desc))
+
+
+def vc_jointattn_bwd_workspace_bytes(desc) -> int:
+    return _lib().vc_jointattn_bwd_workspace_bytes(ctypes.byref(desc))
+
+
+def vc_jointattn_fwd(desc, q, k, v, text_len, key_mask, o, lse, stream=None):
+    _call("vc_jointattn_fwd", ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(text_len), _ptr(key_mask),
+          _ptr(o), _ptr(lse), _stream(stream))
+
+
+def vc_jointattn_bwd(desc, q, k, v, o, lse, dout, text_len, key_mask, dq, dk, dv, workspace, workspace_bytes,
+                     stream=None):
+    _call("vc_jointattn_bwd", ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _ptr(dout),
+          _ptr(text_len), _ptr(key_mask), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(workspace), int(workspace_bytes),
+          _stream(stream))
+
+
+def vc_jointattn_bwd_prepare(desc, o, dout, workspace, workspace_bytes, stream=None):
+    _call("vc_jointattn_bwd_prepare", ctypes.byref(desc), _ptr(o), _ptr(dout), _ptr(workspace),
+          int(workspace_bytes), _stream(stream))
+
+
+def vc_jointattn_bwd_main(desc, q, k, v, lse, dout, text_len, key_mask, dk, dv, workspace, workspace_bytes,
+                          stream=None):
+    _call("vc_jointattn_bwd_main", ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(lse), _ptr(dout),
+          _ptr(text_len), _ptr(key_mask), _ptr(dk), _ptr(dv), _ptr(workspace), int(workspace_bytes),
+          _stream(stream))
+
+
+def vc_jointattn_bwd_finish(desc, dq, workspace, workspace_bytes, stream=None):
+    _call("vc_jointattn_bwd_finish", ctypes.byref(desc), _ptr(dq), _ptr(workspace), int(workspace_bytes),
+          _stream(stream))
+
+
+# --------------------------------------------------------------------------
+# Tensor-level helpers: allocate outputs with torch, then call the library.
+# --------------------------------------------------------------------------
+
+def _check_tensor(name, t, shape, dtype):
+    import torch
+    if t.device.type != "cuda":
+        raise ValueError("%s must be on a GPU" % name)
+    if t.dtype != dtype:
+        raise ValueError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError("%s has shape %s, expected %s" % (name, tuple(t.shape), tuple(shape)))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    del torch
+
+
+def fwd(q, k, v, desc, text_len=None, key_mask=None, out=None, lse=None):
+    """(o, lse) for bf16 q, k, v of shape [B, N, H, D]."""
+    import torch
+    B, N, H, D = q.shape
+    for n, t in (("q", q), ("k", k), ("v", v)):
+        _check_tensor(n, t, (B, N, H, D), torch.bfloat16)
+    if vc_jointattn_tokens(desc) != N:
+        raise ValueError("descriptor gives N=%d, tensors have N=%d" % (vc_jointattn_tokens(desc), N))
+    if text_len is not None:
+        _check_tensor("text_len", text_len, (B,), torch.int32)
+    if key_mask is not None:
+        _check_tensor("key_mask", key_mask, (B, N), torch.uint8)
+    o = torch.empty_like(q) if out is None else out
+    lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device) if lse is None else lse
+    vc_jointattn_fwd(desc, q, k, v, text_len, key_mask, o, lse)
+    return o, lse
+
+
+def workspace(desc, device):
+    import torch
+    nbytes = vc_jointattn_bwd_workspace_bytes(desc)
+    if nbytes == 0:
+        raise ValueError("invalid descriptor")
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+def bwd(q, k, v, o, lse, dout, desc, text_len=None, key_mask=None, ws=None, dq=None, dk=None, dv=None):
+    """(dq, dk, dv) for bf16 tensors of shape [B, N, H, D]."""
+    import torch
+    B, N, H, D = q.shape
+    for n, t in (("q", q), ("k", k), ("v", v), ("o", o), ("dout", dout)):
+        _check_tensor(n, t, (B, N, H, D), torch.bfloat16)
+    _check_tensor("lse", lse, (B, H, N), torch.float32)
+    ws = workspace(desc, q.device) if ws is None else ws
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(q) if dk is None else dk
+    dv = torch.empty_like(q) if dv is None else dv
+    vc_jointattn_bwd(desc, q, k, v, o, lse, dout, text_len, key_mask, dq, dk, dv, ws, ws.numel())
+    return dq, dk, dv
+
+
+def _autograd_function():
+    import torch
+
+    class JointAttention(torch.autograd.Function):
+        """Autograd wrapper: forward returns O; LSE is kept for backward."""
+
+        @staticmethod
+        def forward(ctx, q, k, v, desc, text_len=None, key_mask=None):
+            o, lse = fwd(q, k, v, desc, text_len, key_mask)
+            ctx.save_for_backward(q, k, v, o, lse)
+            ctx.desc = desc
+            ctx.text_len = text_len
+            ctx.key_mask = key_mask
+            return o
+
+        @staticmethod
+        def backward(ctx, do):
+            q, k, v, o, lse = ctx.saved_tensors
+            dq, dk, dv = bwd(q, k, v, o, lse, do.contiguous(), ctx.desc, ctx.text_len, ctx.key_mask)
+            return dq, dk, dv, None, None, None
+
+    return JointAttention
+
+
+def joint_attention(q, k, v, desc, text_len=None, key_mask=None):
+    """Differentiable joint attention (bf16 in, bf16 out)."""
+    return _autograd_function().apply(q, k, v, desc, text_len, key_mask)

@@ -1,0 +1,80 @@
+"""Helpers for the GPU parity tests: run the HIP path through the C ABI and
+compare with the oracle element by element."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+
+# Bar for bf16 inputs, per output tensor (O, LSE, dQ, dK, dV):
+#   max |gpu - ref| <= 2e-2  and  sum |gpu - ref| / sum |ref| <= 5e-3.
+MAX_ABS = 2e-2
+MEAN_REL = 5e-3
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+# Where the exact result is zero up to rounding (e.g. dQ with a single valid key),
+# the L1 ratio is ill-posed; there the bar is max-abs <= ZERO_ABS instead.
+ZERO_MEAN = 1e-6
+ZERO_ABS = 1e-3
+
+
+def metrics(gpu: np.ndarray, ref: np.ndarray) -> dict:
+    g = np.asarray(gpu, dtype=np.float64)
+    r = np.asarray(ref, dtype=np.float64)
+    assert g.shape == r.shape, (g.shape, r.shape)
+    both_inf = np.isneginf(g) & np.isneginf(r)
+    g = np.where(both_inf, 0.0, g)
+    r = np.where(both_inf, 0.0, r)
+    d = np.abs(g - r)
+    denom = np.abs(r).sum()
+    return {
+        "max_abs": float(d.max()) if d.size else 0.0,
+        "mean_rel": float(d.sum() / denom) if denom > 0 else float(d.sum()),
+        "norm_max": float(d.max() / max(np.abs(r).max(), 1e-30)) if d.size else 0.0,
+        "finite": bool(np.isfinite(g).all()),
+        "degenerate": bool(d.size and np.abs(r).mean() < ZERO_MEAN),
+    }
+
+
+def assert_close(name: str, gpu, ref, max_abs=MAX_ABS, mean_rel=MEAN_REL):
+    m = metrics(gpu, ref)
+    log("   %-4s max_abs=%.3e mean_rel=%.3e norm_max=%.3e" % (name, m["max_abs"], m["mean_rel"], m["norm_max"]))
+    assert m["finite"], "%s has non-finite values" % name
+    if m["degenerate"]:
+        assert m["max_abs"] <= ZERO_ABS, "%s (exactly zero reference) max_abs %.3e" % (name, m["max_abs"])
+        return m
+    assert m["max_abs"] <= max_abs, "%s max_abs %.3e > %.1e" % (name, m["max_abs"], max_abs)
+    assert m["mean_rel"] <= mean_rel, "%s mean_rel %.3e > %.1e" % (name, m["mean_rel"], mean_rel)
+    return m
+
+
+def to_gpu_bf16(x: np.ndarray):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(x)).to("cuda").to(torch.bfloat16).contiguous()
+
+
+def bf16_values(t) -> np.ndarray:
+    """The exact values a bf16 tensor holds, widened to float64 on the host."""
+    import torch
+    return t.to(torch.float64).cpu().numpy()
+
+
+def run_gpu(desc, q, k, v, do, text_len=None, key_mask=None, host=True):
+    """fwd + bwd through the C ABI. Returns host float64 arrays (host=True) or
+    the device tensors themselves."""
+    import torch
+    import paper_2501_08453_amd as vc
+    o, lse = vc.fwd(q, k, v, desc, text_len, key_mask)
+    dq, dk, dv = vc.bwd(q, k, v, o, lse, do, desc, text_len, key_mask)
+    torch.cuda.synchronize()
+    dev = {"o": o, "lse": lse, "dq": dq, "dk": dk, "dv": dv}
+    if not host:
+        return dev
+    out = {n: bf16_values(t) for n, t in dev.items() if n != "lse"}
+    out["lse"] = lse.cpu().numpy().astype(np.float64)
+    return out

@@ -1,0 +1,107 @@
+"""Host-side checks of the C ABI: the library loads, exports what the header
+declares, and reports argument errors before touching a device.
+
+No call here reaches a kernel launch: every call fails validation first (the
+device-error case runs only where no GPU is present).
+"""
+import ctypes
+
+import pytest
+
+import paper_2501_08453_amd as vc
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return vc._lib()
+
+
+def good_desc(**kw):
+    d = dict(batch=1, heads=2, head_dim=64, text_slot=16, frames=2, grid_h=8, grid_w=8)
+    d.update(kw)
+    return vc.make_desc(**d)
+
+
+def test_exports_every_declared_function(lib):
+    names = vc.header_functions()
+    assert set(names) >= {"vc_jointattn_fwd", "vc_jointattn_bwd", "vc_jointattn_bwd_workspace_bytes",
+                          "vc_status_string", "vc_jointattn_abi_version"}
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(vc._SIGS) == set(names)
+
+
+def test_version_and_strings(lib):
+    assert vc.vc_jointattn_abi_version() == 1
+    for code in vc.STATUS:
+        assert isinstance(vc.vc_status_string(code), str) and vc.vc_status_string(code)
+    assert vc.vc_status_string(12345) == "unknown status"
+
+
+def test_tokens_and_workspace():
+    d = good_desc()
+    assert vc.vc_jointattn_tokens(d) == 16 + 2 * 8 * 8
+    d3 = vc.make_desc(1, 24, 128, 256, 16, 45, 80)
+    n = 57856
+    assert vc.vc_jointattn_tokens(d3) == n
+    dd = 24 * n * 4
+    assert vc.vc_jointattn_bwd_workspace_bytes(d3) == ((dd + 255) // 256) * 256 + n * 24 * 128 * 4
+    assert vc.vc_jointattn_tokens(good_desc(head_dim=96)) == -3
+    assert vc.vc_jointattn_bwd_workspace_bytes(good_desc(frames=0)) == 0
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(head_dim=96), -3), (dict(head_dim=0), -3), (dict(batch=0), -2), (dict(heads=0), -2),
+    (dict(text_slot=-1), -2), (dict(frames=0), -2), (dict(grid_h=-3), -2), (dict(grid_w=0), -2),
+    (dict(frames=1 << 20, grid_h=1 << 10, grid_w=4), -2),
+])
+def test_bad_descriptor(lib, kw, code):
+    d = good_desc(**kw)
+    p = 1 << 20  # never dereferenced: validation fails first
+    assert lib.vc_jointattn_fwd(ctypes.byref(d), p, p, p, None, None, p, p, None) == code
+    assert lib.vc_jointattn_bwd(ctypes.byref(d), p, p, p, p, p, p, None, None, p, p, p, p, 1 << 30, None) == code
+
+
+def test_null_descriptor_and_pointers(lib):
+    p = 1 << 20
+    assert lib.vc_jointattn_fwd(None, p, p, p, None, None, p, p, None) == -1
+    d = good_desc()
+    assert lib.vc_jointattn_fwd(ctypes.byref(d), None, p, p, None, None, p, p, None) == -1
+    assert lib.vc_jointattn_fwd(ctypes.byref(d), p, p, p, None, None, p, None, None) == -1
+    assert lib.vc_jointattn_bwd(ctypes.byref(d), p, p, p, p, p, None, None, None, p, p, p, p, 1 << 30, None) == -1
+    assert lib.vc_jointattn_bwd_main(ctypes.byref(d), p, p, None, p, p, None, None, p, p, p, 1 << 30, None) == -1
+
+
+def test_misaligned_pointers(lib):
+    d = good_desc()
+    p = 1 << 20
+    assert lib.vc_jointattn_fwd(ctypes.byref(d), p + 2, p, p, None, None, p, p, None) == -4
+    assert lib.vc_jointattn_fwd(ctypes.byref(d), p, p, p, p + 2, None, p, p, None) == -4  # text_len int32
+    assert lib.vc_jointattn_bwd_prepare(ctypes.byref(d), p, p, p + 16, 1 << 30, None) == -4  # workspace 256
+    assert lib.vc_jointattn_bwd_finish(ctypes.byref(d), p + 8, p, 1 << 30, None) == -4
+
+
+def test_workspace_checks(lib):
+    d = good_desc()
+    p = 1 << 20
+    need = vc.vc_jointattn_bwd_workspace_bytes(d)
+    assert lib.vc_jointattn_bwd_prepare(ctypes.byref(d), p, p, None, need, None) == -5
+    assert lib.vc_jointattn_bwd_prepare(ctypes.byref(d), p, p, p, need - 1, None) == -5
+    assert lib.vc_jointattn_bwd(ctypes.byref(d), p, p, p, p, p, p, None, None, p, p, p, p, need - 4, None) == -5
+
+
+def test_no_device_is_reported():
+    torch = pytest.importorskip("torch")
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present; this case checks the error path without one")
+    lib = vc._lib()
+    d = good_desc()
+    p = 1 << 20
+    assert lib.vc_jointattn_fwd(ctypes.byref(d), p, p, p, None, None, p, p, None) == -6
+
+
+def test_binding_fails_loudly_without_library(monkeypatch):
+    monkeypatch.setattr(vc, "_LIB", None)
+    monkeypatch.setattr(vc, "LIB_PATH", "/nonexistent/libvc_jointattn.so")
+    with pytest.raises(RuntimeError, match="not built"):
+        vc.vc_jointattn_abi_version()
