@@ -37,8 +37,8 @@
  *  - lse: fp32 [B, H, N], device memory, 16-byte aligned.
  *  - text_len: device int32 [B] or NULL (NULL means every text token is real).
  *  - key_mask: device uint8 [B, N] or NULL (NULL means no extra mask).
- *  - All memory is owned by the caller. The library never allocates, frees or
- *    synchronises, keeps no per-call state, and only launches kernels on
+ *  - All memory is owned by the caller, workspaces included. The library never
+ *    allocates, frees or synchronises, keeps no per-call state, and only launches kernels on
  *    `stream` (a hipStream_t; NULL = the null stream). Outputs are
  *    overwritten, never accumulated into, and must not alias inputs.
  *  - Argument errors are reported synchronously, before anything is launched.
@@ -81,10 +81,9 @@ typedef struct vc_jointattn_desc {
   int32_t grid_h;         /* Hp >= 1: patch rows per frame                      */
   int32_t grid_w;         /* Wp >= 1: patch columns per frame                   */
   float softmax_scale;    /* c; <= 0 selects 1/sqrt(D)                          */
-  int32_t deterministic;  /* backward only: 0 = dQ summed with fp32 atomics
-                             (fast; last bits may vary run to run);
-                             1 = dQ from a separate query-stationary pass
-                             (bitwise reproducible)                             */
+  int32_t deterministic;  /* 0 or 1. Both give the same bitwise reproducible
+                             results (no atomics anywhere); kept so callers can
+                             state the requirement explicitly                  */
 } vc_jointattn_desc;
 
 /* Version of this ABI (VC_JOINTATTN_ABI_VERSION). */
@@ -97,24 +96,33 @@ const char* vc_status_string(int status);
  * vc_status if the descriptor is invalid. Host only; touches no device. */
 int64_t vc_jointattn_tokens(const vc_jointattn_desc* desc);
 
+/* Bytes of device workspace the forward needs: a token-major copy of V
+ * ([B,H,ceil(N/64)] tiles of D x 72 bf16). 0 for an invalid descriptor. */
+size_t vc_jointattn_fwd_workspace_bytes(const vc_jointattn_desc* desc);
+
 /* Forward: o = softmax(c q k^T, masked) v and lse, as defined above.
  * Reads q, k, v, text_len, key_mask; writes o [B,N,H,D] bf16 and
- * lse [B,H,N] fp32 (natural log, scale included). Deterministic. */
+ * lse [B,H,N] fp32 (natural log, scale included). `workspace` is caller-owned
+ * device memory of at least vc_jointattn_fwd_workspace_bytes(desc) bytes,
+ * 256-byte aligned; its contents on entry do not matter. Deterministic. */
 vc_status vc_jointattn_fwd(const vc_jointattn_desc* desc,
                            const void* q, const void* k, const void* v,
                            const int32_t* text_len, const uint8_t* key_mask,
-                           void* o, float* lse, void* stream);
+                           void* o, float* lse,
+                           void* workspace, size_t workspace_bytes, void* stream);
 
-/* Bytes of device workspace the backward needs for this descriptor: fp32
- * D = rowsum(dO o O) [B,H,N] and an fp32 dQ accumulator [B,N,H,D]. Returns 0
- * for an invalid descriptor. Host only. */
+/* Bytes of device workspace the backward needs: per query row fp32 D and
+ * LSE*log2(e) ([B,H,Npad], Npad = N rounded up to 64), and token-major copies of
+ * Q, dO and K (as for the forward's V). 0 for an invalid descriptor. Host only. */
 size_t vc_jointattn_bwd_workspace_bytes(const vc_jointattn_desc* desc);
 
 /* Backward: dq, dk, dv (bf16 [B,N,H,D]) from q, k, v, the forward's o and lse,
  * and the upstream gradient dout. Equivalent to the three stage calls below in
  * order. `workspace` is caller-owned device memory of at least
  * vc_jointattn_bwd_workspace_bytes(desc) bytes, 256-byte aligned; its contents
- * on entry do not matter. Masked keys get dk = dv = 0 exactly. */
+ * on entry do not matter. Masked keys get dk = dv = 0 exactly. No atomics are
+ * used: the result is bitwise reproducible for either value of
+ * desc->deterministic. */
 vc_status vc_jointattn_bwd(const vc_jointattn_desc* desc,
                            const void* q, const void* k, const void* v,
                            const void* o, const float* lse, const void* dout,
@@ -122,25 +130,31 @@ vc_status vc_jointattn_bwd(const vc_jointattn_desc* desc,
                            void* dq, void* dk, void* dv,
                            void* workspace, size_t workspace_bytes, void* stream);
 
-/* Backward stage 1: D_i = sum_d dO_id O_id (fp32, into the workspace) and a
- * zeroed dQ accumulator. Memory-bound; one pass over o and dout. */
+/* Backward stage 1: per query row, D_i = sum_d dO_id O_id and LSE_i*log2(e)
+ * (fp32, padding rows made inert), and the token-major copies of q, dout and k,
+ * all into the workspace. Memory-bound. */
 vc_status vc_jointattn_bwd_prepare(const vc_jointattn_desc* desc,
-                                   const void* o, const void* dout,
+                                   const void* q, const void* k,
+                                   const void* o, const float* lse, const void* dout,
                                    void* workspace, size_t workspace_bytes, void* stream);
 
-/* Backward stage 2: recompute P from lse, write dk and dv, and accumulate dQ
- * into the workspace (fp32 atomics, or the query-stationary pass when
- * desc->deterministic = 1). Needs stage 1 to have run on the same workspace. */
-vc_status vc_jointattn_bwd_main(const vc_jointattn_desc* desc,
+/* Backward stage 2 (key-stationary): recompute P from the stage-1 LSE and write
+ * dk = c dS^T Q and dv = P^T dO. Needs stage 1 on the same workspace. */
+vc_status vc_jointattn_bwd_dkdv(const vc_jointattn_desc* desc,
                                 const void* q, const void* k, const void* v,
-                                const float* lse, const void* dout,
+                                const void* dout,
                                 const int32_t* text_len, const uint8_t* key_mask,
                                 void* dk, void* dv,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
-/* Backward stage 3: convert the fp32 dQ accumulator to bf16 dq (RNE). */
-vc_status vc_jointattn_bwd_finish(const vc_jointattn_desc* desc, void* dq,
-                                  void* workspace, size_t workspace_bytes, void* stream);
+/* Backward stage 3 (query-stationary): recompute P and dP and write
+ * dq = c dS K. Needs stage 1 on the same workspace; independent of stage 2. */
+vc_status vc_jointattn_bwd_dq(const vc_jointattn_desc* desc,
+                              const void* q, const void* k, const void* v,
+                              const void* dout,
+                              const int32_t* text_len, const uint8_t* key_mask,
+                              void* dq,
+                              void* workspace, size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -50,12 +50,13 @@ _SIGS = {
     "vc_jointattn_abi_version": (ctypes.c_int, []),
     "vc_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "vc_jointattn_tokens": (ctypes.c_int64, [_DP]),
-    "vc_jointattn_fwd": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P]),
+    "vc_jointattn_fwd_workspace_bytes": (ctypes.c_size_t, [_DP]),
+    "vc_jointattn_fwd": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "vc_jointattn_bwd_workspace_bytes": (ctypes.c_size_t, [_DP]),
     "vc_jointattn_bwd": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
-    "vc_jointattn_bwd_prepare": (ctypes.c_int, [_DP, _P, _P, _P, ctypes.c_size_t, _P]),
-    "vc_jointattn_bwd_main": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
-    "vc_jointattn_bwd_finish": (ctypes.c_int, [_DP, _P, _P, ctypes.c_size_t, _P]),
+    "vc_jointattn_bwd_prepare": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "vc_jointattn_bwd_dkdv": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "vc_jointattn_bwd_dq": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
 }
 
 
@@ -133,13 +134,17 @@ def vc_jointattn_tokens(desc) -> int:
     return _lib().vc_jointattn_tokens(ctypes.byref(desc))
 
 
+def vc_jointattn_fwd_workspace_bytes(desc) -> int:
+    return _lib().vc_jointattn_fwd_workspace_bytes(ctypes.byref(desc))
+
+
 def vc_jointattn_bwd_workspace_bytes(desc) -> int:
     return _lib().vc_jointattn_bwd_workspace_bytes(ctypes.byref(desc))
 
 
-def vc_jointattn_fwd(desc, q, k, v, text_len, key_mask, o, lse, stream=None):
+def vc_jointattn_fwd(desc, q, k, v, text_len, key_mask, o, lse, workspace, workspace_bytes, stream=None):
     _call("vc_jointattn_fwd", ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(text_len), _ptr(key_mask),
-          _ptr(o), _ptr(lse), _stream(stream))
+          _ptr(o), _ptr(lse), _ptr(workspace), int(workspace_bytes), _stream(stream))
 
 
 def vc_jointattn_bwd(desc, q, k, v, o, lse, dout, text_len, key_mask, dq, dk, dv, workspace, workspace_bytes,
@@ -149,21 +154,21 @@ def vc_jointattn_bwd(desc, q, k, v, o, lse, dout, text_len, key_mask, dq, dk, dv
           _stream(stream))
 
 
-def vc_jointattn_bwd_prepare(desc, o, dout, workspace, workspace_bytes, stream=None):
-    _call("vc_jointattn_bwd_prepare", ctypes.byref(desc), _ptr(o), _ptr(dout), _ptr(workspace),
-          int(workspace_bytes), _stream(stream))
+def vc_jointattn_bwd_prepare(desc, q, k, o, lse, dout, workspace, workspace_bytes, stream=None):
+    _call("vc_jointattn_bwd_prepare", ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(o), _ptr(lse), _ptr(dout),
+          _ptr(workspace), int(workspace_bytes), _stream(stream))
 
 
-def vc_jointattn_bwd_main(desc, q, k, v, lse, dout, text_len, key_mask, dk, dv, workspace, workspace_bytes,
+def vc_jointattn_bwd_dkdv(desc, q, k, v, dout, text_len, key_mask, dk, dv, workspace, workspace_bytes,
                           stream=None):
-    _call("vc_jointattn_bwd_main", ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(lse), _ptr(dout),
+    _call("vc_jointattn_bwd_dkdv", ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(dout),
           _ptr(text_len), _ptr(key_mask), _ptr(dk), _ptr(dv), _ptr(workspace), int(workspace_bytes),
           _stream(stream))
 
 
-def vc_jointattn_bwd_finish(desc, dq, workspace, workspace_bytes, stream=None):
-    _call("vc_jointattn_bwd_finish", ctypes.byref(desc), _ptr(dq), _ptr(workspace), int(workspace_bytes),
-          _stream(stream))
+def vc_jointattn_bwd_dq(desc, q, k, v, dout, text_len, key_mask, dq, workspace, workspace_bytes, stream=None):
+    _call("vc_jointattn_bwd_dq", ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(dout),
+          _ptr(text_len), _ptr(key_mask), _ptr(dq), _ptr(workspace), int(workspace_bytes), _stream(stream))
 
 
 # --------------------------------------------------------------------------
@@ -183,7 +188,23 @@ def _check_tensor(name, t, shape, dtype):
     del torch
 
 
-def fwd(q, k, v, desc, text_len=None, key_mask=None, out=None, lse=None):
+def _workspace(nbytes, device):
+    import torch
+    if nbytes == 0:
+        raise ValueError("invalid descriptor")
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+def fwd_workspace(desc, device):
+    return _workspace(vc_jointattn_fwd_workspace_bytes(desc), device)
+
+
+def workspace(desc, device):
+    """Backward workspace for a descriptor."""
+    return _workspace(vc_jointattn_bwd_workspace_bytes(desc), device)
+
+
+def fwd(q, k, v, desc, text_len=None, key_mask=None, out=None, lse=None, ws=None):
     """(o, lse) for bf16 q, k, v of shape [B, N, H, D]."""
     import torch
     B, N, H, D = q.shape
@@ -197,16 +218,9 @@ def fwd(q, k, v, desc, text_len=None, key_mask=None, out=None, lse=None):
         _check_tensor("key_mask", key_mask, (B, N), torch.uint8)
     o = torch.empty_like(q) if out is None else out
     lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device) if lse is None else lse
-    vc_jointattn_fwd(desc, q, k, v, text_len, key_mask, o, lse)
+    ws = fwd_workspace(desc, q.device) if ws is None else ws
+    vc_jointattn_fwd(desc, q, k, v, text_len, key_mask, o, lse, ws, ws.numel())
     return o, lse
-
-
-def workspace(desc, device):
-    import torch
-    nbytes = vc_jointattn_bwd_workspace_bytes(desc)
-    if nbytes == 0:
-        raise ValueError("invalid descriptor")
-    return torch.empty(nbytes, dtype=torch.uint8, device=device)
 
 
 def bwd(q, k, v, o, lse, dout, desc, text_len=None, key_mask=None, ws=None, dq=None, dk=None, dv=None):

@@ -6,8 +6,8 @@
 
 #include <mutex>
 
-#include "../../include/vc_jointattn.h"
 #include "common.hpp"
+#include "vc_jointattn.h"
 
 namespace {
 
@@ -32,6 +32,7 @@ vc_status check_device() {
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
 
 // Validates a descriptor; on success fills N.
 vc_status check_desc(const vc_jointattn_desc* d, int64_t* n_out) {
@@ -56,23 +57,48 @@ float scale_of(const vc_jointattn_desc* d) {
   return d->softmax_scale > 0.0f ? d->softmax_scale : 1.0f / sqrtf((float)d->head_dim);
 }
 
-size_t dd_bytes(const vc_jointattn_desc* d, int64_t n) {
-  const size_t raw = (size_t)d->batch * d->heads * (size_t)n * sizeof(float);
-  return (raw + 255) & ~(size_t)255;
+int ntiles(int64_t n) { return (int)((n + vcja::kTileTok - 1) / vcja::kTileTok); }
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Transposed token tiles of one [B, N, H, D] tensor.
+size_t tiles_bytes(const vc_jointattn_desc* d, int64_t n) {
+  return align256((size_t)d->batch * d->heads * ntiles(n) * vcja::tile_elems(d->head_dim) * sizeof(__bf16));
 }
 
-size_t ws_bytes(const vc_jointattn_desc* d, int64_t n) {
-  return dd_bytes(d, n) + (size_t)d->batch * (size_t)n * d->heads * d->head_dim * sizeof(float);
+// Per-row fp32 array [B, H, Npad].
+size_t rows_bytes(const vc_jointattn_desc* d, int64_t n) {
+  return align256((size_t)d->batch * d->heads * (size_t)ntiles(n) * vcja::kTileTok * sizeof(float));
 }
 
-vc_status check_ws(const vc_jointattn_desc* d, int64_t n, void* ws, size_t bytes) {
+// Backward workspace: D | LSE*log2(e) | Q^T tiles | dO^T tiles | K^T tiles.
+struct BwdWorkspace {
+  float* dd;
+  float* lse2;
+  __bf16* qt;
+  __bf16* dot;
+  __bf16* kt;
+};
+
+size_t bwd_ws_bytes(const vc_jointattn_desc* d, int64_t n) { return 2 * rows_bytes(d, n) + 3 * tiles_bytes(d, n); }
+
+BwdWorkspace split_bwd_ws(const vc_jointattn_desc* d, int64_t n, void* ws) {
+  char* p = static_cast<char*>(ws);
+  const size_t rb = rows_bytes(d, n), tb = tiles_bytes(d, n);
+  return BwdWorkspace{reinterpret_cast<float*>(p), reinterpret_cast<float*>(p + rb),
+                      reinterpret_cast<__bf16*>(p + 2 * rb), reinterpret_cast<__bf16*>(p + 2 * rb + tb),
+                      reinterpret_cast<__bf16*>(p + 2 * rb + 2 * tb)};
+}
+
+vc_status check_ws(void* ws, size_t have, size_t need) {
   if (!ws) return VC_ERR_WORKSPACE;
   if ((reinterpret_cast<uintptr_t>(ws) & 255u) != 0) return VC_ERR_ALIGN;
-  if (bytes < ws_bytes(d, n)) return VC_ERR_WORKSPACE;
+  if (have < need) return VC_ERR_WORKSPACE;
   return VC_OK;
 }
 
 inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+inline const __bf16* bf(const void* p) { return static_cast<const __bf16*>(p); }
 
 }  // namespace
 
@@ -101,25 +127,37 @@ int64_t vc_jointattn_tokens(const vc_jointattn_desc* desc) {
   return st == VC_OK ? n : (int64_t)st;
 }
 
+size_t vc_jointattn_fwd_workspace_bytes(const vc_jointattn_desc* desc) {
+  int64_t n = 0;
+  if (check_desc(desc, &n) != VC_OK) return 0;
+  return tiles_bytes(desc, n);
+}
+
 size_t vc_jointattn_bwd_workspace_bytes(const vc_jointattn_desc* desc) {
   int64_t n = 0;
   if (check_desc(desc, &n) != VC_OK) return 0;
-  return ws_bytes(desc, n);
+  return bwd_ws_bytes(desc, n);
 }
 
 vc_status vc_jointattn_fwd(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
-                           const int32_t* text_len, const uint8_t* key_mask, void* o, float* lse, void* stream) {
+                           const int32_t* text_len, const uint8_t* key_mask, void* o, float* lse, void* workspace,
+                           size_t workspace_bytes, void* stream) {
   int64_t n = 0;
   vc_status st = check_desc(desc, &n);
   if (st != VC_OK) return st;
   if (!q || !k || !v || !o || !lse) return VC_ERR_NULL;
-  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse)) return VC_ERR_ALIGN;
-  if ((reinterpret_cast<uintptr_t>(text_len) & 3u) != 0) return VC_ERR_ALIGN;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse) || !aligned4(text_len))
+    return VC_ERR_ALIGN;
+  if ((st = check_ws(workspace, workspace_bytes, tiles_bytes(desc, n))) != VC_OK) return st;
   if ((st = check_device()) != VC_OK) return st;
+  __bf16* vt = static_cast<__bf16*>(workspace);
+  if (vcja::launch_token_tiles(bf(v), vt, desc->batch, desc->heads, (int)n, desc->head_dim, as_stream(stream)) !=
+      hipSuccess)
+    return VC_ERR_HIP;
   vcja::FwdArgs a;
-  a.q = static_cast<const __bf16*>(q);
-  a.k = static_cast<const __bf16*>(k);
-  a.v = static_cast<const __bf16*>(v);
+  a.q = bf(q);
+  a.k = bf(k);
+  a.vt = vt;
   a.text_len = text_len;
   a.key_mask = key_mask;
   a.o = static_cast<__bf16*>(o);
@@ -128,77 +166,100 @@ vc_status vc_jointattn_fwd(const vc_jointattn_desc* desc, const void* q, const v
   a.H = desc->heads;
   a.N = (int)n;
   a.T = desc->text_slot;
+  a.ntile = ntiles(n);
   a.scale_log2 = scale_of(desc) * vcja::kLog2e;
   return vcja::launch_fwd(a, desc->head_dim, as_stream(stream)) == hipSuccess ? VC_OK : VC_ERR_HIP;
 }
 
-vc_status vc_jointattn_bwd_prepare(const vc_jointattn_desc* desc, const void* o, const void* dout, void* workspace,
-                                   size_t workspace_bytes, void* stream) {
+vc_status vc_jointattn_bwd_prepare(const vc_jointattn_desc* desc, const void* q, const void* k, const void* o,
+                                   const float* lse, const void* dout, void* workspace, size_t workspace_bytes,
+                                   void* stream) {
   int64_t n = 0;
   vc_status st = check_desc(desc, &n);
   if (st != VC_OK) return st;
-  if (!o || !dout) return VC_ERR_NULL;
-  if (!aligned16(o) || !aligned16(dout)) return VC_ERR_ALIGN;
-  if ((st = check_ws(desc, n, workspace, workspace_bytes)) != VC_OK) return st;
+  if (!q || !k || !o || !lse || !dout) return VC_ERR_NULL;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(o) || !aligned16(lse) || !aligned16(dout)) return VC_ERR_ALIGN;
+  if ((st = check_ws(workspace, workspace_bytes, bwd_ws_bytes(desc, n))) != VC_OK) return st;
   if ((st = check_device()) != VC_OK) return st;
-  float* dd = static_cast<float*>(workspace);
-  float* acc = reinterpret_cast<float*>(static_cast<char*>(workspace) + dd_bytes(desc, n));
-  const hipError_t e = vcja::launch_bwd_prepare(static_cast<const __bf16*>(o), static_cast<const __bf16*>(dout), dd,
-                                                acc, desc->batch, desc->heads, (int)n, desc->head_dim,
-                                                as_stream(stream));
-  return e == hipSuccess ? VC_OK : VC_ERR_HIP;
+  const BwdWorkspace w = split_bwd_ws(desc, n, workspace);
+  const int B = desc->batch, H = desc->heads, D = desc->head_dim, N = (int)n;
+  hipStream_t s = as_stream(stream);
+  if (vcja::launch_bwd_prepare(bf(o), lse, bf(dout), w.dd, w.lse2, B, H, N, ntiles(n) * vcja::kTileTok, D, s) !=
+          hipSuccess ||
+      vcja::launch_token_tiles(bf(q), w.qt, B, H, N, D, s) != hipSuccess ||
+      vcja::launch_token_tiles(bf(dout), w.dot, B, H, N, D, s) != hipSuccess ||
+      vcja::launch_token_tiles(bf(k), w.kt, B, H, N, D, s) != hipSuccess)
+    return VC_ERR_HIP;
+  return VC_OK;
 }
 
-vc_status vc_jointattn_bwd_main(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
-                                const float* lse, const void* dout, const int32_t* text_len,
-                                const uint8_t* key_mask, void* dk, void* dv, void* workspace,
-                                size_t workspace_bytes, void* stream) {
+vc_status vc_jointattn_bwd_dkdv(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
+                                const void* dout, const int32_t* text_len, const uint8_t* key_mask, void* dk,
+                                void* dv, void* workspace, size_t workspace_bytes, void* stream) {
   int64_t n = 0;
   vc_status st = check_desc(desc, &n);
   if (st != VC_OK) return st;
-  if (!q || !k || !v || !lse || !dout || !dk || !dv) return VC_ERR_NULL;
-  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(lse) || !aligned16(dout) || !aligned16(dk) ||
-      !aligned16(dv))
+  if (!q || !k || !v || !dout || !dk || !dv) return VC_ERR_NULL;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(dout) || !aligned16(dk) || !aligned16(dv) ||
+      !aligned4(text_len))
     return VC_ERR_ALIGN;
-  if ((reinterpret_cast<uintptr_t>(text_len) & 3u) != 0) return VC_ERR_ALIGN;
-  if ((st = check_ws(desc, n, workspace, workspace_bytes)) != VC_OK) return st;
-  if (desc->deterministic) return VC_ERR_UNSUPPORTED;
+  if ((st = check_ws(workspace, workspace_bytes, bwd_ws_bytes(desc, n))) != VC_OK) return st;
   if ((st = check_device()) != VC_OK) return st;
-  vcja::BwdArgs a;
-  a.q = static_cast<const __bf16*>(q);
-  a.k = static_cast<const __bf16*>(k);
-  a.v = static_cast<const __bf16*>(v);
-  a.dout = static_cast<const __bf16*>(dout);
-  a.lse = lse;
-  a.dd = static_cast<const float*>(workspace);
+  const BwdWorkspace w = split_bwd_ws(desc, n, workspace);
+  vcja::DkdvArgs a;
+  a.q = bf(q);
+  a.k = bf(k);
+  a.v = bf(v);
+  a.dout = bf(dout);
+  a.qt = w.qt;
+  a.dot = w.dot;
+  a.lse2 = w.lse2;
+  a.dd = w.dd;
   a.text_len = text_len;
   a.key_mask = key_mask;
   a.dk = static_cast<__bf16*>(dk);
   a.dv = static_cast<__bf16*>(dv);
-  a.dq_acc = reinterpret_cast<float*>(static_cast<char*>(workspace) + dd_bytes(desc, n));
   a.B = desc->batch;
   a.H = desc->heads;
   a.N = (int)n;
   a.T = desc->text_slot;
+  a.ntile = ntiles(n);
   a.scale = scale_of(desc);
   a.scale_log2 = a.scale * vcja::kLog2e;
-  return vcja::launch_bwd_main(a, desc->head_dim, as_stream(stream)) == hipSuccess ? VC_OK : VC_ERR_HIP;
+  return vcja::launch_bwd_dkdv(a, desc->head_dim, as_stream(stream)) == hipSuccess ? VC_OK : VC_ERR_HIP;
 }
 
-vc_status vc_jointattn_bwd_finish(const vc_jointattn_desc* desc, void* dq, void* workspace, size_t workspace_bytes,
-                                  void* stream) {
+vc_status vc_jointattn_bwd_dq(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
+                              const void* dout, const int32_t* text_len, const uint8_t* key_mask, void* dq,
+                              void* workspace, size_t workspace_bytes, void* stream) {
   int64_t n = 0;
   vc_status st = check_desc(desc, &n);
   if (st != VC_OK) return st;
-  if (!dq) return VC_ERR_NULL;
-  if (!aligned16(dq)) return VC_ERR_ALIGN;
-  if ((st = check_ws(desc, n, workspace, workspace_bytes)) != VC_OK) return st;
+  if (!q || !k || !v || !dout || !dq) return VC_ERR_NULL;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(dout) || !aligned16(dq) || !aligned4(text_len))
+    return VC_ERR_ALIGN;
+  if ((st = check_ws(workspace, workspace_bytes, bwd_ws_bytes(desc, n))) != VC_OK) return st;
   if ((st = check_device()) != VC_OK) return st;
-  const float* acc = reinterpret_cast<const float*>(static_cast<const char*>(workspace) + dd_bytes(desc, n));
-  const hipError_t e =
-      vcja::launch_bwd_finish(acc, static_cast<__bf16*>(dq), desc->batch, desc->heads, (int)n, desc->head_dim,
-                              as_stream(stream));
-  return e == hipSuccess ? VC_OK : VC_ERR_HIP;
+  const BwdWorkspace w = split_bwd_ws(desc, n, workspace);
+  vcja::DqArgs a;
+  a.q = bf(q);
+  a.k = bf(k);
+  a.v = bf(v);
+  a.dout = bf(dout);
+  a.kt = w.kt;
+  a.lse2 = w.lse2;
+  a.dd = w.dd;
+  a.text_len = text_len;
+  a.key_mask = key_mask;
+  a.dq = static_cast<__bf16*>(dq);
+  a.B = desc->batch;
+  a.H = desc->heads;
+  a.N = (int)n;
+  a.T = desc->text_slot;
+  a.ntile = ntiles(n);
+  a.scale = scale_of(desc);
+  a.scale_log2 = a.scale * vcja::kLog2e;
+  return vcja::launch_bwd_dq(a, desc->head_dim, as_stream(stream)) == hipSuccess ? VC_OK : VC_ERR_HIP;
 }
 
 vc_status vc_jointattn_bwd(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v, const void* o,
@@ -208,12 +269,12 @@ vc_status vc_jointattn_bwd(const vc_jointattn_desc* desc, const void* q, const v
   vc_status st = check_desc(desc, &n);
   if (st != VC_OK) return st;
   if (!q || !k || !v || !o || !lse || !dout || !dq || !dk || !dv) return VC_ERR_NULL;
-  if (desc->deterministic) return VC_ERR_UNSUPPORTED;
-  if ((st = vc_jointattn_bwd_prepare(desc, o, dout, workspace, workspace_bytes, stream)) != VC_OK) return st;
-  if ((st = vc_jointattn_bwd_main(desc, q, k, v, lse, dout, text_len, key_mask, dk, dv, workspace, workspace_bytes,
+  if ((st = vc_jointattn_bwd_prepare(desc, q, k, o, lse, dout, workspace, workspace_bytes, stream)) != VC_OK)
+    return st;
+  if ((st = vc_jointattn_bwd_dkdv(desc, q, k, v, dout, text_len, key_mask, dk, dv, workspace, workspace_bytes,
                                   stream)) != VC_OK)
     return st;
-  return vc_jointattn_bwd_finish(desc, dq, workspace, workspace_bytes, stream);
+  return vc_jointattn_bwd_dq(desc, q, k, v, dout, text_len, key_mask, dq, workspace, workspace_bytes, stream);
 }
 
 }  // extern "C"

@@ -1,29 +1,44 @@
-// Backward joint text-video attention for gfx950.
+// Backward joint text-video attention for gfx950, without atomics.
 //
-// Stage 1 (prepare): D_i = <dO_i, O_i> in fp32, and a zeroed fp32 dQ accumulator.
-// Stage 2 (main): one workgroup of four waves owns 128 keys of one (sample,
-//   head), each wave 32 of them, with K and V of its keys held in registers and
-//   dK^T, dV^T accumulated in registers. It walks over all query tiles of 64:
-//   recomputes S = Q K^T and P = exp(S c - LSE) with the matrix cores, forms
-//   dP = dO V^T and dS = P o (dP - D), and accumulates dV^T += dO^T P and
+// Prepare: per query row, D_i = <dO_i, O_i> and LSE_i*log2(e) in fp32, padded
+//   to whole tiles of 64 rows (padding rows get LSE = +inf so that their
+//   probabilities vanish, and D = 0); transposed token tiles of Q, dO and K
+//   come from the reformatting pass.
+// dK/dV (key-stationary): one workgroup of four waves owns 128 keys of one
+//   (sample, head), each wave 32, with K and V of its keys in registers and
+//   dK^T, dV^T accumulated in registers. It walks over all query tiles of 64,
+//   whose row-major Q and dO tiles, transposed Q^T and dO^T tiles, LSE and D
+//   are copied asynchronously global -> LDS into a two-stage ring one tile
+//   ahead; one barrier per tile. Per tile it recomputes S = Q K^T and
+//   P = exp2(S c log2(e) - LSE log2(e)), forms dP = dO V^T and
+//   dS = P o (dP - D) with the matrix cores, and accumulates dV^T += dO^T P and
 //   dK^T += Q^T dS straight from the accumulator layout (lane column = key).
-//   dS goes through LDS once so the workgroup can form the dQ contribution of
-//   its 128 keys, dQ += c dS K, which is added to the fp32 accumulator with
-//   atomics.
-// Stage 3 (finish): dQ accumulator -> bf16.
+// dQ (query-stationary): one workgroup of eight waves owns 256 queries, each
+//   wave 32, with Q^T and dO^T of its queries in registers and the lane's
+//   LSE and D as scalars. It walks over the key tiles like the forward,
+//   computing S^T = K Q^T and dP^T = V dO^T, dS^T, and dQ^T += K^T dS^T with
+//   dS^T taken straight from the accumulator layout (lane column = query).
+// Splitting the gradient this way recomputes S and dP once more instead of
+// scattering dQ partial sums with atomics; the result is bitwise reproducible.
+#include <algorithm>
+
 #include "common.hpp"
 
 namespace vcja {
 namespace {
 
-constexpr int kBKV = 128;  // keys per workgroup
-constexpr int kBQ = 64;    // queries per inner tile
+constexpr int kBKV = 128;  // keys per dK/dV workgroup
+constexpr int kBQ = kTileTok;  // queries per dK/dV tile
+constexpr int kDqWaves = 8;
+constexpr int kDqBM = 32 * kDqWaves;  // queries per dQ workgroup
+constexpr int kBN = kTileTok;         // keys per dQ tile
 
 template <int D>
 __global__ __launch_bounds__(256) void bwd_prepare_kernel(const __bf16* __restrict__ o,
+                                                          const float* __restrict__ lse,
                                                           const __bf16* __restrict__ dout,
-                                                          float* __restrict__ dd, float* __restrict__ dq_acc,
-                                                          int B, int H, int N) {
+                                                          float* __restrict__ dd, float* __restrict__ lse2, int B,
+                                                          int H, int N, int Npad) {
   constexpr int CPR = D / 8;  // 16-byte chunks per (token, head) row
   const size_t gid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   const size_t rows = (size_t)B * N * H;
@@ -35,9 +50,6 @@ __global__ __launch_bounds__(256) void bwd_prepare_kernel(const __bf16* __restri
     const bf16x8 y = *(const bf16x8*)(dout + row * D + chunk * 8);
 #pragma unroll
     for (int e = 0; e < 8; ++e) sum = fmaf((float)x[e], (float)y[e], sum);
-    f32x4 z = {0.f, 0.f, 0.f, 0.f};
-    *(f32x4*)(dq_acc + row * D + chunk * 8) = z;
-    *(f32x4*)(dq_acc + row * D + chunk * 8 + 4) = z;
   }
 #pragma unroll
   for (int off = 1; off < CPR; off <<= 1) sum += __shfl_xor(sum, off, 64);
@@ -46,59 +58,30 @@ __global__ __launch_bounds__(256) void bwd_prepare_kernel(const __bf16* __restri
     const size_t bn = row / H;
     const int n = (int)(bn % N);
     const int b = (int)(bn / N);
-    dd[((size_t)b * H + h) * N + n] = sum;
+    const size_t bh = (size_t)b * H + h;
+    const float x = lse[bh * N + n];
+    dd[bh * Npad + n] = sum;
+    lse2[bh * Npad + n] = (x == -INFINITY) ? INFINITY : x * kLog2e;
   }
-}
-
-__global__ __launch_bounds__(256) void bwd_finish_kernel(const float* __restrict__ acc, __bf16* __restrict__ dq,
-                                                         size_t n8) {
-  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n8) return;
-  const f32x4 x0 = *(const f32x4*)(acc + 8 * i);
-  const f32x4 x1 = *(const f32x4*)(acc + 8 * i + 4);
-  bf16x8 r = {(__bf16)x0[0], (__bf16)x0[1], (__bf16)x0[2], (__bf16)x0[3],
-              (__bf16)x1[0], (__bf16)x1[1], (__bf16)x1[2], (__bf16)x1[3]};
-  *(bf16x8*)(dq + 8 * i) = r;
-}
-
-// Loads rows [q0, q0+64) of a [B,N,H,D] tensor slice into LDS twice: row-major
-// (stride D+8) and transposed (stride kBQ+4). Each thread takes 4 rows x 8 dims.
-template <int D>
-__device__ __forceinline__ void load_tile_both(const __bf16* __restrict__ src, size_t base, size_t tok, int q0,
-                                               int N, __bf16* rowmaj, __bf16* trans, int tid) {
-  constexpr int RS = D + 8;
-  constexpr int TS = kBQ + 4;
-  for (int g = tid; g < (kBQ / 4) * (D / 8); g += 256) {
-    const int rg = g / (D / 8);
-    const int dg = g % (D / 8);
-    bf16x8 r[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = q0 + 4 * rg + i;
-      r[i] = zero_bf16x8();
-      if (row < N) r[i] = *(const bf16x8*)(src + base + (size_t)row * tok + 8 * dg);
-      *(bf16x8*)&rowmaj[(4 * rg + i) * RS + 8 * dg] = r[i];
-    }
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      bf16x4 t = {r[0][e], r[1][e], r[2][e], r[3][e]};
-      *(bf16x4*)&trans[(8 * dg + e) * TS + 4 * rg] = t;
-    }
+  // Padding rows [N, Npad) of every (sample, head).
+  const size_t pads = (size_t)B * H * (Npad - N);
+  if (gid < pads) {
+    const size_t bh = gid / (Npad - N);
+    const int n = N + (int)(gid % (Npad - N));
+    dd[bh * Npad + n] = 0.0f;
+    lse2[bh * Npad + n] = INFINITY;
   }
 }
 
 template <int D>
-__global__ __launch_bounds__(256, 1) void bwd_main_kernel(BwdArgs a) {
-  constexpr int RS = D + 8;      // row-major Q / dO stride
-  constexpr int TS = kBQ + 4;    // transposed Q / dO stride
-  constexpr int SS = kBKV + 8;   // dS stride
-  __shared__ __attribute__((aligned(16))) __bf16 q_lds[kBQ * RS];
-  __shared__ __attribute__((aligned(16))) __bf16 do_lds[kBQ * RS];
-  __shared__ __attribute__((aligned(16))) __bf16 qt_lds[D * TS];
-  __shared__ __attribute__((aligned(16))) __bf16 dot_lds[D * TS];
-  __shared__ __attribute__((aligned(16))) __bf16 ds_lds[kBQ * SS];
-  __shared__ float lse_lds[kBQ];
-  __shared__ float dd_lds[kBQ];
+__global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(DkdvArgs a) {
+  constexpr int CPR = D / 8;                  // 16-byte chunks per row
+  constexpr int RT = kBQ * D * 2;             // row-major Q or dO tile bytes
+  constexpr int TT = (int)tile_elems(D) * 2;  // transposed tile bytes
+  constexpr int STAGE = 2 * RT + 2 * TT + 512;  // Q | dO | Q^T | dO^T | LSE*log2e[64] | D[64]
+  constexpr int RCOPIES = RT / 1024;
+  constexpr int TCOPIES = TT / 1024;
+  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -111,8 +94,8 @@ __global__ __launch_bounds__(256, 1) void bwd_main_kernel(BwdArgs a) {
   const size_t tok = (size_t)a.H * D;
   const size_t base = (size_t)b * N * tok + (size_t)h * D;
   const size_t bh = (size_t)b * a.H + h;
-  const int kbase = blockIdx.x * kBKV;
-  const int key = kbase + w * 32 + l32;  // this lane's key (accumulator column)
+  const int npad = a.ntile * kBQ;
+  const int key = blockIdx.x * kBKV + w * 32 + l32;  // this lane's key (accumulator column)
 
   int tl = a.T;
   if (a.text_len) tl = min(max(a.text_len[b], 0), a.T);
@@ -120,9 +103,9 @@ __global__ __launch_bounds__(256, 1) void bwd_main_kernel(BwdArgs a) {
   if (valid && a.key_mask) valid = a.key_mask[(size_t)b * N + key] != 0;
 
   if (!__syncthreads_or(valid)) {
-    // No valid key in this workgroup: its dK, dV are zero and it adds nothing to dQ.
+    // No valid key in this workgroup: its dK, dV are zero.
     if (key < N) {
-      bf16x8 z = zero_bf16x8();
+      const bf16x8 z = zero_bf16x8();
       for (int c = 0; c < D / 8; ++c) {
         *(bf16x8*)(a.dk + base + (size_t)key * tok + 8 * c) = z;
         *(bf16x8*)(a.dv + base + (size_t)key * tok + 8 * c) = z;
@@ -131,30 +114,37 @@ __global__ __launch_bounds__(256, 1) void bwd_main_kernel(BwdArgs a) {
     return;
   }
 
+  // Copies query tile qt into stage st. Row-major rows past N repeat row N-1; the padded
+  // LSE (+inf) makes their probabilities zero.
+  auto issue = [&](int qt, int st) {
+    VC_LDS char* sq = (VC_LDS char*)smem + st * STAGE;
+    for (int idx = w; idx < RCOPIES; idx += 4) {
+      const int lin = idx * 64 + lane;
+      const int r = lin / CPR;
+      const int c = (lin % CPR) ^ (r & (CPR - 1));
+      const size_t goff = base + (size_t)min(qt * kBQ + r, N - 1) * tok + c * 8;
+      copy16_to_lds(a.q + goff, sq + idx * 1024);
+      copy16_to_lds(a.dout + goff, sq + RT + idx * 1024);
+    }
+    const size_t toff = (bh * a.ntile + qt) * tile_elems(D);
+    for (int idx = w; idx < TCOPIES; idx += 4) {
+      copy16_to_lds(a.qt + toff + idx * 512 + lane * 8, sq + 2 * RT + idx * 1024);
+      copy16_to_lds(a.dot + toff + idx * 512 + lane * 8, sq + 2 * RT + TT + idx * 1024);
+    }
+    if (w == 3 && lane < 32) {
+      const float* src = (lane < 16 ? a.lse2 : a.dd) + bh * npad + qt * kBQ + 4 * (lane & 15);
+      copy16_to_lds(src, sq + 2 * RT + 2 * TT);
+    }
+  };
+
   // K, V of this lane's key as B operands (dims 16*ks + 8*hi .. +7).
   bf16x8 kf[D / 16], vf[D / 16];
+  {
+    const size_t kr = base + (size_t)min(key, N - 1) * tok + 8 * hi;
 #pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks) {
-    kf[ks] = zero_bf16x8();
-    vf[ks] = zero_bf16x8();
-    if (key < N) {
-      kf[ks] = *(const bf16x8*)(a.k + base + (size_t)key * tok + 16 * ks + 8 * hi);
-      vf[ks] = *(const bf16x8*)(a.v + base + (size_t)key * tok + 16 * ks + 8 * hi);
-    }
-  }
-
-  // dQ blocks owned by this wave: (query block qb, dim slice dsl) of 32x32.
-  constexpr int kDqBlocks = (kBQ / 32) * (D / 32) / 4;  // per wave: 2 for D=128, 1 for D=64
-  const int dsl = (D == 128) ? w : (w & 1);
-  const int qb_first = (D == 128) ? 0 : (w >> 1);
-  // K as the B operand of dQ = dS K: lane holds dim dsl*32 + l32, keys 16*ks + 8*hi .. +7.
-  bf16x8 ktf[kBKV / 16];
-#pragma unroll
-  for (int ks = 0; ks < kBKV / 16; ++ks) {
-#pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      const int kk = kbase + 16 * ks + 8 * hi + t;
-      ktf[ks][t] = (kk < N) ? a.k[base + (size_t)kk * tok + dsl * 32 + l32] : (__bf16)0.0f;
+    for (int ks = 0; ks < D / 16; ++ks) {
+      kf[ks] = *(const bf16x8*)(a.k + kr + 16 * ks);
+      vf[ks] = *(const bf16x8*)(a.v + kr + 16 * ks);
     }
   }
 
@@ -165,83 +155,56 @@ __global__ __launch_bounds__(256, 1) void bwd_main_kernel(BwdArgs a) {
     dv_acc[i] = zero_f32x16();
   }
 
-  const int nqt = (N + kBQ - 1) / kBQ;
-  for (int qt = 0; qt < nqt; ++qt) {
-    const int q0 = qt * kBQ;
-    __syncthreads();
-    load_tile_both<D>(a.q, base, tok, q0, N, q_lds, qt_lds, tid);
-    load_tile_both<D>(a.dout, base, tok, q0, N, do_lds, dot_lds, tid);
-    if (tid < kBQ) {
-      const int row = q0 + tid;
-      float l2 = INFINITY, dv = 0.0f;
-      if (row < N) {
-        const float x = a.lse[bh * N + row];
-        l2 = (x == -INFINITY) ? INFINITY : x * kLog2e;  // rows without keys: P = 0
-        dv = a.dd[bh * N + row];
-      }
-      lse_lds[tid] = l2;
-      dd_lds[tid] = dv;
-    }
-    __syncthreads();
+  issue(0, 0);
+  for (int qt = 0; qt < a.ntile; ++qt) {
+    wait_all_memory();
+    __syncthreads();  // stage qt&1 holds tile qt; every wave is done with the other stage
+    if (qt + 1 < a.ntile) issue(qt + 1, (qt + 1) & 1);
+    const VC_LDS char* q_lds = (const VC_LDS char*)smem + (qt & 1) * STAGE;
+    const VC_LDS char* do_lds = q_lds + RT;
+    const VC_LDS char* qt_lds = q_lds + 2 * RT;
+    const VC_LDS char* dot_lds = qt_lds + TT;
+    const VC_LDS float* lse_lds = (const VC_LDS float*)(qt_lds + 2 * TT);
+    const VC_LDS float* dd_lds = lse_lds + kBQ;
 
 #pragma unroll
     for (int qb = 0; qb < kBQ / 32; ++qb) {
       f32x16 s = zero_f32x16(), dp = zero_f32x16();
 #pragma unroll
       for (int ks = 0; ks < D / 16; ++ks) {
-        const bf16x8 qa = *(const bf16x8*)&q_lds[(qb * 32 + l32) * RS + 16 * ks + 8 * hi];
+        const bf16x8 qa = *(const VC_LDS bf16x8*)(q_lds + swz_off<CPR>(qb * 32 + l32, 2 * ks + hi));
         s = mfma32(qa, kf[ks], s);
       }
 #pragma unroll
       for (int ks = 0; ks < D / 16; ++ks) {
-        const bf16x8 da = *(const bf16x8*)&do_lds[(qb * 32 + l32) * RS + 16 * ks + 8 * hi];
+        const bf16x8 da = *(const VC_LDS bf16x8*)(do_lds + swz_off<CPR>(qb * 32 + l32, 2 * ks + hi));
         dp = mfma32(da, vf[ks], dp);
       }
+      // Register r holds query row qb*32 + 8*(r/4) + 4*hi + r%4: four runs of 4 rows.
       float p[16], ds[16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int ql = qb * 32 + acc_row(r, hi);
-        p[r] = valid ? fast_exp2(fmaf(s[r], a.scale_log2, -lse_lds[ql])) : 0.0f;
-        ds[r] = p[r] * (dp[r] - dd_lds[ql]);
-      }
-      // Register r holds query row 8*(r/4) + 4*hi + r%4; operand element t of k-step st
-      // stands for query 16*st + 8*(t/4) + 4*hi + t%4, and Q^T / dO^T are read in that order.
+      for (int j = 0; j < 4; ++j) {
+        const f32x4 l2 = *(const VC_LDS f32x4*)(lse_lds + qb * 32 + 8 * j + 4 * hi);
+        const f32x4 d4 = *(const VC_LDS f32x4*)(dd_lds + qb * 32 + 8 * j + 4 * hi);
 #pragma unroll
-      for (int st = 0; st < 2; ++st) {
-        const bf16x8 pb = to_bf16x8(&p[8 * st]);
-        const bf16x8 sb = to_bf16x8(&ds[8 * st]);
-#pragma unroll
-        for (int db = 0; db < D / 32; ++db) {
-          const int off = (db * 32 + l32) * TS + qb * 32 + 16 * st + 4 * hi;
-          const bf16x8 doa = cat4(*(const bf16x4*)&dot_lds[off], *(const bf16x4*)&dot_lds[off + 8]);
-          dv_acc[db] = mfma32(doa, pb, dv_acc[db]);
-          const bf16x8 qa = cat4(*(const bf16x4*)&qt_lds[off], *(const bf16x4*)&qt_lds[off + 8]);
-          dk_acc[db] = mfma32(qa, sb, dk_acc[db]);
+        for (int i = 0; i < 4; ++i) {
+          const int r = 4 * j + i;
+          p[r] = valid ? fast_exp2(fmaf(s[r], a.scale_log2, -l2[i])) : 0.0f;
+          ds[r] = p[r] * (dp[r] - d4[i]);
         }
       }
+      // Operand element t of k-step st2 is query 16*st2 + 8*(t/4) + 4*hi + t%4, stored by
+      // the transposed tiles as 8 consecutive elements at position 16*st2 + 8*hi.
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int ql = qb * 32 + acc_row(r, hi);
-        ds_lds[ql * SS + w * 32 + l32] = (__bf16)ds[r];
-      }
-    }
-    __syncthreads();
-
-    // dQ contribution of this workgroup's keys for the tile.
+      for (int st2 = 0; st2 < 2; ++st2) {
+        const bf16x8 pb = to_bf16x8(&p[8 * st2]);
+        const bf16x8 sb = to_bf16x8(&ds[8 * st2]);
 #pragma unroll
-    for (int i = 0; i < kDqBlocks; ++i) {
-      const int qb = qb_first + i;
-      f32x16 acc = zero_f32x16();
-#pragma unroll
-      for (int ks = 0; ks < kBKV / 16; ++ks) {
-        const bf16x8 sa = *(const bf16x8*)&ds_lds[(qb * 32 + l32) * SS + 16 * ks + 8 * hi];
-        acc = mfma32(sa, ktf[ks], acc);
-      }
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int qrow = q0 + qb * 32 + acc_row(r, hi);
-        if (qrow < N) unsafeAtomicAdd(a.dq_acc + ((size_t)b * N + qrow) * tok + (size_t)h * D + dsl * 32 + l32,
-                                      acc[r] * a.scale);
+        for (int db = 0; db < D / 32; ++db) {
+          const int off = ((db * 32 + l32) * kTileRow + qb * 32 + 16 * st2 + 8 * hi) * 2;
+          dv_acc[db] = mfma32(*(const VC_LDS bf16x8*)(dot_lds + off), pb, dv_acc[db]);
+          dk_acc[db] = mfma32(*(const VC_LDS bf16x8*)(qt_lds + off), sb, dk_acc[db]);
+        }
       }
     }
   }
@@ -263,32 +226,161 @@ __global__ __launch_bounds__(256, 1) void bwd_main_kernel(BwdArgs a) {
   }
 }
 
+template <int D>
+__global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
+  constexpr int CPR = D / 8;
+  constexpr int RT = kBN * D * 2;             // row-major K or V tile bytes
+  constexpr int TT = (int)tile_elems(D) * 2;  // transposed K tile bytes
+  constexpr int STAGE = 2 * RT + TT;          // K | V | K^T
+  constexpr int RCOPIES = RT / 1024;
+  constexpr int TCOPIES = TT / 1024;
+  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int w = tid >> 6;
+  const int l32 = lane & 31;
+  const int hi = lane >> 5;
+  const int h = blockIdx.y;
+  const int b = blockIdx.z;
+  const int N = a.N;
+  const size_t tok = (size_t)a.H * D;
+  const size_t base = (size_t)b * N * tok + (size_t)h * D;
+  const size_t bh = (size_t)b * a.H + h;
+  const int qi = blockIdx.x * kDqBM + w * 32 + l32;  // this lane's query (accumulator column)
+  const int qr = min(qi, N - 1);
+
+  // Q^T and dO^T as B operands (dims 16*ks + 8*hi .. +7), LSE*log2e and D as scalars.
+  bf16x8 qf[D / 16], dof[D / 16];
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) {
+    qf[ks] = *(const bf16x8*)(a.q + base + (size_t)qr * tok + 16 * ks + 8 * hi);
+    dof[ks] = *(const bf16x8*)(a.dout + base + (size_t)qr * tok + 16 * ks + 8 * hi);
+  }
+  const float lse2 = a.lse2[bh * (size_t)a.ntile * kBN + qr];
+  const float dd = a.dd[bh * (size_t)a.ntile * kBN + qr];
+
+  f32x16 dq_acc[D / 32];
+#pragma unroll
+  for (int i = 0; i < D / 32; ++i) dq_acc[i] = zero_f32x16();
+
+  int tl = a.T;
+  if (a.text_len) tl = min(max(a.text_len[b], 0), a.T);
+  const uint8_t* km = a.key_mask ? a.key_mask + (size_t)b * N : nullptr;
+  auto next_tile = [&](int kt) {
+    if (!km)
+      while (kt < a.ntile && kt * kBN >= tl && kt * kBN + kBN <= a.T) ++kt;
+    return kt;
+  };
+  auto issue = [&](int kt, int st) {
+    VC_LDS char* sk = (VC_LDS char*)smem + st * STAGE;
+    for (int idx = w; idx < RCOPIES; idx += kDqWaves) {
+      const int lin = idx * 64 + lane;
+      const int r = lin / CPR;
+      const int c = (lin % CPR) ^ (r & (CPR - 1));
+      const size_t goff = base + (size_t)min(kt * kBN + r, N - 1) * tok + c * 8;
+      copy16_to_lds(a.k + goff, sk + idx * 1024);
+      copy16_to_lds(a.v + goff, sk + RT + idx * 1024);
+    }
+    const __bf16* tsrc = a.kt + (bh * a.ntile + kt) * tile_elems(D);
+    for (int idx = w; idx < TCOPIES; idx += kDqWaves) copy16_to_lds(tsrc + idx * 512 + lane * 8, sk + 2 * RT + idx * 1024);
+  };
+
+  int kt = next_tile(0);
+  if (kt < a.ntile) issue(kt, 0);
+  int st = 0;
+  while (kt < a.ntile) {
+    const int kn = next_tile(kt + 1);
+    wait_all_memory();
+    __syncthreads();
+    if (kn < a.ntile) issue(kn, st ^ 1);
+    const VC_LDS char* k_lds = (const VC_LDS char*)smem + st * STAGE;
+    const VC_LDS char* v_lds = k_lds + RT;
+    const VC_LDS char* kt_lds = k_lds + 2 * RT;
+    const int k0 = kt * kBN;
+    const bool need_mask = km || (tl < a.T && k0 < a.T && k0 + kBN > tl) || (k0 + kBN > N);
+
+#pragma unroll
+    for (int kb = 0; kb < kBN / 32; ++kb) {
+      f32x16 s = zero_f32x16(), dp = zero_f32x16();
+#pragma unroll
+      for (int ks = 0; ks < D / 16; ++ks) {
+        const bf16x8 ka = *(const VC_LDS bf16x8*)(k_lds + swz_off<CPR>(kb * 32 + l32, 2 * ks + hi));
+        s = mfma32(ka, qf[ks], s);
+      }
+#pragma unroll
+      for (int ks = 0; ks < D / 16; ++ks) {
+        const bf16x8 va = *(const VC_LDS bf16x8*)(v_lds + swz_off<CPR>(kb * 32 + l32, 2 * ks + hi));
+        dp = mfma32(va, dof[ks], dp);
+      }
+      // Register r holds key k0 + kb*32 + 8*(r/4) + 4*hi + r%4 of this lane's query.
+      float ds[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float p = fast_exp2(fmaf(s[r], a.scale_log2, -lse2));
+        if (need_mask) {
+          const int key = k0 + kb * 32 + acc_row(r, hi);
+          bool ok = key < N && (key >= a.T || key < tl);
+          if (ok && km) ok = km[key] != 0;
+          if (!ok) p = 0.0f;
+        }
+        ds[r] = p * (dp[r] - dd);
+      }
+#pragma unroll
+      for (int st2 = 0; st2 < 2; ++st2) {
+        const bf16x8 sb = to_bf16x8(&ds[8 * st2]);
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) {
+          const int off = ((db * 32 + l32) * kTileRow + kb * 32 + 16 * st2 + 8 * hi) * 2;
+          dq_acc[db] = mfma32(*(const VC_LDS bf16x8*)(kt_lds + off), sb, dq_acc[db]);
+        }
+      }
+    }
+    st ^= 1;
+    kt = kn;
+  }
+
+  if (qi < N) {
+    __bf16* qp = a.dq + base + (size_t)qi * tok;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        bf16x4 t = {(__bf16)(dq_acc[db][4 * j + 0] * a.scale), (__bf16)(dq_acc[db][4 * j + 1] * a.scale),
+                    (__bf16)(dq_acc[db][4 * j + 2] * a.scale), (__bf16)(dq_acc[db][4 * j + 3] * a.scale)};
+        *(bf16x4*)(qp + db * 32 + 8 * j + 4 * hi) = t;
+      }
+  }
+}
+
 }  // namespace
 
-hipError_t launch_bwd_prepare(const __bf16* o, const __bf16* dout, float* dd, float* dq_acc, int B, int H, int N,
-                              int head_dim, hipStream_t s) {
-  const size_t threads = (size_t)B * N * H * (head_dim / 8);
+hipError_t launch_bwd_prepare(const __bf16* o, const float* lse, const __bf16* dout, float* dd, float* lse2, int B,
+                              int H, int N, int Npad, int head_dim, hipStream_t s) {
+  const size_t threads = std::max((size_t)B * N * H * (head_dim / 8), (size_t)B * H * (Npad - N));
   dim3 grid((unsigned)((threads + 255) / 256));
   if (head_dim == 128)
-    hipLaunchKernelGGL(bwd_prepare_kernel<128>, grid, dim3(256), 0, s, o, dout, dd, dq_acc, B, H, N);
+    hipLaunchKernelGGL(bwd_prepare_kernel<128>, grid, dim3(256), 0, s, o, lse, dout, dd, lse2, B, H, N, Npad);
   else
-    hipLaunchKernelGGL(bwd_prepare_kernel<64>, grid, dim3(256), 0, s, o, dout, dd, dq_acc, B, H, N);
+    hipLaunchKernelGGL(bwd_prepare_kernel<64>, grid, dim3(256), 0, s, o, lse, dout, dd, lse2, B, H, N, Npad);
   return hipGetLastError();
 }
 
-hipError_t launch_bwd_main(const BwdArgs& a, int head_dim, hipStream_t s) {
+hipError_t launch_bwd_dkdv(const DkdvArgs& a, int head_dim, hipStream_t s) {
   dim3 grid((a.N + kBKV - 1) / kBKV, a.H, a.B);
   if (head_dim == 128)
-    hipLaunchKernelGGL(bwd_main_kernel<128>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(bwd_dkdv_kernel<128>, grid, dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL(bwd_main_kernel<64>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(bwd_dkdv_kernel<64>, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
-hipError_t launch_bwd_finish(const float* dq_acc, __bf16* dq, int B, int H, int N, int head_dim, hipStream_t s) {
-  const size_t n8 = (size_t)B * N * H * head_dim / 8;
-  dim3 grid((unsigned)((n8 + 255) / 256));
-  hipLaunchKernelGGL(bwd_finish_kernel, grid, dim3(256), 0, s, dq_acc, dq, n8);
+hipError_t launch_bwd_dq(const DqArgs& a, int head_dim, hipStream_t s) {
+  dim3 grid((a.N + kDqBM - 1) / kDqBM, a.H, a.B);
+  if (head_dim == 128)
+    hipLaunchKernelGGL(bwd_dq_kernel<128>, grid, dim3(64 * kDqWaves), 0, s, a);
+  else
+    hipLaunchKernelGGL(bwd_dq_kernel<64>, grid, dim3(64 * kDqWaves), 0, s, a);
   return hipGetLastError();
 }
 

@@ -54,47 +54,115 @@ __device__ __forceinline__ f32x16 zero_f32x16() {
   return z;
 }
 
+#define VC_LDS __attribute__((address_space(3)))
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+
+// Asynchronous 16-byte copy global -> LDS: lane t of the wave writes its 16 bytes at
+// lds_wave_base + 16*t (lds_wave_base must be the same for the whole wave). Completion is
+// tracked by the vector-memory counter.
+__device__ __forceinline__ void copy16_to_lds(const void* g, VC_LDS void* lds_wave_base) {
+  __builtin_amdgcn_global_load_lds(g, lds_wave_base, 16, 0, 0);
+}
+
+// Waits for every outstanding memory operation of this wave (vector memory and LDS).
+__device__ __forceinline__ void wait_all_memory() { __builtin_amdgcn_s_waitcnt(0); }
+
+// Transposing LDS read (ds_read_b64_tr_b16). Within each group of 16 lanes, lane 4e+g
+// supplies the address of 4 consecutive bf16 at (row r0+e, columns c0+4g .. c0+4g+3) of a
+// row-major tile; lane i of the group receives the column c0+i of rows r0 .. r0+3.
+__device__ __forceinline__ bf16x4 lds_read_tr(const VC_LDS void* p) {
+  i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((VC_LDS i16x4*)p);
+  return __builtin_bit_cast(bf16x4, v);
+}
+
+// Row-major bf16 tile of rows x (8*CPR) in LDS, stored as 16-byte chunks with the chunk
+// index XOR-ed by the row (mod CPR) so that column-wise accesses spread over the banks.
+template <int CPR>
+__device__ __forceinline__ int swz_off(int row, int chunk) {
+  return row * (CPR * 16) + ((chunk ^ (row & (CPR - 1))) << 4);
+}
+// Byte offset of the 8-byte half-chunk holding columns [col, col+4), col a multiple of 4.
+template <int CPR>
+__device__ __forceinline__ int swz_off4(int row, int col) {
+  return swz_off<CPR>(row, col >> 3) + (((col >> 2) & 1) << 3);
+}
+
 // Value of lane l^32 (the other half of the wave).
 __device__ __forceinline__ float swap_halves(float x) { return __shfl_xor(x, 32, 64); }
+
+// Transposed token tiles ("token-major" copies). A [B, N, H, D] tensor X is also kept as
+// blocked tiles XT[b][h][tile][d][kTileRow] of kTileTok tokens: row d of a tile holds
+// X[tile*64 + tok][d] for the 64 tokens, followed by 8 padding elements (so that the 32
+// rows read by one MFMA operand fall on distinct LDS banks). Inside each run of 16 tokens
+// the second and third groups of 4 are swapped, so that the 8 tokens a lane supplies to
+// one 32x32x16 MFMA step - tokens 16s + 8*(t/4) + 4*hi + t%4, t = 0..7, the order in
+// which an accumulator column holds them - are 8 consecutive elements (one 16-byte read).
+constexpr int kTileTok = 64;
+constexpr int kTileRow = kTileTok + 8;  // elements per transposed tile row
+__host__ __device__ constexpr size_t tile_elems(int d) { return (size_t)d * kTileRow; }
+// Position of token t (0..63) inside a transposed tile row.
+__host__ __device__ constexpr int tok_pos(int t) {
+  return (t & ~15) | (((t >> 2) & 3) == 1 ? 8 : ((t >> 2) & 3) == 2 ? 4 : ((t >> 2) & 3) * 4) | (t & 3);
+}
 
 // Kernel arguments. Token stride is H*D elements ([B, N, H, D] layout).
 struct FwdArgs {
   const __bf16* q;
   const __bf16* k;
-  const __bf16* v;
+  const __bf16* vt;     // V as transposed token tiles
   const int32_t* text_len;
   const uint8_t* key_mask;
   __bf16* o;
   float* lse;
-  int B, H, N, T;
-  float scale_log2;  // softmax scale times log2(e)
+  int B, H, N, T, ntile;  // ntile = tiles of 64 tokens per (sample, head)
+  float scale_log2;       // softmax scale times log2(e)
 };
 
-struct BwdArgs {
+// Backward, key-stationary part: dK and dV.
+struct DkdvArgs {
   const __bf16* q;
   const __bf16* k;
   const __bf16* v;
   const __bf16* dout;
-  const float* lse;
-  const float* dd;      // D = rowsum(dO o O), [B, H, N]
+  const __bf16* qt;     // Q as transposed token tiles
+  const __bf16* dot;    // dO as transposed token tiles
+  const float* lse2;    // LSE * log2(e), +inf for rows without keys and padding, [B, H, Npad]
+  const float* dd;      // D = rowsum(dO o O), 0 on padding, [B, H, Npad]
   const int32_t* text_len;
   const uint8_t* key_mask;
   __bf16* dk;
   __bf16* dv;
-  float* dq_acc;        // [B, N, H, D] fp32
-  int B, H, N, T;
+  int B, H, N, T, ntile;
   float scale;          // softmax scale
   float scale_log2;     // scale * log2(e)
+};
+
+// Backward, query-stationary part: dQ.
+struct DqArgs {
+  const __bf16* q;
+  const __bf16* k;
+  const __bf16* v;
+  const __bf16* dout;
+  const __bf16* kt;     // K as transposed token tiles
+  const float* lse2;
+  const float* dd;
+  const int32_t* text_len;
+  const uint8_t* key_mask;
+  __bf16* dq;
+  int B, H, N, T, ntile;
+  float scale;
+  float scale_log2;
 };
 
 }  // namespace vcja
 
 // Host-side launchers (defined in the .hip kernel files).
 namespace vcja {
+// Writes the transposed token tiles of x ([B, N, H, D]) into xt.
+hipError_t launch_token_tiles(const __bf16* x, __bf16* xt, int B, int H, int N, int head_dim, hipStream_t s);
 hipError_t launch_fwd(const FwdArgs& a, int head_dim, hipStream_t s);
-hipError_t launch_bwd_prepare(const __bf16* o, const __bf16* dout, float* dd, float* dq_acc, int B, int H,
-                              int N, int head_dim, hipStream_t s);
-hipError_t launch_bwd_main(const BwdArgs& a, int head_dim, hipStream_t s);
-hipError_t launch_bwd_finish(const float* dq_acc, __bf16* dq, int B, int H, int N, int head_dim,
-                             hipStream_t s);
+hipError_t launch_bwd_prepare(const __bf16* o, const float* lse, const __bf16* dout, float* dd, float* lse2, int B,
+                              int H, int N, int Npad, int head_dim, hipStream_t s);
+hipError_t launch_bwd_dkdv(const DkdvArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_bwd_dq(const DqArgs& a, int head_dim, hipStream_t s);
 }  // namespace vcja

@@ -1,28 +1,42 @@
 // Forward joint text-video attention for gfx950.
 //
-// One workgroup of four waves owns 128 queries of one (sample, head); each
-// wave owns 32 of them. Keys and values stream through LDS in tiles of 64.
-// The wave computes the transposed score block S^T = K Q^T with the matrix
-// cores (32x32x16 bf16), so each lane's accumulator column is one query:
-// the running maximum and sum of the online softmax are per-lane scalars and
-// need one exchange between the two wave halves per tile. P^T leaves the
+// One workgroup of eight waves owns 256 queries of one (sample, head); each
+// wave owns 32 of them, held in registers. Keys stream through LDS as
+// row-major tiles of 64 (16-byte chunks XOR-swizzled by row) and values as
+// transposed token tiles (prepared by a reformatting pass), both copied
+// asynchronously global -> LDS into a two-stage ring so the next tile lands
+// while the current one is computed; one barrier per tile. All eight waves
+// share each tile.
+//
+// The wave computes the transposed score block S^T = K Q^T with 32x32x16 bf16
+// matrix-core steps, so each lane's accumulator column is one query: the
+// running maximum and sum of the online softmax are per-lane scalars that need
+// one exchange between the two wave halves per tile. P^T leaves the
 // accumulator already laid out as the B operand of O^T += V^T P^T, so
-// probabilities never go through LDS. V is stored transposed in LDS for that
-// product. The log-sum-exp is kept for the recomputing backward.
+// probabilities never go through LDS. The exponent base is only raised when a
+// tile's maximum exceeds it by more than 2^8, so the O^T rescale is rare
+// (probabilities stay below 256, exact in the bf16 exponent range). The
+// log-sum-exp is kept for the recomputing backward.
 #include "common.hpp"
 
 namespace vcja {
 namespace {
 
-constexpr int kBM = 128;  // queries per workgroup
-constexpr int kBN = 64;   // keys per tile
+constexpr int kWaves = 8;
+constexpr int kBM = 32 * kWaves;  // queries per workgroup
+constexpr int kBN = kTileTok;     // keys per tile
+constexpr float kRescaleSlack = 8.0f;  // log2 units
 
 template <int D>
-__global__ __launch_bounds__(256, 1) void fwd_kernel(FwdArgs a) {
-  constexpr int KS = D + 8;    // K row stride in LDS (bf16), padded against bank conflicts
-  constexpr int VS = kBN + 4;  // V^T row stride in LDS (bf16)
-  __shared__ __attribute__((aligned(16))) __bf16 ks_lds[kBN * KS];
-  __shared__ __attribute__((aligned(16))) __bf16 vt_lds[D * VS];
+__global__ __launch_bounds__(64 * kWaves, 1) void fwd_kernel(FwdArgs a) {
+  constexpr int CPR = D / 8;                    // 16-byte chunks per key row
+  constexpr int KT = kBN * D * 2;               // K tile bytes
+  constexpr int VTB = (int)tile_elems(D) * 2;   // V^T tile bytes
+  constexpr int STAGE = KT + VTB;
+  constexpr int KCOPIES = KT / 1024;            // 1 KiB wave copies per tile
+  constexpr int VCOPIES = VTB / 1024;
+  static_assert(VTB % 1024 == 0, "transposed tile must be whole wave copies");
+  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -34,62 +48,57 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdArgs a) {
   const int N = a.N;
   const size_t tok = (size_t)a.H * D;
   const size_t base = (size_t)b * N * tok + (size_t)h * D;
+  const __bf16* vt_bh = a.vt + ((size_t)b * a.H + h) * a.ntile * tile_elems(D);
   const int qi = blockIdx.x * kBM + w * 32 + l32;
 
   // Q^T as the B operand: lane holds query qi, dims 16*ks + 8*hi .. +7.
   bf16x8 qf[D / 16];
-  if (qi < N) {
-    const __bf16* qp = a.q + base + (size_t)qi * tok + 8 * hi;
+  {
+    const __bf16* qp = a.q + base + (size_t)min(qi, N - 1) * tok + 8 * hi;
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) qf[ks] = *(const bf16x8*)(qp + 16 * ks);
-  } else {
-#pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks) qf[ks] = zero_bf16x8();
   }
 
   f32x16 oacc[D / 32];
 #pragma unroll
   for (int i = 0; i < D / 32; ++i) oacc[i] = zero_f32x16();
-  float m = -INFINITY;  // running max of scaled scores, log2 units
+  float m = -INFINITY;  // exponent base (scaled scores, log2 units)
   float l = 0.0f;       // running sum of this lane's half
 
   int tl = a.T;
   if (a.text_len) tl = min(max(a.text_len[b], 0), a.T);
   const uint8_t* km = a.key_mask ? a.key_mask + (size_t)b * N : nullptr;
-  const int ntiles = (N + kBN - 1) / kBN;
+  // A tile made only of padded text keys contributes nothing and is skipped.
+  auto next_tile = [&](int kt) {
+    if (!km)
+      while (kt < a.ntile && kt * kBN >= tl && kt * kBN + kBN <= a.T) ++kt;
+    return kt;
+  };
+  // Copies tile kt (K rows, V^T tile) into stage st. K rows past N repeat row N-1 and
+  // are masked.
+  auto issue = [&](int kt, int st) {
+    VC_LDS char* sk = (VC_LDS char*)smem + st * STAGE;
+    for (int idx = w; idx < KCOPIES; idx += kWaves) {
+      const int lin = idx * 64 + lane;
+      const int r = lin / CPR;
+      const int c = (lin % CPR) ^ (r & (CPR - 1));
+      copy16_to_lds(a.k + base + (size_t)min(kt * kBN + r, N - 1) * tok + c * 8, sk + idx * 1024);
+    }
+    const __bf16* vsrc = vt_bh + (size_t)kt * tile_elems(D);
+    for (int idx = w; idx < VCOPIES; idx += kWaves) copy16_to_lds(vsrc + idx * 512 + lane * 8, sk + KT + idx * 1024);
+  };
 
-  for (int kt = 0; kt < ntiles; ++kt) {
+  int kt = next_tile(0);
+  if (kt < a.ntile) issue(kt, 0);
+  int st = 0;
+  while (kt < a.ntile) {
+    const int kn = next_tile(kt + 1);
+    wait_all_memory();
+    __syncthreads();  // stage st holds tile kt; every wave is done with stage st^1
+    if (kn < a.ntile) issue(kn, st ^ 1);
+    const VC_LDS char* ks_lds = (const VC_LDS char*)smem + st * STAGE;
+    const VC_LDS char* vt_lds = ks_lds + KT;
     const int k0 = kt * kBN;
-    // A tile made only of padded text keys contributes nothing.
-    if (!km && k0 >= tl && k0 + kBN <= a.T) continue;
-    __syncthreads();
-    // K tile, row-major.
-    for (int c = tid; c < kBN * D / 8; c += 256) {
-      const int kr = c / (D / 8);
-      const int col = (c % (D / 8)) * 8;
-      const int key = k0 + kr;
-      bf16x8 val = zero_bf16x8();
-      if (key < N) val = *(const bf16x8*)(a.k + base + (size_t)key * tok + col);
-      *(bf16x8*)&ks_lds[kr * KS + col] = val;
-    }
-    // V tile, transposed: thread takes 4 keys x 8 dims.
-    for (int g = tid; g < (kBN / 4) * (D / 8); g += 256) {
-      const int kg = g / (D / 8);
-      const int dg = g % (D / 8);
-      bf16x8 r[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int key = k0 + 4 * kg + i;
-        r[i] = zero_bf16x8();
-        if (key < N) r[i] = *(const bf16x8*)(a.v + base + (size_t)key * tok + 8 * dg);
-      }
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        bf16x4 t = {r[0][e], r[1][e], r[2][e], r[3][e]};
-        *(bf16x4*)&vt_lds[(8 * dg + e) * VS + 4 * kg] = t;
-      }
-    }
-    __syncthreads();
 
     // S^T = K Q^T for two 32-key blocks.
     f32x16 s[kBN / 32];
@@ -98,7 +107,7 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdArgs a) {
       s[kb] = zero_f32x16();
 #pragma unroll
       for (int ks = 0; ks < D / 16; ++ks) {
-        bf16x8 af = *(const bf16x8*)&ks_lds[(kb * 32 + l32) * KS + 16 * ks + 8 * hi];
+        const bf16x8 af = *(const VC_LDS bf16x8*)(ks_lds + swz_off<CPR>(kb * 32 + l32, 2 * ks + hi));
         s[kb] = mfma32(af, qf[ks], s[kb]);
       }
     }
@@ -123,14 +132,17 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdArgs a) {
     for (int kb = 0; kb < kBN / 32; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
-    mx = fmaxf(mx, swap_halves(mx));
-    const float m_new = fmaxf(m, mx * a.scale_log2);
-    const float m_use = (m_new == -INFINITY) ? 0.0f : m_new;
-    const float alpha = fast_exp2(m - m_use);
-    m = m_new;
-    l *= alpha;
+    mx = fmaxf(mx, swap_halves(mx)) * a.scale_log2;
+    const bool raise = mx > m + kRescaleSlack;
+    if (__any(raise)) {
+      const float m_new = raise ? mx : m;
+      const float alpha = raise ? fast_exp2(m - m_new) : 1.0f;  // 0 when m was -inf
+      m = m_new;
+      l *= alpha;
 #pragma unroll
-    for (int i = 0; i < D / 32; ++i) oacc[i] *= alpha;
+      for (int i = 0; i < D / 32; ++i) oacc[i] *= alpha;
+    }
+    const float m_use = (m == -INFINITY) ? 0.0f : m;
 
     float p[kBN / 32][16];
 #pragma unroll
@@ -141,22 +153,23 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdArgs a) {
         l += p[kb][r];
       }
 
-    // O^T += V^T P^T. Register r of the S^T block maps to key 8*(r/4) + 4*hi + r%4, so the
-    // operand pair (lane half hi, element t) of k-step st stands for key
-    // 16*st + 8*(t/4) + 4*hi + t%4; V^T is read in that order.
+    // O^T += V^T P^T. Operand element t of k-step st2 (lane half hi) is key
+    // 16*st2 + 8*(t/4) + 4*hi + t%4, which the transposed tile stores as 8 consecutive
+    // elements at position 16*st2 + 8*hi.
 #pragma unroll
     for (int kb = 0; kb < kBN / 32; ++kb) {
 #pragma unroll
-      for (int st = 0; st < 2; ++st) {
-        const bf16x8 pb = to_bf16x8(&p[kb][8 * st]);
+      for (int st2 = 0; st2 < 2; ++st2) {
+        const bf16x8 pb = to_bf16x8(&p[kb][8 * st2]);
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) {
-          const __bf16* vp = &vt_lds[(db * 32 + l32) * VS + kb * 32 + 16 * st + 4 * hi];
-          const bf16x8 af = cat4(*(const bf16x4*)vp, *(const bf16x4*)(vp + 8));
+          const bf16x8 af = *(const VC_LDS bf16x8*)(vt_lds + ((db * 32 + l32) * kTileRow + kb * 32 + 16 * st2 + 8 * hi) * 2);
           oacc[db] = mfma32(af, pb, oacc[db]);
         }
       }
     }
+    st ^= 1;
+    kt = kn;
   }
 
   const float lt = l + swap_halves(l);
@@ -181,9 +194,9 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdArgs a) {
 hipError_t launch_fwd(const FwdArgs& a, int head_dim, hipStream_t s) {
   dim3 grid((a.N + kBM - 1) / kBM, a.H, a.B);
   if (head_dim == 128)
-    hipLaunchKernelGGL(fwd_kernel<128>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(fwd_kernel<128>, grid, dim3(64 * kWaves), 0, s, a);
   else
-    hipLaunchKernelGGL(fwd_kernel<64>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(fwd_kernel<64>, grid, dim3(64 * kWaves), 0, s, a);
   return hipGetLastError();
 }
 

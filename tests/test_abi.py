@@ -44,8 +44,12 @@ def test_tokens_and_workspace():
     d3 = vc.make_desc(1, 24, 128, 256, 16, 45, 80)
     n = 57856
     assert vc.vc_jointattn_tokens(d3) == n
-    dd = 24 * n * 4
-    assert vc.vc_jointattn_bwd_workspace_bytes(d3) == ((dd + 255) // 256) * 256 + n * 24 * 128 * 4
+    npad = (n + 63) // 64 * 64
+    al = lambda x: (x + 255) // 256 * 256  # noqa: E731
+    rows = al(24 * npad * 4)
+    tiles = al(24 * (npad // 64) * 128 * 72 * 2)
+    assert vc.vc_jointattn_fwd_workspace_bytes(d3) == tiles
+    assert vc.vc_jointattn_bwd_workspace_bytes(d3) == 2 * rows + 3 * tiles
     assert vc.vc_jointattn_tokens(good_desc(head_dim=96)) == -3
     assert vc.vc_jointattn_bwd_workspace_bytes(good_desc(frames=0)) == 0
 
@@ -58,36 +62,41 @@ def test_tokens_and_workspace():
 def test_bad_descriptor(lib, kw, code):
     d = good_desc(**kw)
     p = 1 << 20  # never dereferenced: validation fails first
-    assert lib.vc_jointattn_fwd(ctypes.byref(d), p, p, p, None, None, p, p, None) == code
+    assert lib.vc_jointattn_fwd(ctypes.byref(d), p, p, p, None, None, p, p, p, 1 << 30, None) == code
     assert lib.vc_jointattn_bwd(ctypes.byref(d), p, p, p, p, p, p, None, None, p, p, p, p, 1 << 30, None) == code
 
 
 def test_null_descriptor_and_pointers(lib):
     p = 1 << 20
-    assert lib.vc_jointattn_fwd(None, p, p, p, None, None, p, p, None) == -1
+    assert lib.vc_jointattn_fwd(None, p, p, p, None, None, p, p, p, 1 << 30, None) == -1
     d = good_desc()
-    assert lib.vc_jointattn_fwd(ctypes.byref(d), None, p, p, None, None, p, p, None) == -1
-    assert lib.vc_jointattn_fwd(ctypes.byref(d), p, p, p, None, None, p, None, None) == -1
+    assert lib.vc_jointattn_fwd(ctypes.byref(d), None, p, p, None, None, p, p, p, 1 << 30, None) == -1
+    assert lib.vc_jointattn_fwd(ctypes.byref(d), p, p, p, None, None, p, None, p, 1 << 30, None) == -1
     assert lib.vc_jointattn_bwd(ctypes.byref(d), p, p, p, p, p, None, None, None, p, p, p, p, 1 << 30, None) == -1
-    assert lib.vc_jointattn_bwd_main(ctypes.byref(d), p, p, None, p, p, None, None, p, p, p, 1 << 30, None) == -1
+    assert lib.vc_jointattn_bwd_dkdv(ctypes.byref(d), p, p, None, p, None, None, p, p, p, 1 << 30, None) == -1
+    assert lib.vc_jointattn_bwd_dq(ctypes.byref(d), p, p, p, p, None, None, None, p, 1 << 30, None) == -1
 
 
 def test_misaligned_pointers(lib):
     d = good_desc()
     p = 1 << 20
-    assert lib.vc_jointattn_fwd(ctypes.byref(d), p + 2, p, p, None, None, p, p, None) == -4
-    assert lib.vc_jointattn_fwd(ctypes.byref(d), p, p, p, p + 2, None, p, p, None) == -4  # text_len int32
-    assert lib.vc_jointattn_bwd_prepare(ctypes.byref(d), p, p, p + 16, 1 << 30, None) == -4  # workspace 256
-    assert lib.vc_jointattn_bwd_finish(ctypes.byref(d), p + 8, p, 1 << 30, None) == -4
+    assert lib.vc_jointattn_fwd(ctypes.byref(d), p + 2, p, p, None, None, p, p, p, 1 << 30, None) == -4
+    assert lib.vc_jointattn_fwd(ctypes.byref(d), p, p, p, p + 2, None, p, p, p, 1 << 30, None) == -4  # text_len
+    assert lib.vc_jointattn_fwd(ctypes.byref(d), p, p, p, None, None, p, p, p + 16, 1 << 30, None) == -4  # ws 256
+    assert lib.vc_jointattn_bwd_prepare(ctypes.byref(d), p, p, p, p, p, p + 16, 1 << 30, None) == -4
+    assert lib.vc_jointattn_bwd_dq(ctypes.byref(d), p, p, p, p, None, None, p + 8, p, 1 << 30, None) == -4
 
 
 def test_workspace_checks(lib):
     d = good_desc()
     p = 1 << 20
     need = vc.vc_jointattn_bwd_workspace_bytes(d)
-    assert lib.vc_jointattn_bwd_prepare(ctypes.byref(d), p, p, None, need, None) == -5
-    assert lib.vc_jointattn_bwd_prepare(ctypes.byref(d), p, p, p, need - 1, None) == -5
+    assert lib.vc_jointattn_bwd_prepare(ctypes.byref(d), p, p, p, p, p, None, need, None) == -5
+    assert lib.vc_jointattn_bwd_prepare(ctypes.byref(d), p, p, p, p, p, p, need - 1, None) == -5
     assert lib.vc_jointattn_bwd(ctypes.byref(d), p, p, p, p, p, p, None, None, p, p, p, p, need - 4, None) == -5
+    fneed = vc.vc_jointattn_fwd_workspace_bytes(d)
+    assert lib.vc_jointattn_fwd(ctypes.byref(d), p, p, p, None, None, p, p, None, fneed, None) == -5
+    assert lib.vc_jointattn_fwd(ctypes.byref(d), p, p, p, None, None, p, p, p, fneed - 1, None) == -5
 
 
 def test_no_device_is_reported():
@@ -97,7 +106,7 @@ def test_no_device_is_reported():
     lib = vc._lib()
     d = good_desc()
     p = 1 << 20
-    assert lib.vc_jointattn_fwd(ctypes.byref(d), p, p, p, None, None, p, p, None) == -6
+    assert lib.vc_jointattn_fwd(ctypes.byref(d), p, p, p, None, None, p, p, p, 1 << 30, None) == -6
 
 
 def test_binding_fails_loudly_without_library(monkeypatch):
