@@ -4,7 +4,7 @@
 //   to whole tiles of 64 rows (padding rows get LSE = +inf so that their
 //   probabilities vanish, and D = 0); transposed token tiles of Q, dO and K
 //   come from the reformatting pass.
-// dK/dV (key-stationary): one workgroup of four waves owns 128 keys of one
+// dK/dV (key-stationary): one workgroup of eight waves owns 256 keys of one
 //   (sample, head), each wave 32, with K and V of its keys in registers and
 //   dK^T, dV^T accumulated in registers. It walks over all query tiles of 64,
 //   whose row-major Q and dO tiles, transposed Q^T and dO^T tiles, LSE and D
@@ -27,7 +27,8 @@
 namespace vcja {
 namespace {
 
-constexpr int kBKV = 128;  // keys per dK/dV workgroup
+constexpr int kDkdvWaves = 8;
+constexpr int kBKV = 32 * kDkdvWaves;  // keys per dK/dV workgroup
 constexpr int kBQ = kTileTok;  // queries per dK/dV tile
 constexpr int kDqWaves = 8;
 constexpr int kDqBM = 32 * kDqWaves;  // queries per dQ workgroup
@@ -74,18 +75,18 @@ __global__ __launch_bounds__(256) void bwd_prepare_kernel(const __bf16* __restri
 }
 
 template <int D>
-__global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(DkdvArgs a) {
-  constexpr int CPR = D / 8;                  // 16-byte chunks per row
-  constexpr int RT = kBQ * D * 2;             // row-major Q or dO tile bytes
+__global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a) {
+  constexpr int RT = RowTile<D>::kBytes;      // row-major Q or dO tile bytes
+  constexpr int RS = RowTile<D>::kStride;     // their row stride
   constexpr int TT = (int)tile_elems(D) * 2;  // transposed tile bytes
   constexpr int STAGE = 2 * RT + 2 * TT + 512;  // Q | dO | Q^T | dO^T | LSE*log2e[64] | D[64]
-  constexpr int RCOPIES = RT / 1024;
+  constexpr int RCOPIES = RowTile<D>::kCopies;
   constexpr int TCOPIES = TT / 1024;
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int w = tid >> 6;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index (uniform)
   const int l32 = lane & 31;
   const int hi = lane >> 5;
   const int h = blockIdx.y;
@@ -118,20 +119,16 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(DkdvArgs a) {
   // LSE (+inf) makes their probabilities zero.
   auto issue = [&](int qt, int st) {
     VC_LDS char* sq = (VC_LDS char*)smem + st * STAGE;
-    for (int idx = w; idx < RCOPIES; idx += 4) {
-      const int lin = idx * 64 + lane;
-      const int r = lin / CPR;
-      const int c = (lin % CPR) ^ (r & (CPR - 1));
-      const size_t goff = base + (size_t)min(qt * kBQ + r, N - 1) * tok + c * 8;
-      copy16_to_lds(a.q + goff, sq + idx * 1024);
-      copy16_to_lds(a.dout + goff, sq + RT + idx * 1024);
+    for (int idx = w; idx < RCOPIES; idx += kDkdvWaves) {
+      copy_row_tile<D>(a.q + base, tok, qt * kBQ, N, sq, idx, lane);
+      copy_row_tile<D>(a.dout + base, tok, qt * kBQ, N, sq + RT, idx, lane);
     }
     const size_t toff = (bh * a.ntile + qt) * tile_elems(D);
-    for (int idx = w; idx < TCOPIES; idx += 4) {
+    for (int idx = w; idx < TCOPIES; idx += kDkdvWaves) {
       copy16_to_lds(a.qt + toff + idx * 512 + lane * 8, sq + 2 * RT + idx * 1024);
       copy16_to_lds(a.dot + toff + idx * 512 + lane * 8, sq + 2 * RT + TT + idx * 1024);
     }
-    if (w == 3 && lane < 32) {
+    if (w == kDkdvWaves - 1 && lane < 32) {
       const float* src = (lane < 16 ? a.lse2 : a.dd) + bh * npad + qt * kBQ + 4 * (lane & 15);
       copy16_to_lds(src, sq + 2 * RT + 2 * TT);
     }
@@ -167,17 +164,17 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(DkdvArgs a) {
     const VC_LDS float* lse_lds = (const VC_LDS float*)(qt_lds + 2 * TT);
     const VC_LDS float* dd_lds = lse_lds + kBQ;
 
-#pragma unroll
+#pragma unroll 1
     for (int qb = 0; qb < kBQ / 32; ++qb) {
       f32x16 s = zero_f32x16(), dp = zero_f32x16();
 #pragma unroll
       for (int ks = 0; ks < D / 16; ++ks) {
-        const bf16x8 qa = *(const VC_LDS bf16x8*)(q_lds + swz_off<CPR>(qb * 32 + l32, 2 * ks + hi));
+        const bf16x8 qa = *(const VC_LDS bf16x8*)(q_lds + (qb * 32 + l32) * RS + (2 * ks + hi) * 16);
         s = mfma32(qa, kf[ks], s);
       }
 #pragma unroll
       for (int ks = 0; ks < D / 16; ++ks) {
-        const bf16x8 da = *(const VC_LDS bf16x8*)(do_lds + swz_off<CPR>(qb * 32 + l32, 2 * ks + hi));
+        const bf16x8 da = *(const VC_LDS bf16x8*)(do_lds + (qb * 32 + l32) * RS + (2 * ks + hi) * 16);
         dp = mfma32(da, vf[ks], dp);
       }
       // Register r holds query row qb*32 + 8*(r/4) + 4*hi + r%4: four runs of 4 rows.
@@ -228,17 +225,17 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(DkdvArgs a) {
 
 template <int D>
 __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
-  constexpr int CPR = D / 8;
-  constexpr int RT = kBN * D * 2;             // row-major K or V tile bytes
+  constexpr int RT = RowTile<D>::kBytes;      // row-major K or V tile bytes
+  constexpr int RS = RowTile<D>::kStride;
   constexpr int TT = (int)tile_elems(D) * 2;  // transposed K tile bytes
   constexpr int STAGE = 2 * RT + TT;          // K | V | K^T
-  constexpr int RCOPIES = RT / 1024;
+  constexpr int RCOPIES = RowTile<D>::kCopies;
   constexpr int TCOPIES = TT / 1024;
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int w = tid >> 6;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index (uniform)
   const int l32 = lane & 31;
   const int hi = lane >> 5;
   const int h = blockIdx.y;
@@ -275,12 +272,8 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
   auto issue = [&](int kt, int st) {
     VC_LDS char* sk = (VC_LDS char*)smem + st * STAGE;
     for (int idx = w; idx < RCOPIES; idx += kDqWaves) {
-      const int lin = idx * 64 + lane;
-      const int r = lin / CPR;
-      const int c = (lin % CPR) ^ (r & (CPR - 1));
-      const size_t goff = base + (size_t)min(kt * kBN + r, N - 1) * tok + c * 8;
-      copy16_to_lds(a.k + goff, sk + idx * 1024);
-      copy16_to_lds(a.v + goff, sk + RT + idx * 1024);
+      copy_row_tile<D>(a.k + base, tok, kt * kBN, N, sk, idx, lane);
+      copy_row_tile<D>(a.v + base, tok, kt * kBN, N, sk + RT, idx, lane);
     }
     const __bf16* tsrc = a.kt + (bh * a.ntile + kt) * tile_elems(D);
     for (int idx = w; idx < TCOPIES; idx += kDqWaves) copy16_to_lds(tsrc + idx * 512 + lane * 8, sk + 2 * RT + idx * 1024);
@@ -305,12 +298,12 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
       f32x16 s = zero_f32x16(), dp = zero_f32x16();
 #pragma unroll
       for (int ks = 0; ks < D / 16; ++ks) {
-        const bf16x8 ka = *(const VC_LDS bf16x8*)(k_lds + swz_off<CPR>(kb * 32 + l32, 2 * ks + hi));
+        const bf16x8 ka = *(const VC_LDS bf16x8*)(k_lds + (kb * 32 + l32) * RS + (2 * ks + hi) * 16);
         s = mfma32(ka, qf[ks], s);
       }
 #pragma unroll
       for (int ks = 0; ks < D / 16; ++ks) {
-        const bf16x8 va = *(const VC_LDS bf16x8*)(v_lds + swz_off<CPR>(kb * 32 + l32, 2 * ks + hi));
+        const bf16x8 va = *(const VC_LDS bf16x8*)(v_lds + (kb * 32 + l32) * RS + (2 * ks + hi) * 16);
         dp = mfma32(va, dof[ks], dp);
       }
       // Register r holds key k0 + kb*32 + 8*(r/4) + 4*hi + r%4 of this lane's query.
@@ -369,9 +362,9 @@ hipError_t launch_bwd_prepare(const __bf16* o, const float* lse, const __bf16* d
 hipError_t launch_bwd_dkdv(const DkdvArgs& a, int head_dim, hipStream_t s) {
   dim3 grid((a.N + kBKV - 1) / kBKV, a.H, a.B);
   if (head_dim == 128)
-    hipLaunchKernelGGL(bwd_dkdv_kernel<128>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(bwd_dkdv_kernel<128>, grid, dim3(64 * kDkdvWaves), 0, s, a);
   else
-    hipLaunchKernelGGL(bwd_dkdv_kernel<64>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(bwd_dkdv_kernel<64>, grid, dim3(64 * kDkdvWaves), 0, s, a);
   return hipGetLastError();
 }
 

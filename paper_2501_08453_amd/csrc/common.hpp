@@ -12,6 +12,7 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
+constexpr int kTileTok = 64;  // tokens per tile (keys or queries) in every kernel
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -75,16 +76,30 @@ __device__ __forceinline__ bf16x4 lds_read_tr(const VC_LDS void* p) {
   return __builtin_bit_cast(bf16x4, v);
 }
 
-// Row-major bf16 tile of rows x (8*CPR) in LDS, stored as 16-byte chunks with the chunk
-// index XOR-ed by the row (mod CPR) so that column-wise accesses spread over the banks.
-template <int CPR>
-__device__ __forceinline__ int swz_off(int row, int chunk) {
-  return row * (CPR * 16) + ((chunk ^ (row & (CPR - 1))) << 4);
-}
-// Byte offset of the 8-byte half-chunk holding columns [col, col+4), col a multiple of 4.
-template <int CPR>
-__device__ __forceinline__ int swz_off4(int row, int col) {
-  return swz_off<CPR>(row, col >> 3) + (((col >> 2) & 1) << 3);
+// Row-major bf16 tile of 64 token rows x D in LDS with one 16-byte pad chunk per row:
+// row stride D*2 + 16 bytes, so the 16 rows read by one quarter-wave at a common column
+// fall on distinct banks, and every k-step of an operand read is an immediate offset
+// from one per-lane base address.
+template <int D>
+struct RowTile {
+  static constexpr int kChunks = D / 8 + 1;             // 16-byte chunks per row, pad included
+  static constexpr int kStride = kChunks * 16;          // bytes per row
+  static constexpr int kBytes = kTileTok * kStride;     // bytes per tile
+  static constexpr int kCopies = kTileTok * kChunks / 64;  // 1 KiB wave copies per tile
+  static_assert(kTileTok * kChunks % 64 == 0, "tile must be whole wave copies");
+};
+
+// Issues wave copy `idx` of a row tile: rows row0 .. row0+63 of the [B, N, H, D] tensor
+// slice at src (row r at src + r*tok), rows clamped to N-1. The pad chunk of each row
+// repeats the row's last chunk.
+template <int D>
+__device__ __forceinline__ void copy_row_tile(const __bf16* src, size_t tok, int row0, int N, VC_LDS char* dst,
+                                              int idx, int lane) {
+  constexpr int CH = RowTile<D>::kChunks;
+  const int lin = idx * 64 + lane;
+  const int r = lin / CH;
+  const int c = min(lin - r * CH, CH - 2);
+  copy16_to_lds(src + (size_t)min(row0 + r, N - 1) * tok + c * 8, dst + idx * 1024);
 }
 
 // Value of lane l^32 (the other half of the wave).
@@ -97,7 +112,6 @@ __device__ __forceinline__ float swap_halves(float x) { return __shfl_xor(x, 32,
 // the second and third groups of 4 are swapped, so that the 8 tokens a lane supplies to
 // one 32x32x16 MFMA step - tokens 16s + 8*(t/4) + 4*hi + t%4, t = 0..7, the order in
 // which an accumulator column holds them - are 8 consecutive elements (one 16-byte read).
-constexpr int kTileTok = 64;
 constexpr int kTileRow = kTileTok + 8;  // elements per transposed tile row
 __host__ __device__ constexpr size_t tile_elems(int d) { return (size_t)d * kTileRow; }
 // Position of token t (0..63) inside a transposed tile row.

@@ -2,7 +2,7 @@
 //
 // One workgroup of eight waves owns 256 queries of one (sample, head); each
 // wave owns 32 of them, held in registers. Keys stream through LDS as
-// row-major tiles of 64 (16-byte chunks XOR-swizzled by row) and values as
+// row-major tiles of 64 (rows padded by 16 bytes) and values as
 // transposed token tiles (prepared by a reformatting pass), both copied
 // asynchronously global -> LDS into a two-stage ring so the next tile lands
 // while the current one is computed; one barrier per tile. All eight waves
@@ -29,18 +29,18 @@ constexpr float kRescaleSlack = 8.0f;  // log2 units
 
 template <int D>
 __global__ __launch_bounds__(64 * kWaves, 1) void fwd_kernel(FwdArgs a) {
-  constexpr int CPR = D / 8;                    // 16-byte chunks per key row
-  constexpr int KT = kBN * D * 2;               // K tile bytes
+  constexpr int KT = RowTile<D>::kBytes;        // K tile bytes
+  constexpr int KS = RowTile<D>::kStride;       // K row stride
   constexpr int VTB = (int)tile_elems(D) * 2;   // V^T tile bytes
   constexpr int STAGE = KT + VTB;
-  constexpr int KCOPIES = KT / 1024;            // 1 KiB wave copies per tile
+  constexpr int KCOPIES = RowTile<D>::kCopies;  // 1 KiB wave copies per tile
   constexpr int VCOPIES = VTB / 1024;
   static_assert(VTB % 1024 == 0, "transposed tile must be whole wave copies");
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int w = tid >> 6;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index (uniform)
   const int l32 = lane & 31;
   const int hi = lane >> 5;
   const int h = blockIdx.y;
@@ -78,12 +78,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void fwd_kernel(FwdArgs a) {
   // are masked.
   auto issue = [&](int kt, int st) {
     VC_LDS char* sk = (VC_LDS char*)smem + st * STAGE;
-    for (int idx = w; idx < KCOPIES; idx += kWaves) {
-      const int lin = idx * 64 + lane;
-      const int r = lin / CPR;
-      const int c = (lin % CPR) ^ (r & (CPR - 1));
-      copy16_to_lds(a.k + base + (size_t)min(kt * kBN + r, N - 1) * tok + c * 8, sk + idx * 1024);
-    }
+    for (int idx = w; idx < KCOPIES; idx += kWaves) copy_row_tile<D>(a.k + base, tok, kt * kBN, N, sk, idx, lane);
     const __bf16* vsrc = vt_bh + (size_t)kt * tile_elems(D);
     for (int idx = w; idx < VCOPIES; idx += kWaves) copy16_to_lds(vsrc + idx * 512 + lane * 8, sk + KT + idx * 1024);
   };
@@ -107,7 +102,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void fwd_kernel(FwdArgs a) {
       s[kb] = zero_f32x16();
 #pragma unroll
       for (int ks = 0; ks < D / 16; ++ks) {
-        const bf16x8 af = *(const VC_LDS bf16x8*)(ks_lds + swz_off<CPR>(kb * 32 + l32, 2 * ks + hi));
+        const bf16x8 af = *(const VC_LDS bf16x8*)(ks_lds + (kb * 32 + l32) * KS + (2 * ks + hi) * 16);
         s[kb] = mfma32(af, qf[ks], s[kb]);
       }
     }
