@@ -100,8 +100,8 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
 
   int tl = a.T;
   if (a.text_len) tl = min(max(a.text_len[b], 0), a.T);
-  bool valid = key < N && (key >= a.T || key < tl);
-  if (valid && a.key_mask) valid = a.key_mask[(size_t)b * N + key] != 0;
+  bool valid = (key < N) & ((key >= a.T) | (key < tl));
+  if (a.key_mask) valid = valid & (a.key_mask[(size_t)b * N + min(key, N - 1)] != 0);
 
   if (!__syncthreads_or(valid)) {
     // No valid key in this workgroup: its dK, dV are zero.
@@ -311,11 +311,11 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         float p = fast_exp2(fmaf(s[r], a.scale_log2, -lse2));
-        if (need_mask) {
+        if (need_mask) {  // branch-free per element; the mask byte is loaded unconditionally
           const int key = k0 + kb * 32 + acc_row(r, hi);
-          bool ok = key < N && (key >= a.T || key < tl);
-          if (ok && km) ok = km[key] != 0;
-          if (!ok) p = 0.0f;
+          const bool mv = km ? km[min(key, N - 1)] != 0 : true;
+          const bool ok = (key < N) & ((key >= a.T) | (key < tl)) & mv;
+          p = ok ? p : 0.0f;
         }
         ds[r] = p * (dp[r] - dd);
       }

@@ -102,8 +102,29 @@ __device__ __forceinline__ void copy_row_tile(const __bf16* src, size_t tok, int
   copy16_to_lds(src + (size_t)min(row0 + r, N - 1) * tok + c * 8, dst + idx * 1024);
 }
 
+// Scheduling hint for the basic block it ends: issue `lead` LDS reads, then `n` times
+// {1 matrix-core op, 1 LDS read, v vector-ALU ops}, so that independent vector work
+// (softmax, elementwise gradients) executes while the matrix core is busy.
+template <int lead, int n, int v>
+__device__ __forceinline__ void interleave_mfma_valu() {
+  __builtin_amdgcn_sched_group_barrier(0x100, lead, 0);
+#pragma unroll
+  for (int i = 0; i < n; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, v, 0);
+  }
+}
+
 // Value of lane l^32 (the other half of the wave).
 __device__ __forceinline__ float swap_halves(float x) { return __shfl_xor(x, 32, 64); }
+
+// max / sum of x over lanes l and l^32.
+__device__ __forceinline__ float halves_max(float x) { return fmaxf(x, swap_halves(x)); }
+__device__ __forceinline__ float halves_sum(float x) { return x + swap_halves(x); }
+
+// Keeps the compiler from moving any instruction across this point.
+__device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 
 // Transposed token tiles ("token-major" copies). A [B, N, H, D] tensor X is also kept as
 // blocked tiles XT[b][h][tile][d][kTileRow] of kTileTok tokens: row d of a tile holds

@@ -2,21 +2,25 @@
 //
 // One workgroup of eight waves owns 256 queries of one (sample, head); each
 // wave owns 32 of them, held in registers. Keys stream through LDS as
-// row-major tiles of 64 (rows padded by 16 bytes) and values as
-// transposed token tiles (prepared by a reformatting pass), both copied
-// asynchronously global -> LDS into a two-stage ring so the next tile lands
-// while the current one is computed; one barrier per tile. All eight waves
-// share each tile.
+// row-major tiles of 64 (rows padded by 16 bytes) and values as transposed
+// token tiles (prepared by a reformatting pass), both copied asynchronously
+// global -> LDS into a three-stage ring; one barrier per tile. All eight
+// waves share each tile.
 //
 // The wave computes the transposed score block S^T = K Q^T with 32x32x16 bf16
 // matrix-core steps, so each lane's accumulator column is one query: the
 // running maximum and sum of the online softmax are per-lane scalars that need
 // one exchange between the two wave halves per tile. P^T leaves the
 // accumulator already laid out as the B operand of O^T += V^T P^T, so
-// probabilities never go through LDS. The exponent base is only raised when a
-// tile's maximum exceeds it by more than 2^8, so the O^T rescale is rare
-// (probabilities stay below 256, exact in the bf16 exponent range). The
-// log-sum-exp is kept for the recomputing backward.
+// probabilities never go through LDS.
+//
+// Software pipeline inside each wave: at step j the matrix cores get the
+// scores of tile j+1 and then O += P_j V_j back to back, and the softmax of
+// tile j+1 runs on the vector ALUs while the P_j V_j products execute. The
+// exponent base is only raised when a tile's maximum exceeds it by more than
+// 2^8, so the O rescale (which must wait for the products in flight) is rare;
+// probabilities stay below 256. The log-sum-exp is kept for the recomputing
+// backward.
 #include "common.hpp"
 
 namespace vcja {
@@ -25,18 +29,131 @@ namespace {
 constexpr int kWaves = 8;
 constexpr int kBM = 32 * kWaves;  // queries per workgroup
 constexpr int kBN = kTileTok;     // keys per tile
+constexpr int kStages = 3;
 constexpr float kRescaleSlack = 8.0f;  // log2 units
 
 template <int D>
+struct FwdTile {
+  static constexpr int KT = RowTile<D>::kBytes;       // K tile bytes
+  static constexpr int KS = RowTile<D>::kStride;      // K row stride
+  static constexpr int VTB = (int)tile_elems(D) * 2;  // V^T tile bytes
+  static constexpr int STAGE = KT + VTB;
+};
+
+// S^T (keys x queries) of one 64-key tile: two 32x32 blocks, A = K rows from LDS,
+// B = this wave's Q^T fragments.
+template <int D>
+__device__ __forceinline__ void scores(const VC_LDS char* ks_lds, const bf16x8* qf, int l32, int hi, f32x16* s) {
+  constexpr int KS = FwdTile<D>::KS;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) s[kb] = zero_f32x16();
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      const bf16x8 af = *(const VC_LDS bf16x8*)(ks_lds + (kb * 32 + l32) * KS + (2 * ks + hi) * 16);
+      s[kb] = mfma32(af, qf[ks], s[kb]);
+    }
+  }
+}
+
+// O^T += V^T P^T for one 64-key tile. Operand element t of k-step st2 (lane half hi) is
+// key 16*st2 + 8*(t/4) + 4*hi + t%4, stored by the transposed tile as 8 consecutive
+// elements at position 16*st2 + 8*hi.
+template <int D>
+__device__ __forceinline__ void accumulate_pv(const VC_LDS char* vt_lds, const bf16x8* pb, int l32, int hi,
+                                              f32x16* oacc) {
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int st2 = 0; st2 < 2; ++st2)
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) {
+        const bf16x8 af =
+            *(const VC_LDS bf16x8*)(vt_lds + ((db * 32 + l32) * kTileRow + kb * 32 + 16 * st2 + 8 * hi) * 2);
+        oacc[db] = mfma32(af, pb[2 * kb + st2], oacc[db]);
+      }
+}
+
+struct KeyMask {
+  int N, T, tl;
+  const uint8_t* km;
+  __device__ __forceinline__ bool tile_needs_mask(int k0) const {
+    return km || (tl < T && k0 < T && k0 + kBN > tl) || (k0 + kBN > N);
+  }
+  // Sets scores of invalid keys to -inf. Branch-free per element: the validity test is
+  // plain arithmetic and the optional mask byte is loaded unconditionally (clamped index).
+  __device__ __forceinline__ void apply(f32x16* s, int k0, int hi) const {
+    if (km) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = k0 + kb * 32 + acc_row(r, hi);
+          const uint8_t mv = km[min(key, N - 1)];
+          const bool ok = (key < N) & ((key >= T) | (key < tl)) & (mv != 0);
+          s[kb][r] = ok ? s[kb][r] : -INFINITY;
+        }
+    } else {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = k0 + kb * 32 + acc_row(r, hi);
+          const bool ok = (key < N) & ((key >= T) | (key < tl));
+          s[kb][r] = ok ? s[kb][r] : -INFINITY;
+        }
+    }
+  }
+};
+
+// Online-softmax state update from a tile's scores (log2 units): new exponent base m,
+// the factor alpha rescaling what was accumulated against the old base (1 when the
+// base is not raised, 0 when there was nothing yet), and the base to subtract.
+__device__ __forceinline__ float softmax_base(const f32x16* s, float scale_log2, float& m, float& alpha,
+                                              bool& raise) {
+  float mx[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) mx[c] = fmaxf(s[c >> 1][8 * (c & 1)], s[c >> 1][8 * (c & 1) + 1]);
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int t = 2; t < 8; ++t) mx[c] = fmaxf(mx[c], s[c >> 1][8 * (c & 1) + t]);
+  const float tmax = halves_max(fmaxf(fmaxf(mx[0], mx[1]), fmaxf(mx[2], mx[3]))) * scale_log2;
+  raise = tmax > m + kRescaleSlack;
+  const float m_new = raise ? tmax : m;
+  alpha = raise ? fast_exp2(m - m_new) : 1.0f;
+  m = m_new;
+  return (m == -INFINITY) ? 0.0f : m;
+}
+
+// Probabilities of 8 scores (one PV operand) against base m_use, and their sum.
+__device__ __forceinline__ bf16x8 softmax_probs8(const f32x16& s, int half, float scale_log2, float m_use,
+                                                 float& sum) {
+  float p[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) p[t] = fast_exp2(fmaf(s[8 * half + t], scale_log2, -m_use));
+  sum += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
+  return to_bf16x8(p);
+}
+
+// V^T operand fragments of PV chunk c (key block c/2, k-step c%2) for every dim block.
+template <int D>
+__device__ __forceinline__ void load_vt_chunk(const VC_LDS char* vt_lds, int c, int l32, int hi, bf16x8* f) {
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+    f[db] = *(const VC_LDS bf16x8*)(vt_lds + ((db * 32 + l32) * kTileRow + (c >> 1) * 32 + 16 * (c & 1) + 8 * hi) * 2);
+}
+
+template <int D>
 __global__ __launch_bounds__(64 * kWaves, 1) void fwd_kernel(FwdArgs a) {
-  constexpr int KT = RowTile<D>::kBytes;        // K tile bytes
-  constexpr int KS = RowTile<D>::kStride;       // K row stride
-  constexpr int VTB = (int)tile_elems(D) * 2;   // V^T tile bytes
-  constexpr int STAGE = KT + VTB;
+  constexpr int KT = FwdTile<D>::KT;
+  constexpr int VTB = FwdTile<D>::VTB;
+  constexpr int STAGE = FwdTile<D>::STAGE;
   constexpr int KCOPIES = RowTile<D>::kCopies;  // 1 KiB wave copies per tile
   constexpr int VCOPIES = VTB / 1024;
   static_assert(VTB % 1024 == 0, "transposed tile must be whole wave copies");
-  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+  __shared__ __attribute__((aligned(1024))) char smem[kStages * STAGE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -59,19 +176,15 @@ __global__ __launch_bounds__(64 * kWaves, 1) void fwd_kernel(FwdArgs a) {
     for (int ks = 0; ks < D / 16; ++ks) qf[ks] = *(const bf16x8*)(qp + 16 * ks);
   }
 
-  f32x16 oacc[D / 32];
-#pragma unroll
-  for (int i = 0; i < D / 32; ++i) oacc[i] = zero_f32x16();
-  float m = -INFINITY;  // exponent base (scaled scores, log2 units)
-  float l = 0.0f;       // running sum of this lane's half
-
-  int tl = a.T;
-  if (a.text_len) tl = min(max(a.text_len[b], 0), a.T);
-  const uint8_t* km = a.key_mask ? a.key_mask + (size_t)b * N : nullptr;
+  KeyMask mask;
+  mask.N = N;
+  mask.T = a.T;
+  mask.tl = a.text_len ? min(max(a.text_len[b], 0), a.T) : a.T;
+  mask.km = a.key_mask ? a.key_mask + (size_t)b * N : nullptr;
   // A tile made only of padded text keys contributes nothing and is skipped.
   auto next_tile = [&](int kt) {
-    if (!km)
-      while (kt < a.ntile && kt * kBN >= tl && kt * kBN + kBN <= a.T) ++kt;
+    if (!mask.km)
+      while (kt < a.ntile && kt * kBN >= mask.tl && kt * kBN + kBN <= a.T) ++kt;
     return kt;
   };
   // Copies tile kt (K rows, V^T tile) into stage st. K rows past N repeat row N-1 and
@@ -82,92 +195,94 @@ __global__ __launch_bounds__(64 * kWaves, 1) void fwd_kernel(FwdArgs a) {
     const __bf16* vsrc = vt_bh + (size_t)kt * tile_elems(D);
     for (int idx = w; idx < VCOPIES; idx += kWaves) copy16_to_lds(vsrc + idx * 512 + lane * 8, sk + KT + idx * 1024);
   };
+  auto stage_ptr = [&](int st) { return (const VC_LDS char*)smem + st * STAGE; };
 
-  int kt = next_tile(0);
-  if (kt < a.ntile) issue(kt, 0);
-  int st = 0;
-  while (kt < a.ntile) {
-    const int kn = next_tile(kt + 1);
+  f32x16 oacc[D / 32];
+#pragma unroll
+  for (int i = 0; i < D / 32; ++i) oacc[i] = zero_f32x16();
+  float m = -INFINITY;  // exponent base (scaled scores, log2 units)
+  float l = 0.0f;       // running sum of this lane's half
+  bf16x8 pb[4];         // probabilities of the current tile as PV operands
+
+  int cur = next_tile(0);
+  if (cur < a.ntile) {
+    int nxt = next_tile(cur + 1);
+    issue(cur, 0);
+    if (nxt < a.ntile) issue(nxt, 1);
     wait_all_memory();
-    __syncthreads();  // stage st holds tile kt; every wave is done with stage st^1
-    if (kn < a.ntile) issue(kn, st ^ 1);
-    const VC_LDS char* ks_lds = (const VC_LDS char*)smem + st * STAGE;
-    const VC_LDS char* vt_lds = ks_lds + KT;
-    const int k0 = kt * kBN;
-
-    // S^T = K Q^T for two 32-key blocks.
-    f32x16 s[kBN / 32];
+    __syncthreads();
+    // Prologue: scores and softmax of the first tile.
+    {
+      f32x16 s[2];
+      scores<D>(stage_ptr(0), qf, l32, hi, s);
+      if (mask.tile_needs_mask(cur * kBN)) mask.apply(s, cur * kBN, hi);
+      float alpha;
+      bool raise;
+      const float m_use = softmax_base(s, a.scale_log2, m, alpha, raise);
 #pragma unroll
-    for (int kb = 0; kb < kBN / 32; ++kb) {
-      s[kb] = zero_f32x16();
-#pragma unroll
-      for (int ks = 0; ks < D / 16; ++ks) {
-        const bf16x8 af = *(const VC_LDS bf16x8*)(ks_lds + (kb * 32 + l32) * KS + (2 * ks + hi) * 16);
-        s[kb] = mfma32(af, qf[ks], s[kb]);
-      }
+      for (int c = 0; c < 4; ++c) pb[c] = softmax_probs8(s[c >> 1], c & 1, a.scale_log2, m_use, l);
     }
-
-    const bool need_mask = km || (tl < a.T && k0 < a.T && k0 + kBN > tl) || (k0 + kBN > N);
-    if (need_mask) {
+    int st = 0;  // stage of tile `cur`
+    // Pending rescale of O: probabilities computed against a raised base must only be
+    // added after O is brought to that base (done before the next P V, so that the
+    // P V products of the current tile and the softmax of the next share one branch-free
+    // stretch of code).
+    float alpha = 1.0f;
+    bool raise = false;
+    // Steady state: scores of `nxt` and P V of `cur` on the matrix cores, softmax of
+    // `nxt` on the vector ALUs.
+    while (nxt < a.ntile) {
+      const int nn = next_tile(nxt + 1);
+      const int st_nxt = st == kStages - 1 ? 0 : st + 1;
+      const int st_nn = st_nxt == kStages - 1 ? 0 : st_nxt + 1;
+      wait_all_memory();
+      __syncthreads();  // `nxt` landed; every wave is done with the stage `nn` will use
+      if (nn < a.ntile) issue(nn, st_nn);
+      if (__any(raise)) {
 #pragma unroll
-      for (int kb = 0; kb < kBN / 32; ++kb) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = k0 + kb * 32 + acc_row(r, hi);
-          bool ok = key < N && (key >= a.T || key < tl);
-          if (ok && km) ok = km[key] != 0;
-          if (!ok) s[kb][r] = -INFINITY;
-        }
+        for (int i = 0; i < D / 32; ++i) oacc[i] *= alpha;
       }
+      f32x16 s[2];
+      scores<D>(stage_ptr(st_nxt), qf, l32, hi, s);
+      if (mask.tile_needs_mask(nxt * kBN)) mask.apply(s, nxt * kBN, hi);
+      // P V of `cur` in four chunks of D/32 products; between them the vector ALUs do
+      // the softmax of `nxt`: first its new base, then one operand's probabilities per
+      // chunk. Fragments of the next chunk are read one chunk ahead.
+      const VC_LDS char* vt_lds = stage_ptr(st) + KT;
+      bf16x8 fa[D / 32], fb[D / 32];
+      load_vt_chunk<D>(vt_lds, 0, l32, hi, fa);
+      float m_use = 0.0f, psum = 0.0f;
+      bf16x8 pn[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        sched_fence();
+        if (c < 3) load_vt_chunk<D>(vt_lds, c + 1, l32, hi, fb);
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) oacc[db] = mfma32(fa[db], pb[c], oacc[db]);
+        if (c == 0)
+          m_use = softmax_base(s, a.scale_log2, m, alpha, raise);
+        else
+          pn[c - 1] = softmax_probs8(s[(c - 1) >> 1], (c - 1) & 1, a.scale_log2, m_use, psum);
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) fa[db] = fb[db];
+      }
+      sched_fence();
+      pn[3] = softmax_probs8(s[1], 1, a.scale_log2, m_use, psum);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) pb[c] = pn[c];
+      l = fmaf(l, alpha, psum);
+      st = st_nxt;
+      cur = nxt;
+      nxt = nn;
     }
-
-    // Online softmax; this lane's column is query qi.
-    float mx = -INFINITY;
-#pragma unroll
-    for (int kb = 0; kb < kBN / 32; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
-    mx = fmaxf(mx, swap_halves(mx)) * a.scale_log2;
-    const bool raise = mx > m + kRescaleSlack;
     if (__any(raise)) {
-      const float m_new = raise ? mx : m;
-      const float alpha = raise ? fast_exp2(m - m_new) : 1.0f;  // 0 when m was -inf
-      m = m_new;
-      l *= alpha;
 #pragma unroll
       for (int i = 0; i < D / 32; ++i) oacc[i] *= alpha;
     }
-    const float m_use = (m == -INFINITY) ? 0.0f : m;
-
-    float p[kBN / 32][16];
-#pragma unroll
-    for (int kb = 0; kb < kBN / 32; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        p[kb][r] = fast_exp2(fmaf(s[kb][r], a.scale_log2, -m_use));
-        l += p[kb][r];
-      }
-
-    // O^T += V^T P^T. Operand element t of k-step st2 (lane half hi) is key
-    // 16*st2 + 8*(t/4) + 4*hi + t%4, which the transposed tile stores as 8 consecutive
-    // elements at position 16*st2 + 8*hi.
-#pragma unroll
-    for (int kb = 0; kb < kBN / 32; ++kb) {
-#pragma unroll
-      for (int st2 = 0; st2 < 2; ++st2) {
-        const bf16x8 pb = to_bf16x8(&p[kb][8 * st2]);
-#pragma unroll
-        for (int db = 0; db < D / 32; ++db) {
-          const bf16x8 af = *(const VC_LDS bf16x8*)(vt_lds + ((db * 32 + l32) * kTileRow + kb * 32 + 16 * st2 + 8 * hi) * 2);
-          oacc[db] = mfma32(af, pb, oacc[db]);
-        }
-      }
-    }
-    st ^= 1;
-    kt = kn;
+    accumulate_pv<D>(stage_ptr(st) + KT, pb, l32, hi, oacc);
   }
 
-  const float lt = l + swap_halves(l);
+  const float lt = halves_sum(l);
   const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
   if (qi < N) {
     __bf16* op = a.o + base + (size_t)qi * tok;
