@@ -44,7 +44,12 @@ def flops(w, text_len):
 
 
 def cpu_baseline(w, g, text_len, target_s):
-    """Time the fp64 oracle on a bounded block of query rows of head 0, sample 0."""
+    """Time the fp64 oracle on a bounded block of query rows of head 0, sample 0.
+
+    Rows are doubled from 1024 until one run takes a quarter of the target, then the
+    block is scaled to about the target (at most every row of the head). The oracle's
+    thread pool uses every host core it may run on.
+    """
     import torch
     import oracle.ref_attention as ora
     N, D = w.tokens, w.head_dim
@@ -52,15 +57,20 @@ def cpu_baseline(w, g, text_len, target_s):
     valid = ora.key_validity(1, N, w.text_slot, None if text_len is None else text_len[:1])
     c = ora.default_scale(D)
     nkv = int(valid[0].sum())
-    rows = 64
-    t0 = time.perf_counter()
-    ora.rowblock_fwd_bwd(qh, kh, vh, doh, valid[0], c, 0, 0, np.arange(rows))
-    t = time.perf_counter() - t0
-    if t < target_s / 3:
-        rows = int(min(N, max(rows, rows * (target_s / max(t, 1e-3)) * 0.9)))
+
+    def run(rows):
         t0 = time.perf_counter()
         ora.rowblock_fwd_bwd(qh, kh, vh, doh, valid[0], c, 0, 0, np.arange(rows))
-        t = time.perf_counter() - t0
+        return time.perf_counter() - t0
+
+    rows = min(N, 1024)
+    t = run(rows)
+    while t < target_s / 4 and rows < N:
+        rows = min(N, rows * 2)
+        t = run(rows)
+    if t < target_s * 0.75 and rows < N:
+        rows = int(min(N, rows * target_s / max(t, 1e-3)))
+        t = run(rows)
     fl = 12.0 * rows * nkv * D
     return {
         "value": fl / t / 1e12,
@@ -73,6 +83,33 @@ def cpu_baseline(w, g, text_len, target_s):
     }
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_bwd_dkdv_long720p.json")
+KERNEL_SOURCES = ["paper_2501_08453_amd/csrc/bwd.hip", "paper_2501_08453_amd/csrc/common.hpp"]
+
+
+def kernel_source_digest() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def traffic_record():
+    """HBM bytes per launch of the dK/dV kernel measured with hardware counters (FETCH_SIZE
+    + WRITE_SIZE, scaled by a plain copy of known size), if the record matches the current
+    kernel sources; None otherwise."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_digest") != kernel_source_digest():
+        return None
+    return rec.get("bytes_per_launch")
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -81,6 +118,9 @@ def main(argv=None):
     ap.add_argument("--workload", type=int, default=W.HEADLINE, choices=sorted(W.WORKLOADS))
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the oracle timing")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="after the run, copy this many MiB device-to-device with one plain copy "
+                         "kernel (reference for hardware byte counters)")
     args = ap.parse_args(argv)
     if args.gpus != 1:
         print("bench.py measures one GPU only: the path shards by heads with no communication inside "
@@ -184,9 +224,19 @@ def main(argv=None):
             "algorithmic_flops_per_launch": dkdv_flops,
         },
     }
+    tr = traffic_record()
+    if tr is not None:
+        line["roofline"]["traffic"] = tr
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, g, text_len, args.cpu_seconds)
     print(json.dumps(line), flush=True)
+    if args.copy_calibration_mib:
+        n = args.copy_calibration_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
     return 0
 
 

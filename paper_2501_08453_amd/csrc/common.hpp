@@ -123,6 +123,11 @@ __device__ __forceinline__ float swap_halves(float x) { return __shfl_xor(x, 32,
 __device__ __forceinline__ float halves_max(float x) { return fmaxf(x, swap_halves(x)); }
 __device__ __forceinline__ float halves_sum(float x) { return x + swap_halves(x); }
 
+// Wave issue priority: raised around matrix-core phases so that a wave's MFMAs issue back
+// to back while the other wave on the SIMD fills the gaps with vector work.
+__device__ __forceinline__ void prio_high() { __builtin_amdgcn_s_setprio(1); }
+__device__ __forceinline__ void prio_low() { __builtin_amdgcn_s_setprio(0); }
+
 // Keeps the compiler from moving any instruction across this point.
 __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 
