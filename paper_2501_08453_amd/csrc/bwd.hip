@@ -309,16 +309,18 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
       // Register r holds key k0 + kb*32 + 8*(r/4) + 4*hi + r%4 of this lane's query.
       float ds[16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float p = fast_exp2(fmaf(s[r], a.scale_log2, -lse2));
-        if (need_mask) {  // branch-free per element; the mask byte is loaded unconditionally
+      for (int r = 0; r < 16; ++r) ds[r] = fast_exp2(fmaf(s[r], a.scale_log2, -lse2));
+      if (need_mask) {  // branch-free per element; the mask byte is loaded unconditionally
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
           const int key = k0 + kb * 32 + acc_row(r, hi);
-          const bool mv = km ? km[min(key, N - 1)] != 0 : true;
-          const bool ok = (key < N) & ((key >= a.T) | (key < tl)) & mv;
-          p = ok ? p : 0.0f;
+          const uint8_t mv = km ? km[min(key, N - 1)] : (uint8_t)1;
+          const bool ok = (key < N) & ((key >= a.T) | (key < tl)) & (mv != 0);
+          ds[r] = ok ? ds[r] : 0.0f;
         }
-        ds[r] = p * (dp[r] - dd);
       }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) ds[r] = ds[r] * (dp[r] - dd);
 #pragma unroll
       for (int st2 = 0; st2 < 2; ++st2) {
         const bf16x8 sb = to_bf16x8(&ds[8 * st2]);

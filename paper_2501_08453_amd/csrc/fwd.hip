@@ -4,8 +4,10 @@
 // wave owns 32 of them, held in registers. Keys stream through LDS as
 // row-major tiles of 64 (rows padded by 16 bytes) and values as transposed
 // token tiles (prepared by a reformatting pass), both copied asynchronously
-// global -> LDS into a three-stage ring; one barrier per tile. All eight
-// waves share each tile.
+// global -> LDS. Scores read the K tile one step before the P V products read
+// the V^T tile of the same keys, so each has its own two-slot ring (tile t in
+// slot t mod 2): the copies of step j+1 are in flight during step j, and one
+// barrier per tile suffices. All eight waves share each tile.
 //
 // The wave computes the transposed score block S^T = K Q^T with 32x32x16 bf16
 // matrix-core steps, so each lane's accumulator column is one query: the
@@ -27,9 +29,9 @@ namespace vcja {
 namespace {
 
 constexpr int kWaves = 8;
+constexpr int kWavesPerSimd = 2;  // register budget: two waves share each SIMD
 constexpr int kBM = 32 * kWaves;  // queries per workgroup
 constexpr int kBN = kTileTok;     // keys per tile
-constexpr int kStages = 3;
 constexpr float kRescaleSlack = 8.0f;  // log2 units
 
 template <int D>
@@ -37,7 +39,7 @@ struct FwdTile {
   static constexpr int KT = RowTile<D>::kBytes;       // K tile bytes
   static constexpr int KS = RowTile<D>::kStride;      // K row stride
   static constexpr int VTB = (int)tile_elems(D) * 2;  // V^T tile bytes
-  static constexpr int STAGE = KT + VTB;
+  static constexpr int LDS = 2 * KT + 2 * VTB;        // K ring | V^T ring
 };
 
 // S^T (keys x queries) of one 64-key tile: two 32x32 blocks, A = K rows from LDS,
@@ -146,14 +148,13 @@ __device__ __forceinline__ void load_vt_chunk(const VC_LDS char* vt_lds, int c, 
 }
 
 template <int D>
-__global__ __launch_bounds__(64 * kWaves, 1) void fwd_kernel(FwdArgs a) {
+__global__ __launch_bounds__(64 * kWaves, kWavesPerSimd * 4 / kWaves) void fwd_kernel(FwdArgs a) {
   constexpr int KT = FwdTile<D>::KT;
   constexpr int VTB = FwdTile<D>::VTB;
-  constexpr int STAGE = FwdTile<D>::STAGE;
   constexpr int KCOPIES = RowTile<D>::kCopies;  // 1 KiB wave copies per tile
   constexpr int VCOPIES = VTB / 1024;
   static_assert(VTB % 1024 == 0, "transposed tile must be whole wave copies");
-  __shared__ __attribute__((aligned(1024))) char smem[kStages * STAGE];
+  __shared__ __attribute__((aligned(1024))) char smem[FwdTile<D>::LDS];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -187,15 +188,19 @@ __global__ __launch_bounds__(64 * kWaves, 1) void fwd_kernel(FwdArgs a) {
       while (kt < a.ntile && kt * kBN >= mask.tl && kt * kBN + kBN <= a.T) ++kt;
     return kt;
   };
-  // Copies tile kt (K rows, V^T tile) into stage st. K rows past N repeat row N-1 and
-  // are masked.
-  auto issue = [&](int kt, int st) {
-    VC_LDS char* sk = (VC_LDS char*)smem + st * STAGE;
-    for (int idx = w; idx < KCOPIES; idx += kWaves) copy_row_tile<D>(a.k + base, tok, kt * kBN, N, sk, idx, lane);
-    const __bf16* vsrc = vt_bh + (size_t)kt * tile_elems(D);
-    for (int idx = w; idx < VCOPIES; idx += kWaves) copy16_to_lds(vsrc + idx * 512 + lane * 8, sk + KT + idx * 1024);
+  // Copies tile kt's K rows (rows past N repeat row N-1 and are masked) or V^T tile into
+  // ring slot `slot`.
+  auto issue_k = [&](int kt, int slot) {
+    VC_LDS char* dst = (VC_LDS char*)smem + slot * KT;
+    for (int idx = w; idx < KCOPIES; idx += kWaves) copy_row_tile<D>(a.k + base, tok, kt * kBN, N, dst, idx, lane);
   };
-  auto stage_ptr = [&](int st) { return (const VC_LDS char*)smem + st * STAGE; };
+  auto issue_v = [&](int kt, int slot) {
+    VC_LDS char* dst = (VC_LDS char*)smem + 2 * KT + slot * VTB;
+    const __bf16* vsrc = vt_bh + (size_t)kt * tile_elems(D);
+    for (int idx = w; idx < VCOPIES; idx += kWaves) copy16_to_lds(vsrc + idx * 512 + lane * 8, dst + idx * 1024);
+  };
+  auto k_slot = [&](int slot) { return (const VC_LDS char*)smem + slot * KT; };
+  auto v_slot = [&](int slot) { return (const VC_LDS char*)smem + 2 * KT + slot * VTB; };
 
   f32x16 oacc[D / 32];
 #pragma unroll
@@ -207,14 +212,16 @@ __global__ __launch_bounds__(64 * kWaves, 1) void fwd_kernel(FwdArgs a) {
   int cur = next_tile(0);
   if (cur < a.ntile) {
     int nxt = next_tile(cur + 1);
-    issue(cur, 0);
-    if (nxt < a.ntile) issue(nxt, 1);
+    int par = 0;  // ring slot of tile `cur`
+    issue_k(cur, 0);
+    issue_v(cur, 0);
+    if (nxt < a.ntile) issue_k(nxt, 1);
     wait_all_memory();
     __syncthreads();
     // Prologue: scores and softmax of the first tile.
     {
       f32x16 s[2];
-      scores<D>(stage_ptr(0), qf, l32, hi, s);
+      scores<D>(k_slot(0), qf, l32, hi, s);
       if (mask.tile_needs_mask(cur * kBN)) mask.apply(s, cur * kBN, hi);
       float alpha;
       bool raise;
@@ -222,7 +229,6 @@ __global__ __launch_bounds__(64 * kWaves, 1) void fwd_kernel(FwdArgs a) {
 #pragma unroll
       for (int c = 0; c < 4; ++c) pb[c] = softmax_probs8(s[c >> 1], c & 1, a.scale_log2, m_use, l);
     }
-    int st = 0;  // stage of tile `cur`
     // Pending rescale of O: probabilities computed against a raised base must only be
     // added after O is brought to that base (done before the next P V, so that the
     // P V products of the current tile and the softmax of the next share one branch-free
@@ -233,22 +239,22 @@ __global__ __launch_bounds__(64 * kWaves, 1) void fwd_kernel(FwdArgs a) {
     // `nxt` on the vector ALUs.
     while (nxt < a.ntile) {
       const int nn = next_tile(nxt + 1);
-      const int st_nxt = st == kStages - 1 ? 0 : st + 1;
-      const int st_nn = st_nxt == kStages - 1 ? 0 : st_nxt + 1;
       wait_all_memory();
-      __syncthreads();  // `nxt` landed; every wave is done with the stage `nn` will use
-      if (nn < a.ntile) issue(nn, st_nn);
+      __syncthreads();  // K of `nxt` and V^T of `cur` landed; K of `cur` and V^T of the
+                        // previous tile are no longer read by any wave
+      if (nn < a.ntile) issue_k(nn, par);
+      issue_v(nxt, par ^ 1);
       if (__any(raise)) {
 #pragma unroll
         for (int i = 0; i < D / 32; ++i) oacc[i] *= alpha;
       }
       f32x16 s[2];
-      scores<D>(stage_ptr(st_nxt), qf, l32, hi, s);
+      scores<D>(k_slot(par ^ 1), qf, l32, hi, s);
       if (mask.tile_needs_mask(nxt * kBN)) mask.apply(s, nxt * kBN, hi);
       // P V of `cur` in four chunks of D/32 products; between them the vector ALUs do
       // the softmax of `nxt`: first its new base, then one operand's probabilities per
       // chunk. Fragments of the next chunk are read one chunk ahead.
-      const VC_LDS char* vt_lds = stage_ptr(st) + KT;
+      const VC_LDS char* vt_lds = v_slot(par);
       bf16x8 fa[D / 32], fb[D / 32];
       load_vt_chunk<D>(vt_lds, 0, l32, hi, fa);
       float m_use = 0.0f, psum = 0.0f;
@@ -271,7 +277,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void fwd_kernel(FwdArgs a) {
 #pragma unroll
       for (int c = 0; c < 4; ++c) pb[c] = pn[c];
       l = fmaf(l, alpha, psum);
-      st = st_nxt;
+      par ^= 1;
       cur = nxt;
       nxt = nn;
     }
@@ -279,7 +285,9 @@ __global__ __launch_bounds__(64 * kWaves, 1) void fwd_kernel(FwdArgs a) {
 #pragma unroll
       for (int i = 0; i < D / 32; ++i) oacc[i] *= alpha;
     }
-    accumulate_pv<D>(stage_ptr(st) + KT, pb, l32, hi, oacc);
+    wait_all_memory();
+    __syncthreads();  // V^T of the last tile landed
+    accumulate_pv<D>(v_slot(par), pb, l32, hi, oacc);
   }
 
   const float lt = halves_sum(l);
