@@ -18,11 +18,16 @@
 //
 // Software pipeline inside each wave: at step j the matrix cores get the
 // scores of tile j+1 and then O += P_j V_j back to back, and the softmax of
-// tile j+1 runs on the vector ALUs while the P_j V_j products execute. The
-// exponent base is only raised when a tile's maximum exceeds it by more than
-// 2^8, so the O rescale (which must wait for the products in flight) is rare;
-// probabilities stay below 256. The log-sum-exp is kept for the recomputing
-// backward.
+// tile j+1 runs on the vector ALUs while the P_j V_j products execute.
+//
+// The online softmax keeps a per-query exponent base m and does not take the
+// tile maximum on the common path: probabilities are formed against the
+// current base and summed (in the bf16 precision the P V product uses, two at
+// a time); only when a lane's sum of 32 probabilities exceeds 2^13 (or is not
+// finite, e.g. before the first valid key) does the wave raise the base to the
+// tile maximum and recompute the tile. Probabilities therefore stay below
+// 2^13 and the O rescale, which must wait for the products in flight, is rare.
+// The log-sum-exp is kept for the recomputing backward.
 #include "common.hpp"
 
 namespace vcja {
@@ -32,7 +37,7 @@ constexpr int kWaves = 8;
 constexpr int kWavesPerSimd = 2;  // register budget: two waves share each SIMD
 constexpr int kBM = 32 * kWaves;  // queries per workgroup
 constexpr int kBN = kTileTok;     // keys per tile
-constexpr float kRescaleSlack = 8.0f;  // log2 units
+constexpr float kSumLimit = 8192.0f;  // largest accepted sum of a lane's 32 probabilities
 
 template <int D>
 struct FwdTile {
@@ -109,11 +114,31 @@ struct KeyMask {
   }
 };
 
-// Online-softmax state update from a tile's scores (log2 units): new exponent base m,
-// the factor alpha rescaling what was accumulated against the old base (1 when the
-// base is not raised, 0 when there was nothing yet), and the base to subtract.
-__device__ __forceinline__ float softmax_base(const f32x16* s, float scale_log2, float& m, float& alpha,
-                                              bool& raise) {
+// Sum of eight bf16 values (two at a time, fp32 accumulation) added to sum.
+__device__ __forceinline__ float add_bf16x8(bf16x8 x, float sum) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) sum = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{x[2 * i], x[2 * i + 1]}, ones, sum, false);
+  return sum;
+}
+
+// Probabilities 2^(s c log2(e) - m) of 8 scores (one PV operand), rounded to bf16, with
+// their sum added to sum.
+__device__ __forceinline__ bf16x8 probs8(const f32x16& s, int half, float scale_log2, float m, float& sum) {
+  float p[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) p[t] = fast_exp2(fmaf(s[8 * half + t], scale_log2, -m));
+  const bf16x8 r = to_bf16x8(p);
+  sum = add_bf16x8(r, sum);
+  return r;
+}
+
+// Rare path: raises the exponent base of the queries (lanes) that need it to the tile
+// maximum (both wave halves agree), recomputes the tile's probabilities and their sum,
+// and returns the factor that rescales what was accumulated against the old base.
+__device__ __forceinline__ float raise_base(const f32x16* s, float scale_log2, bool need, float& m, bf16x8* pb,
+                                            float& psum) {
   float mx[4];
 #pragma unroll
   for (int c = 0; c < 4; ++c) mx[c] = fmaxf(s[c >> 1][8 * (c & 1)], s[c >> 1][8 * (c & 1) + 1]);
@@ -122,21 +147,15 @@ __device__ __forceinline__ float softmax_base(const f32x16* s, float scale_log2,
 #pragma unroll
     for (int t = 2; t < 8; ++t) mx[c] = fmaxf(mx[c], s[c >> 1][8 * (c & 1) + t]);
   const float tmax = halves_max(fmaxf(fmaxf(mx[0], mx[1]), fmaxf(mx[2], mx[3]))) * scale_log2;
-  raise = tmax > m + kRescaleSlack;
-  const float m_new = raise ? tmax : m;
-  alpha = raise ? fast_exp2(m - m_new) : 1.0f;
+  need = need | (swap_halves(need ? 1.0f : 0.0f) != 0.0f);
+  const float m_new = need ? fmaxf(m, tmax) : m;
+  const float alpha = m_new == m ? 1.0f : fast_exp2(m - m_new);
   m = m_new;
-  return (m == -INFINITY) ? 0.0f : m;
-}
-
-// Probabilities of 8 scores (one PV operand) against base m_use, and their sum.
-__device__ __forceinline__ bf16x8 softmax_probs8(const f32x16& s, int half, float scale_log2, float m_use,
-                                                 float& sum) {
-  float p[8];
+  const float m_use = m == -INFINITY ? 0.0f : m;  // no valid key yet: all probabilities 0
+  psum = 0.0f;
 #pragma unroll
-  for (int t = 0; t < 8; ++t) p[t] = fast_exp2(fmaf(s[8 * half + t], scale_log2, -m_use));
-  sum += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
-  return to_bf16x8(p);
+  for (int c = 0; c < 4; ++c) pb[c] = probs8(s[c >> 1], c & 1, scale_log2, m_use, psum);
+  return alpha;
 }
 
 // V^T operand fragments of PV chunk c (key block c/2, k-step c%2) for every dim block.
@@ -223,11 +242,7 @@ __global__ __launch_bounds__(64 * kWaves, kWavesPerSimd * 4 / kWaves) void fwd_k
       f32x16 s[2];
       scores<D>(k_slot(0), qf, l32, hi, s);
       if (mask.tile_needs_mask(cur * kBN)) mask.apply(s, cur * kBN, hi);
-      float alpha;
-      bool raise;
-      const float m_use = softmax_base(s, a.scale_log2, m, alpha, raise);
-#pragma unroll
-      for (int c = 0; c < 4; ++c) pb[c] = softmax_probs8(s[c >> 1], c & 1, a.scale_log2, m_use, l);
+      raise_base(s, a.scale_log2, true, m, pb, l);
     }
     // Pending rescale of O: probabilities computed against a raised base must only be
     // added after O is brought to that base (done before the next P V, so that the
@@ -257,7 +272,7 @@ __global__ __launch_bounds__(64 * kWaves, kWavesPerSimd * 4 / kWaves) void fwd_k
       const VC_LDS char* vt_lds = v_slot(par);
       bf16x8 fa[D / 32], fb[D / 32];
       load_vt_chunk<D>(vt_lds, 0, l32, hi, fa);
-      float m_use = 0.0f, psum = 0.0f;
+      float psum = 0.0f;
       bf16x8 pn[4];
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
@@ -265,15 +280,15 @@ __global__ __launch_bounds__(64 * kWaves, kWavesPerSimd * 4 / kWaves) void fwd_k
         if (c < 3) load_vt_chunk<D>(vt_lds, c + 1, l32, hi, fb);
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) oacc[db] = mfma32(fa[db], pb[c], oacc[db]);
-        if (c == 0)
-          m_use = softmax_base(s, a.scale_log2, m, alpha, raise);
-        else
-          pn[c - 1] = softmax_probs8(s[(c - 1) >> 1], (c - 1) & 1, a.scale_log2, m_use, psum);
+        pn[c] = probs8(s[c >> 1], c & 1, a.scale_log2, m, psum);
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) fa[db] = fb[db];
       }
       sched_fence();
-      pn[3] = softmax_probs8(s[1], 1, a.scale_log2, m_use, psum);
+      const bool need = !(psum <= kSumLimit);
+      alpha = 1.0f;
+      raise = __any(need);
+      if (raise) alpha = raise_base(s, a.scale_log2, need, m, pn, psum);
 #pragma unroll
       for (int c = 0; c < 4; ++c) pb[c] = pn[c];
       l = fmaf(l, alpha, psum);
