@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define VC_JOINTATTN_ABI_VERSION 1
+#define VC_JOINTATTN_ABI_VERSION 2
 
 typedef enum vc_status {
   VC_OK = 0,
@@ -154,6 +154,40 @@ vc_status vc_jointattn_bwd_dq(const vc_jointattn_desc* desc,
                               const void* dout,
                               const int32_t* text_len, const uint8_t* key_mask,
                               void* dq,
+                              void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Temporal attention branch (Sec. III-B: besides the full-sequence branch the
+ * block attends over the video sequence [B, F, L, ...] regrouped as
+ * [B*L, F, ...], L = Hp*Wp tokens per frame; the branch outputs are added).
+ * It is computed in place on the joint layout: the video token of frame f at
+ * spatial position l, row T + f*L + l, attends to the F rows T + f'*L + l,
+ * f' = 0..F-1, with key_mask (NULL = none) applied to those keys; a query with
+ * no valid key gets O = 0, LSE = -inf. Text rows take no part: their o, dq, dk,
+ * dv are written as 0 and their lse as -inf. text_len is not used. Requires
+ * F <= 32 (VC_ERR_SHAPE otherwise). Tensor conventions as above; results are
+ * deterministic and no atomics are used.
+ * ------------------------------------------------------------------------- */
+
+/* Temporal forward: writes o [B,N,H,D] bf16 and lse [B,H,N] fp32 (natural log).
+ * Needs no workspace. */
+vc_status vc_temporalattn_fwd(const vc_jointattn_desc* desc,
+                              const void* q, const void* k, const void* v,
+                              const uint8_t* key_mask,
+                              void* o, float* lse, void* stream);
+
+/* Bytes of device workspace the temporal backward needs: per row fp32 D and
+ * LSE*log2(e) ([B,H,Npad]). 0 for an invalid descriptor. Host only. */
+size_t vc_temporalattn_bwd_workspace_bytes(const vc_jointattn_desc* desc);
+
+/* Temporal backward: dq, dk, dv from q, k, v, the temporal forward's o and lse
+ * and dout. `workspace`: caller-owned device memory of at least
+ * vc_temporalattn_bwd_workspace_bytes(desc) bytes, 256-byte aligned. */
+vc_status vc_temporalattn_bwd(const vc_jointattn_desc* desc,
+                              const void* q, const void* k, const void* v,
+                              const void* o, const float* lse, const void* dout,
+                              const uint8_t* key_mask,
+                              void* dq, void* dk, void* dv,
                               void* workspace, size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus

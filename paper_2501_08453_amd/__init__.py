@@ -57,6 +57,9 @@ _SIGS = {
     "vc_jointattn_bwd_prepare": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "vc_jointattn_bwd_dkdv": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "vc_jointattn_bwd_dq": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "vc_temporalattn_fwd": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P]),
+    "vc_temporalattn_bwd_workspace_bytes": (ctypes.c_size_t, [_DP]),
+    "vc_temporalattn_bwd": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
 }
 
 
@@ -171,6 +174,20 @@ def vc_jointattn_bwd_dq(desc, q, k, v, dout, text_len, key_mask, dq, workspace, 
           _ptr(text_len), _ptr(key_mask), _ptr(dq), _ptr(workspace), int(workspace_bytes), _stream(stream))
 
 
+def vc_temporalattn_fwd(desc, q, k, v, key_mask, o, lse, stream=None):
+    _call("vc_temporalattn_fwd", ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(key_mask), _ptr(o), _ptr(lse),
+          _stream(stream))
+
+
+def vc_temporalattn_bwd_workspace_bytes(desc) -> int:
+    return _lib().vc_temporalattn_bwd_workspace_bytes(ctypes.byref(desc))
+
+
+def vc_temporalattn_bwd(desc, q, k, v, o, lse, dout, key_mask, dq, dk, dv, workspace, workspace_bytes, stream=None):
+    _call("vc_temporalattn_bwd", ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _ptr(dout),
+          _ptr(key_mask), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(workspace), int(workspace_bytes), _stream(stream))
+
+
 # --------------------------------------------------------------------------
 # Tensor-level helpers: allocate outputs with torch, then call the library.
 # --------------------------------------------------------------------------
@@ -235,6 +252,40 @@ def bwd(q, k, v, o, lse, dout, desc, text_len=None, key_mask=None, ws=None, dq=N
     dk = torch.empty_like(q) if dk is None else dk
     dv = torch.empty_like(q) if dv is None else dv
     vc_jointattn_bwd(desc, q, k, v, o, lse, dout, text_len, key_mask, dq, dk, dv, ws, ws.numel())
+    return dq, dk, dv
+
+
+def _check_branch_inputs(desc, tensors, key_mask=None):
+    import torch
+    q = tensors[0][1]
+    B, N, H, D = q.shape
+    for n, t in tensors:
+        _check_tensor(n, t, (B, N, H, D), torch.bfloat16)
+    if vc_jointattn_tokens(desc) != N:
+        raise ValueError("descriptor gives N=%d, tensors have N=%d" % (vc_jointattn_tokens(desc), N))
+    if key_mask is not None:
+        _check_tensor("key_mask", key_mask, (B, N), torch.uint8)
+    return B, N, H, D
+
+
+def temporal_fwd(q, k, v, desc, key_mask=None, out=None, lse=None):
+    """Temporal branch (o, lse) for bf16 q, k, v of shape [B, N, H, D] (joint layout)."""
+    import torch
+    B, N, H, D = _check_branch_inputs(desc, (("q", q), ("k", k), ("v", v)), key_mask)
+    o = torch.empty_like(q) if out is None else out
+    lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device) if lse is None else lse
+    vc_temporalattn_fwd(desc, q, k, v, key_mask, o, lse)
+    return o, lse
+
+
+def temporal_bwd(q, k, v, o, lse, dout, desc, key_mask=None, ws=None):
+    """Temporal branch (dq, dk, dv)."""
+    import torch
+    B, N, H, D = _check_branch_inputs(desc, (("q", q), ("k", k), ("v", v), ("o", o), ("dout", dout)), key_mask)
+    _check_tensor("lse", lse, (B, H, N), torch.float32)
+    ws = _workspace(vc_temporalattn_bwd_workspace_bytes(desc), q.device) if ws is None else ws
+    dq, dk, dv = (torch.empty_like(q) for _ in range(3))
+    vc_temporalattn_bwd(desc, q, k, v, o, lse, dout, key_mask, dq, dk, dv, ws, ws.numel())
     return dq, dk, dv
 
 

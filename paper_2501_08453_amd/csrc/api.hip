@@ -98,6 +98,24 @@ vc_status check_ws(void* ws, size_t have, size_t need) {
 }
 
 inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+constexpr int kMaxTemporalFrames = 32;
+
+// Temporal branch arguments common to the forward and the backward.
+vcja::TemporalArgs temporal_args(const vc_jointattn_desc* d, int64_t n) {
+  vcja::TemporalArgs a{};
+  a.B = d->batch;
+  a.H = d->heads;
+  a.N = (int)n;
+  a.T = d->text_slot;
+  a.F = d->frames;
+  a.L = d->grid_h * d->grid_w;
+  a.G = 32 / d->frames;
+  a.npad = ntiles(n) * vcja::kTileTok;
+  a.scale = d->softmax_scale > 0.0f ? d->softmax_scale : 1.0f / sqrtf((float)d->head_dim);
+  a.scale_log2 = a.scale * vcja::kLog2e;
+  return a;
+}
 inline const __bf16* bf(const void* p) { return static_cast<const __bf16*>(p); }
 
 }  // namespace
@@ -275,6 +293,71 @@ vc_status vc_jointattn_bwd(const vc_jointattn_desc* desc, const void* q, const v
                                   stream)) != VC_OK)
     return st;
   return vc_jointattn_bwd_dq(desc, q, k, v, dout, text_len, key_mask, dq, workspace, workspace_bytes, stream);
+}
+
+vc_status vc_temporalattn_fwd(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
+                              const uint8_t* key_mask, void* o, float* lse, void* stream) {
+  int64_t n = 0;
+  vc_status st = check_desc(desc, &n);
+  if (st != VC_OK) return st;
+  if (desc->frames > kMaxTemporalFrames) return VC_ERR_SHAPE;
+  if (!q || !k || !v || !o || !lse) return VC_ERR_NULL;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse)) return VC_ERR_ALIGN;
+  if ((st = check_device()) != VC_OK) return st;
+  vcja::TemporalArgs a = temporal_args(desc, n);
+  a.q = bf(q);
+  a.k = bf(k);
+  a.v = bf(v);
+  a.key_mask = key_mask;
+  a.o = static_cast<__bf16*>(o);
+  a.lse = lse;
+  hipStream_t s = as_stream(stream);
+  if (vcja::launch_text_rows(a.o, nullptr, nullptr, lse, a.B, a.H, a.N, a.T, desc->head_dim, s) != hipSuccess ||
+      vcja::launch_temporal_fwd(a, desc->head_dim, s) != hipSuccess)
+    return VC_ERR_HIP;
+  return VC_OK;
+}
+
+size_t vc_temporalattn_bwd_workspace_bytes(const vc_jointattn_desc* desc) {
+  int64_t n = 0;
+  if (check_desc(desc, &n) != VC_OK) return 0;
+  return 2 * rows_bytes(desc, n);
+}
+
+vc_status vc_temporalattn_bwd(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
+                              const void* o, const float* lse, const void* dout, const uint8_t* key_mask, void* dq,
+                              void* dk, void* dv, void* workspace, size_t workspace_bytes, void* stream) {
+  int64_t n = 0;
+  vc_status st = check_desc(desc, &n);
+  if (st != VC_OK) return st;
+  if (desc->frames > kMaxTemporalFrames) return VC_ERR_SHAPE;
+  if (!q || !k || !v || !o || !lse || !dout || !dq || !dk || !dv) return VC_ERR_NULL;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse) || !aligned16(dout) ||
+      !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
+    return VC_ERR_ALIGN;
+  const size_t rb = rows_bytes(desc, n);
+  if ((st = check_ws(workspace, workspace_bytes, 2 * rb)) != VC_OK) return st;
+  if ((st = check_device()) != VC_OK) return st;
+  vcja::TemporalArgs a = temporal_args(desc, n);
+  float* dd = static_cast<float*>(workspace);
+  float* lse2 = reinterpret_cast<float*>(static_cast<char*>(workspace) + rb);
+  a.q = bf(q);
+  a.k = bf(k);
+  a.v = bf(v);
+  a.dout = bf(dout);
+  a.key_mask = key_mask;
+  a.lse2 = lse2;
+  a.dd = dd;
+  a.o = static_cast<__bf16*>(dq);
+  a.dk = static_cast<__bf16*>(dk);
+  a.dv = static_cast<__bf16*>(dv);
+  hipStream_t s = as_stream(stream);
+  if (vcja::launch_bwd_prepare(bf(o), lse, bf(dout), dd, lse2, a.B, a.H, a.N, a.npad, desc->head_dim, s) !=
+          hipSuccess ||
+      vcja::launch_text_rows(a.o, a.dk, a.dv, nullptr, a.B, a.H, a.N, a.T, desc->head_dim, s) != hipSuccess ||
+      vcja::launch_temporal_bwd(a, desc->head_dim, s) != hipSuccess)
+    return VC_ERR_HIP;
+  return VC_OK;
 }
 
 }  // extern "C"

@@ -194,6 +194,25 @@ struct DqArgs {
   float scale_log2;
 };
 
+// Temporal branch: attention of each spatial position across the F frames. Video token
+// (f, l) sits at T + f*L + l of the joint sequence; one wave handles G = 32/F positions.
+struct TemporalArgs {
+  const __bf16* q;
+  const __bf16* k;
+  const __bf16* v;
+  const __bf16* dout;   // backward only
+  const uint8_t* key_mask;
+  const float* lse2;    // backward: LSE * log2(e) per token, +inf where there is none, [B, H, Npad]
+  const float* dd;      // backward: D = rowsum(dO o O), [B, H, Npad]
+  __bf16* o;            // forward output / backward dQ
+  float* lse;           // forward output
+  __bf16* dk;           // backward
+  __bf16* dv;           // backward
+  int B, H, N, T, F, L, G, npad;
+  float scale;
+  float scale_log2;
+};
+
 }  // namespace vcja
 
 // Host-side launchers (defined in the .hip kernel files).
@@ -205,4 +224,10 @@ hipError_t launch_bwd_prepare(const __bf16* o, const float* lse, const __bf16* d
                               int H, int N, int Npad, int head_dim, hipStream_t s);
 hipError_t launch_bwd_dkdv(const DkdvArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_bwd_dq(const DqArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_temporal_fwd(const TemporalArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_temporal_bwd(const TemporalArgs& a, int head_dim, hipStream_t s);
+// Rows [0, T) of up to three [B, N, H, D] tensors set to zero and, if lse is given, their
+// LSE ([B, H, N]) to -inf.
+hipError_t launch_text_rows(__bf16* x0, __bf16* x1, __bf16* x2, float* lse, int B, int H, int N, int T, int head_dim,
+                            hipStream_t s);
 }  // namespace vcja

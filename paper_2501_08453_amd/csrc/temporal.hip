@@ -1,0 +1,324 @@
+// Temporal attention branch for gfx950: each spatial position attends across the
+// frames (the [B*L, F, ...] regrouping of the multimodal diffusion block), read in
+// place from the joint [B, N, H, D] layout where video token (f, l) is row T + f*L + l.
+//
+// Sequences are short (F <= 32), so one wave packs G = floor(32/F) consecutive
+// positions of one (sample, head) into the 32 slots of a 32x32x16 matrix-core
+// block: slot s holds frame s % F of position l0 + s / F; slots past G*F are
+// padding. Every operand is read straight from global memory (no LDS): rows of
+// Q, K (and dO, V in the backward) as 16-byte chunks, and the transposed operands
+// (V^T, K^T, Q^T, dO^T) gathered element by element in the key order the
+// accumulator layout produces. A key is valid for a query if it belongs to the
+// same position (same group of F slots) and key_mask keeps it. The work is small
+// and bound by memory traffic.
+#include "common.hpp"
+
+namespace vcja {
+namespace {
+
+constexpr int kSlots = 32;
+constexpr int kWavesPerBlock = 4;
+
+// Token row of slot s in the block starting at position l0 (clamped into range for
+// padding slots, whose probabilities are zero).
+struct SlotMap {
+  int T, F, L, G, l0;
+  __device__ __forceinline__ bool ok(int s) const { return s < G * F && l0 + s / F < L; }
+  __device__ __forceinline__ int token(int s) const {
+    const int g = s / F;
+    const int f = s - g * F;
+    const int l = l0 + g < L ? l0 + g : l0;
+    return T + f * L + l;
+  }
+};
+
+// Slot held by register r of a lane of half hi in a 32x32 accumulator (row index).
+__device__ __forceinline__ int acc_slot(int r, int hi) { return acc_row(r, hi); }
+
+// Slot of operand element t of k-step st for a lane of half hi: the order in which the
+// accumulator rows of 8 consecutive registers are numbered.
+__device__ __forceinline__ int op_slot(int st, int t, int hi) { return 16 * st + 8 * (t >> 2) + 4 * hi + (t & 3); }
+
+template <int D>
+__global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_fwd_kernel(TemporalArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int l32 = lane & 31;
+  const int hi = lane >> 5;
+  const int blk = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+  const int h = blockIdx.y;
+  const int b = blockIdx.z;
+  SlotMap sm{a.T, a.F, a.L, a.G, blk * a.G};
+  if (sm.l0 >= a.L) return;  // whole wave
+  const size_t tok = (size_t)a.H * D;
+  const size_t base = (size_t)b * a.N * tok + (size_t)h * D;
+
+  // This lane's slot as query (B operand column) and as key (A operand row).
+  const int s = l32;
+  const int g = s / a.F;
+  const bool q_ok = sm.ok(s);
+  const int n = sm.token(s);
+  bf16x8 qf[D / 16], kf[D / 16];
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) {
+    qf[ks] = *(const bf16x8*)(a.q + base + (size_t)n * tok + 16 * ks + 8 * hi);
+    kf[ks] = *(const bf16x8*)(a.k + base + (size_t)n * tok + 16 * ks + 8 * hi);
+  }
+  // S^T = K Q^T: lane column = query slot s, register r = key slot acc_slot(r, hi).
+  f32x16 sacc = zero_f32x16();
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) sacc = mfma32(kf[ks], qf[ks], sacc);
+
+  // Keys of the same group (position) only; padding and masked keys excluded.
+  const int lo = g * a.F;
+  const uint8_t* km = a.key_mask ? a.key_mask + (size_t)b * a.N : nullptr;
+  float mx = -INFINITY;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int j = acc_slot(r, hi);
+    bool ok = q_ok & (j >= lo) & (j < lo + a.F);
+    if (km) ok = ok & (km[sm.token(j)] != 0);
+    sacc[r] = ok ? sacc[r] : -INFINITY;
+    mx = fmaxf(mx, sacc[r]);
+  }
+  mx = halves_max(mx);
+  const float m2 = mx == -INFINITY ? 0.0f : mx * a.scale_log2;
+  float p[16], sum = 0.0f;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    p[r] = fast_exp2(fmaf(sacc[r], a.scale_log2, -m2));
+    sum += p[r];
+  }
+  sum = halves_sum(sum);
+
+  // O^T = V^T P^T over the 32 key slots (two k-steps of 16).
+  bf16x8 pb[2];
+  pb[0] = to_bf16x8(&p[0]);
+  pb[1] = to_bf16x8(&p[8]);
+  size_t vrow[2][8];
+#pragma unroll
+  for (int st = 0; st < 2; ++st)
+#pragma unroll
+    for (int t = 0; t < 8; ++t) vrow[st][t] = base + (size_t)sm.token(op_slot(st, t, hi)) * tok;
+  const float inv = sum > 0.0f ? 1.0f / sum : 0.0f;
+  __bf16* op = a.o + base + (size_t)n * tok;
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db) {
+    f32x16 oacc = zero_f32x16();
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+      bf16x8 vt;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) vt[t] = a.v[vrow[st][t] + db * 32 + l32];
+      oacc = mfma32(vt, pb[st], oacc);
+    }
+    if (q_ok) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        bf16x4 o4 = {(__bf16)(oacc[4 * j + 0] * inv), (__bf16)(oacc[4 * j + 1] * inv),
+                     (__bf16)(oacc[4 * j + 2] * inv), (__bf16)(oacc[4 * j + 3] * inv)};
+        *(bf16x4*)(op + db * 32 + 8 * j + 4 * hi) = o4;
+      }
+    }
+  }
+  if (q_ok && hi == 0)
+    a.lse[((size_t)b * a.H + h) * a.N + n] = sum > 0.0f ? (m2 + __log2f(sum)) * kLn2 : -INFINITY;
+}
+
+// Backward. LSE*log2(e) and D = rowsum(dO o O) per token come from the preparation pass
+// ([B, H, npad], +inf / 0 where a row has no key). Two orientations of the same block:
+// lane = query (S^T, dP^T, dS^T) gives dQ^T = c K^T dS^T; lane = key (S, dP, dS) gives
+// dV^T = dO^T P and dK^T = c Q^T dS. The transposed A operands are gathered in the slot
+// order the accumulator layout produces.
+template <int D>
+__global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_bwd_kernel(TemporalArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int l32 = lane & 31;
+  const int hi = lane >> 5;
+  const int blk = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+  const int h = blockIdx.y;
+  const int b = blockIdx.z;
+  SlotMap sm{a.T, a.F, a.L, a.G, blk * a.G};
+  if (sm.l0 >= a.L) return;  // whole wave
+  const size_t tok = (size_t)a.H * D;
+  const size_t base = (size_t)b * a.N * tok + (size_t)h * D;
+  const size_t rbase = ((size_t)b * a.H + h) * a.npad;
+  const uint8_t* km = a.key_mask ? a.key_mask + (size_t)b * a.N : nullptr;
+
+  const int s = l32;  // this lane's slot (query in one orientation, key in the other)
+  const int lo = (s / a.F) * a.F;
+  const bool s_ok = sm.ok(s);
+  const int n = sm.token(s);
+  bf16x8 qf[D / 16], kf[D / 16], vf[D / 16], dof[D / 16];
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) {
+    const size_t off = base + (size_t)n * tok + 16 * ks + 8 * hi;
+    qf[ks] = *(const bf16x8*)(a.q + off);
+    kf[ks] = *(const bf16x8*)(a.k + off);
+    vf[ks] = *(const bf16x8*)(a.v + off);
+    dof[ks] = *(const bf16x8*)(a.dout + off);
+  }
+  // Rows of the slots an operand element t of k-step st refers to (gathers).
+  size_t grow[2][8];
+#pragma unroll
+  for (int st = 0; st < 2; ++st)
+#pragma unroll
+    for (int t = 0; t < 8; ++t) grow[st][t] = base + (size_t)sm.token(op_slot(st, t, hi)) * tok;
+
+  // ---- lane = query: dQ ----
+  {
+    f32x16 sacc = zero_f32x16(), pacc = zero_f32x16();
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) {
+      sacc = mfma32(kf[ks], qf[ks], sacc);
+      pacc = mfma32(vf[ks], dof[ks], pacc);
+    }
+    const float l2 = s_ok ? a.lse2[rbase + n] : INFINITY;
+    const float d = s_ok ? a.dd[rbase + n] : 0.0f;
+    float ds[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int j = acc_slot(r, hi);
+      bool ok = s_ok & (j >= lo) & (j < lo + a.F);
+      if (km) ok = ok & (km[sm.token(j)] != 0);
+      const float p = ok ? fast_exp2(fmaf(sacc[r], a.scale_log2, -l2)) : 0.0f;
+      ds[r] = p * (pacc[r] - d);
+    }
+    bf16x8 sb[2];
+    sb[0] = to_bf16x8(&ds[0]);
+    sb[1] = to_bf16x8(&ds[8]);
+    __bf16* dqp = a.o + base + (size_t)n * tok;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+      f32x16 acc = zero_f32x16();
+#pragma unroll
+      for (int st = 0; st < 2; ++st) {
+        bf16x8 kt;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) kt[t] = a.k[grow[st][t] + db * 32 + l32];
+        acc = mfma32(kt, sb[st], acc);
+      }
+      if (s_ok) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          bf16x4 o4 = {(__bf16)(acc[4 * j + 0] * a.scale), (__bf16)(acc[4 * j + 1] * a.scale),
+                       (__bf16)(acc[4 * j + 2] * a.scale), (__bf16)(acc[4 * j + 3] * a.scale)};
+          *(bf16x4*)(dqp + db * 32 + 8 * j + 4 * hi) = o4;
+        }
+      }
+    }
+  }
+  // ---- lane = key: dK, dV ----
+  {
+    f32x16 sacc = zero_f32x16(), pacc = zero_f32x16();
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) {
+      sacc = mfma32(qf[ks], kf[ks], sacc);
+      pacc = mfma32(dof[ks], vf[ks], pacc);
+    }
+    bool k_ok = s_ok;
+    if (km) k_ok = k_ok & (km[n] != 0);
+    float p[16], ds[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int i = acc_slot(r, hi);  // query slot
+      const bool ok = k_ok & (i >= lo) & (i < lo + a.F) & sm.ok(i);
+      const int ni = sm.token(i);
+      const float l2 = a.lse2[rbase + ni];
+      const float d = a.dd[rbase + ni];
+      p[r] = ok ? fast_exp2(fmaf(sacc[r], a.scale_log2, -l2)) : 0.0f;
+      ds[r] = p[r] * (pacc[r] - d);
+    }
+    bf16x8 pb[2], sb[2];
+    pb[0] = to_bf16x8(&p[0]);
+    pb[1] = to_bf16x8(&p[8]);
+    sb[0] = to_bf16x8(&ds[0]);
+    sb[1] = to_bf16x8(&ds[8]);
+    __bf16* dkp = a.dk + base + (size_t)n * tok;
+    __bf16* dvp = a.dv + base + (size_t)n * tok;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+      f32x16 vacc = zero_f32x16(), kacc = zero_f32x16();
+#pragma unroll
+      for (int st = 0; st < 2; ++st) {
+        bf16x8 dot, qt;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+          dot[t] = a.dout[grow[st][t] + db * 32 + l32];
+          qt[t] = a.q[grow[st][t] + db * 32 + l32];
+        }
+        vacc = mfma32(dot, pb[st], vacc);
+        kacc = mfma32(qt, sb[st], kacc);
+      }
+      if (s_ok) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          bf16x4 v4 = {(__bf16)vacc[4 * j + 0], (__bf16)vacc[4 * j + 1], (__bf16)vacc[4 * j + 2],
+                       (__bf16)vacc[4 * j + 3]};
+          bf16x4 k4 = {(__bf16)(kacc[4 * j + 0] * a.scale), (__bf16)(kacc[4 * j + 1] * a.scale),
+                       (__bf16)(kacc[4 * j + 2] * a.scale), (__bf16)(kacc[4 * j + 3] * a.scale)};
+          *(bf16x4*)(dvp + db * 32 + 8 * j + 4 * hi) = v4;
+          *(bf16x4*)(dkp + db * 32 + 8 * j + 4 * hi) = k4;
+        }
+      }
+    }
+  }
+}
+
+// Zero rows [0, T) of up to three tensors and set their LSE to -inf.
+template <int D>
+__global__ __launch_bounds__(256) void text_rows_kernel(__bf16* x0, __bf16* x1, __bf16* x2, float* lse, int B, int H,
+                                                        int N, int T) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;  // one 16-byte chunk
+  constexpr int CPR = D / 8;
+  const size_t rows = (size_t)B * T * H;
+  if (i < rows * CPR) {
+    const size_t row = i / CPR;
+    const int c = (int)(i % CPR);
+    const int hh = (int)(row % H);
+    const size_t bt = row / H;
+    const int t = (int)(bt % T);
+    const int b = (int)(bt / T);
+    const size_t off = (((size_t)b * N + t) * H + hh) * D + c * 8;
+    const bf16x8 z = zero_bf16x8();
+    if (x0) *(bf16x8*)(x0 + off) = z;
+    if (x1) *(bf16x8*)(x1 + off) = z;
+    if (x2) *(bf16x8*)(x2 + off) = z;
+    if (lse && c == 0) lse[((size_t)b * H + hh) * N + t] = -INFINITY;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_temporal_fwd(const TemporalArgs& a, int head_dim, hipStream_t s) {
+  const int nblk = (a.L + a.G - 1) / a.G;
+  dim3 grid((nblk + kWavesPerBlock - 1) / kWavesPerBlock, a.H, a.B);
+  if (head_dim == 128)
+    hipLaunchKernelGGL(temporal_fwd_kernel<128>, grid, dim3(64 * kWavesPerBlock), 0, s, a);
+  else
+    hipLaunchKernelGGL(temporal_fwd_kernel<64>, grid, dim3(64 * kWavesPerBlock), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_temporal_bwd(const TemporalArgs& a, int head_dim, hipStream_t s) {
+  const int nblk = (a.L + a.G - 1) / a.G;
+  dim3 grid((nblk + kWavesPerBlock - 1) / kWavesPerBlock, a.H, a.B);
+  if (head_dim == 128)
+    hipLaunchKernelGGL(temporal_bwd_kernel<128>, grid, dim3(64 * kWavesPerBlock), 0, s, a);
+  else
+    hipLaunchKernelGGL(temporal_bwd_kernel<64>, grid, dim3(64 * kWavesPerBlock), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_text_rows(__bf16* x0, __bf16* x1, __bf16* x2, float* lse, int B, int H, int N, int T, int head_dim,
+                            hipStream_t s) {
+  if (T <= 0) return hipSuccess;
+  const size_t chunks = (size_t)B * T * H * (head_dim / 8);
+  dim3 grid((unsigned)((chunks + 255) / 256));
+  if (head_dim == 128)
+    hipLaunchKernelGGL(text_rows_kernel<128>, grid, dim3(256), 0, s, x0, x1, x2, lse, B, H, N, T);
+  else
+    hipLaunchKernelGGL(text_rows_kernel<64>, grid, dim3(256), 0, s, x0, x1, x2, lse, B, H, N, T);
+  return hipGetLastError();
+}
+
+}  // namespace vcja

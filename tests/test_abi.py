@@ -32,7 +32,7 @@ def test_exports_every_declared_function(lib):
 
 
 def test_version_and_strings(lib):
-    assert vc.vc_jointattn_abi_version() == 1
+    assert vc.vc_jointattn_abi_version() == 2
     for code in vc.STATUS:
         assert isinstance(vc.vc_status_string(code), str) and vc.vc_status_string(code)
     assert vc.vc_status_string(12345) == "unknown status"
@@ -114,3 +114,22 @@ def test_binding_fails_loudly_without_library(monkeypatch):
     monkeypatch.setattr(vc, "LIB_PATH", "/nonexistent/libvc_jointattn.so")
     with pytest.raises(RuntimeError, match="not built"):
         vc.vc_jointattn_abi_version()
+
+
+def test_temporal_argument_errors(lib):
+    p = 1 << 20
+    d = good_desc()
+    # more than 32 frames is outside what the temporal kernel packs
+    big = good_desc(frames=33, grid_h=2, grid_w=2)
+    assert lib.vc_temporalattn_fwd(ctypes.byref(big), p, p, p, None, p, p, None) == -2
+    assert lib.vc_temporalattn_bwd(ctypes.byref(big), p, p, p, p, p, p, None, p, p, p, p, 1 << 30, None) == -2
+    assert lib.vc_temporalattn_fwd(ctypes.byref(good_desc(head_dim=48)), p, p, p, None, p, p, None) == -3
+    assert lib.vc_temporalattn_fwd(ctypes.byref(d), p, None, p, None, p, p, None) == -1
+    assert lib.vc_temporalattn_fwd(ctypes.byref(d), p, p, p, None, p + 4, p, None) == -4
+    need = vc.vc_temporalattn_bwd_workspace_bytes(d)
+    npad = (16 + 2 * 64 + 63) // 64 * 64
+    assert need == 2 * ((2 * npad * 4 + 255) // 256 * 256)
+    assert lib.vc_temporalattn_bwd(ctypes.byref(d), p, p, p, p, p, p, None, p, p, p, None, need, None) == -5
+    assert lib.vc_temporalattn_bwd(ctypes.byref(d), p, p, p, p, p, p, None, p, p, p, p, need - 1, None) == -5
+    assert lib.vc_temporalattn_bwd(ctypes.byref(d), p, p, p, p, p, None, None, p, p, p, p, need, None) == -1
+    assert vc.vc_temporalattn_bwd_workspace_bytes(good_desc(batch=0)) == 0

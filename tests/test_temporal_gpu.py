@@ -1,0 +1,139 @@
+"""GPU parity of the temporal attention branch (through the C ABI) against the
+fp64 branch oracle.
+
+Small shapes are compared on every element, for frame counts that pack one to
+sixteen positions into a matrix-core block, position counts that leave a
+ragged last block, both head dims, with and without text and a key mask. The
+workload shapes are compared on sampled spatial positions (positions are
+independent in this branch, so the oracle runs on the sliced positions only)
+plus identities that hold on every head at full size. Tolerances as for the
+joint path (parity_util).
+"""
+import numpy as np
+import pytest
+
+import oracle.ref_branches as orb
+import workloads as W
+from parity_util import assert_close, bf16_values, log, to_gpu_bf16
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(desc, g, key_mask=None):
+    import torch
+    import paper_2501_08453_amd as vc
+    o, lse = vc.temporal_fwd(g["q"], g["k"], g["v"], desc, key_mask)
+    dq, dk, dv = vc.temporal_bwd(g["q"], g["k"], g["v"], o, lse, g["do"], desc, key_mask)
+    torch.cuda.synchronize()
+    out = {n: bf16_values(t) for n, t in (("o", o), ("dq", dq), ("dk", dk), ("dv", dv))}
+    out["lse"] = lse.cpu().numpy().astype(np.float64)
+    return out
+
+
+def _inputs(w, seed):
+    x = W.make_inputs(w, seed=seed)
+    g = {n: to_gpu_bf16(x[n]) for n in ("q", "k", "v", "do")}
+    h = {n: bf16_values(g[n]) for n in g}
+    return g, h
+
+
+SMALL = [
+    # (name, batch, heads, head_dim, text_slot, frames, grid_h, grid_w, masked)
+    ("F1", 1, 2, 64, 4, 1, 3, 5, False),
+    ("F2-ragged", 2, 3, 128, 16, 2, 7, 3, False),
+    ("F5-ragged", 1, 2, 64, 0, 5, 4, 5, True),
+    ("F8", 2, 2, 128, 8, 8, 4, 4, False),
+    ("F16-ragged", 1, 3, 128, 12, 16, 3, 3, True),
+    ("F32", 1, 2, 64, 4, 32, 2, 3, False),
+    ("F13-d128", 1, 1, 128, 0, 13, 5, 3, True),
+]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+def test_temporal_small_all_elements(case):
+    import torch
+    import paper_2501_08453_amd as vc
+    name, B, H, D, T, F, gh, gw, masked = case
+    w = W.custom(B, H, D, T, F, gh, gw, name=name)
+    log("temporal case", name, w.shape)
+    g, h = _inputs(w, seed=500 + len(name))
+    km_np = None
+    km = None
+    if masked:
+        km_np = W.random_key_mask(w, seed=77, keep=0.8)
+        km = torch.from_numpy(km_np).to("cuda")
+    desc = vc.desc_for(w)
+    out = _run(desc, g, km)
+    o, lse = orb.temporal_forward(h["q"], h["k"], h["v"], T, F, km_np)
+    dq, dk, dv = orb.temporal_backward(h["q"], h["k"], h["v"], h["do"], T, F, km_np, lse=lse)
+    assert_close("O", out["o"], o)
+    assert_close("LSE", out["lse"], lse)
+    assert_close("dQ", out["dq"], dq)
+    assert_close("dK", out["dk"], dk)
+    assert_close("dV", out["dv"], dv)
+    # text rows exactly zero / -inf
+    assert np.all(out["o"][:, :T] == 0) and np.all(np.isneginf(out["lse"][:, :, :T]))
+    assert np.all(out["dq"][:, :T] == 0) and np.all(out["dk"][:, :T] == 0) and np.all(out["dv"][:, :T] == 0)
+
+
+@pytest.mark.parametrize("wid", [2, 3, 4, 5])
+def test_temporal_workloads_sampled(wid):
+    import torch
+    import paper_2501_08453_amd as vc
+    w = W.WORKLOADS[wid]
+    B, N, H, D = w.shape
+    T, F, L = w.text_slot, w.frames, w.grid_h * w.grid_w
+    log("temporal workload", w.name, w.shape)
+    g, h = _inputs(w, seed=None)
+    desc = vc.desc_for(w)
+    out = _run(desc, g)
+    rng = np.random.Generator(np.random.PCG64(9000 + wid))
+    pos = np.sort(rng.choice(L, size=min(L, 48), replace=False))
+    pos = np.unique(np.concatenate([pos, [0, L - 1]]))
+    rows = (T + np.arange(F)[:, None] * L + pos[None, :]).reshape(-1)  # frame-major, like the layout
+    sub = lambda a: a[:, rows]  # noqa: E731
+    o, lse = orb.temporal_forward(sub(h["q"]), sub(h["k"]), sub(h["v"]), 0, F)
+    dq, dk, dv = orb.temporal_backward(sub(h["q"]), sub(h["k"]), sub(h["v"]), sub(h["do"]), 0, F, lse=lse)
+    assert_close("O", sub(out["o"]), o)
+    assert_close("LSE", out["lse"][:, :, rows], lse)
+    assert_close("dQ", sub(out["dq"]), dq)
+    assert_close("dK", sub(out["dk"]), dk)
+    assert_close("dV", sub(out["dv"]), dv)
+    # identities on every head at full size: sum_j dV_j = sum_i dO_i over the video rows
+    # (each video query's probabilities sum to 1) and sum_j dK_j = 0. Each dV_j sums only F
+    # rows here, so the bf16 rounding of the outputs and of P (relative 2^-9 per term,
+    # independent signs) accumulates like a random walk over the rows: the bound is six
+    # standard deviations of that walk, per (sample, head, dim).
+    dv_sum = out["dv"].sum(axis=1)
+    do_sum = h["do"][:, T:].sum(axis=1)
+    walk = 2.0 ** -9 * (np.sqrt((h["do"][:, T:] ** 2).sum(axis=1)) + np.sqrt((out["dv"] ** 2).sum(axis=1)))
+    ratio = (np.abs(dv_sum - do_sum) / walk).max()
+    err_dk = np.abs(out["dk"].sum(axis=1)).max()
+    dk_mag = np.abs(out["dk"]).sum(axis=1).mean()
+    log("   |sum dV - sum dO| / rounding walk: max %.2f; |sum dK| max %.3e (sum |dK| ~ %.3e)"
+        % (ratio, err_dk, dk_mag))
+    assert ratio <= 6.0
+    assert err_dk <= 5e-3 * dk_mag
+    del torch
+
+
+def test_temporal_deterministic_and_text_independent():
+    import torch
+    import paper_2501_08453_amd as vc
+    w = W.custom(1, 2, 128, 24, 8, 6, 5)
+    g, h = _inputs(w, seed=1234)
+    desc = vc.desc_for(w)
+    a = _run(desc, g)
+    b = _run(desc, g)
+    for n in a:
+        np.testing.assert_array_equal(a[n], b[n])
+    # text tokens take no part: changing them changes nothing
+    g2 = dict(g)
+    for n in ("q", "k", "v"):
+        t = g[n].clone()
+        t[:, :w.text_slot] = 3.0
+        g2[n] = t
+    c = _run(desc, g2)
+    for n in a:
+        np.testing.assert_array_equal(a[n], c[n])
+    del torch
