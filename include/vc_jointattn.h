@@ -157,6 +157,35 @@ vc_status vc_jointattn_bwd_dq(const vc_jointattn_desc* desc,
                               void* workspace, size_t workspace_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * Spatial attention branch (Sec. III-B: the video sequence [B, F, L, ...]
+ * regrouped as [B*F, L, ...], L = Hp*Wp, each frame on its own; text tokens are
+ * concatenated to the spatial sequence for attention, Sec. V-B). Computed in
+ * place on the joint layout: a video query of frame f attends to the valid text
+ * keys and the valid keys of frame f, rows [T + f*L, T + (f+1)*L) (validity as
+ * for the joint branch: text_len, key_mask). Text rows are not queries of this
+ * branch: their o and dq are 0 and their lse -inf; text keys still receive dk,
+ * dv from every frame. Same arguments, conventions and workspaces as
+ * vc_jointattn_fwd / vc_jointattn_bwd (use their workspace-size queries); each
+ * workgroup visits only the key tiles of the text and of its own frames.
+ * ------------------------------------------------------------------------- */
+
+/* Spatial forward: o [B,N,H,D] bf16 and lse [B,H,N] fp32 (natural log). */
+vc_status vc_spatialattn_fwd(const vc_jointattn_desc* desc,
+                             const void* q, const void* k, const void* v,
+                             const int32_t* text_len, const uint8_t* key_mask,
+                             void* o, float* lse,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
+/* Spatial backward: dq, dk, dv from q, k, v, the spatial forward's o and lse, and
+ * dout; workspace as for vc_jointattn_bwd. Bitwise reproducible, no atomics. */
+vc_status vc_spatialattn_bwd(const vc_jointattn_desc* desc,
+                             const void* q, const void* k, const void* v,
+                             const void* o, const float* lse, const void* dout,
+                             const int32_t* text_len, const uint8_t* key_mask,
+                             void* dq, void* dk, void* dv,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * Temporal attention branch (Sec. III-B: besides the full-sequence branch the
  * block attends over the video sequence [B, F, L, ...] regrouped as
  * [B*L, F, ...], L = Hp*Wp tokens per frame; the branch outputs are added).

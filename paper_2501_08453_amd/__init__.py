@@ -57,6 +57,8 @@ _SIGS = {
     "vc_jointattn_bwd_prepare": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "vc_jointattn_bwd_dkdv": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "vc_jointattn_bwd_dq": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "vc_spatialattn_fwd": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "vc_spatialattn_bwd": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "vc_temporalattn_fwd": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P]),
     "vc_temporalattn_bwd_workspace_bytes": (ctypes.c_size_t, [_DP]),
     "vc_temporalattn_bwd": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
@@ -174,6 +176,18 @@ def vc_jointattn_bwd_dq(desc, q, k, v, dout, text_len, key_mask, dq, workspace, 
           _ptr(text_len), _ptr(key_mask), _ptr(dq), _ptr(workspace), int(workspace_bytes), _stream(stream))
 
 
+def vc_spatialattn_fwd(desc, q, k, v, text_len, key_mask, o, lse, workspace, workspace_bytes, stream=None):
+    _call("vc_spatialattn_fwd", ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(text_len), _ptr(key_mask),
+          _ptr(o), _ptr(lse), _ptr(workspace), int(workspace_bytes), _stream(stream))
+
+
+def vc_spatialattn_bwd(desc, q, k, v, o, lse, dout, text_len, key_mask, dq, dk, dv, workspace, workspace_bytes,
+                       stream=None):
+    _call("vc_spatialattn_bwd", ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _ptr(dout),
+          _ptr(text_len), _ptr(key_mask), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(workspace), int(workspace_bytes),
+          _stream(stream))
+
+
 def vc_temporalattn_fwd(desc, q, k, v, key_mask, o, lse, stream=None):
     _call("vc_temporalattn_fwd", ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(key_mask), _ptr(o), _ptr(lse),
           _stream(stream))
@@ -266,6 +280,30 @@ def _check_branch_inputs(desc, tensors, key_mask=None):
     if key_mask is not None:
         _check_tensor("key_mask", key_mask, (B, N), torch.uint8)
     return B, N, H, D
+
+
+def spatial_fwd(q, k, v, desc, text_len=None, key_mask=None, out=None, lse=None, ws=None):
+    """Spatial branch (o, lse) for bf16 q, k, v of shape [B, N, H, D] (joint layout)."""
+    import torch
+    B, N, H, D = _check_branch_inputs(desc, (("q", q), ("k", k), ("v", v)), key_mask)
+    if text_len is not None:
+        _check_tensor("text_len", text_len, (B,), torch.int32)
+    o = torch.empty_like(q) if out is None else out
+    lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device) if lse is None else lse
+    ws = fwd_workspace(desc, q.device) if ws is None else ws
+    vc_spatialattn_fwd(desc, q, k, v, text_len, key_mask, o, lse, ws, ws.numel())
+    return o, lse
+
+
+def spatial_bwd(q, k, v, o, lse, dout, desc, text_len=None, key_mask=None, ws=None):
+    """Spatial branch (dq, dk, dv)."""
+    import torch
+    B, N, H, D = _check_branch_inputs(desc, (("q", q), ("k", k), ("v", v), ("o", o), ("dout", dout)), key_mask)
+    _check_tensor("lse", lse, (B, H, N), torch.float32)
+    ws = workspace(desc, q.device) if ws is None else ws
+    dq, dk, dv = (torch.empty_like(q) for _ in range(3))
+    vc_spatialattn_bwd(desc, q, k, v, o, lse, dout, text_len, key_mask, dq, dk, dv, ws, ws.numel())
+    return dq, dk, dv
 
 
 def temporal_fwd(q, k, v, desc, key_mask=None, out=None, lse=None):

@@ -157,9 +157,14 @@ size_t vc_jointattn_bwd_workspace_bytes(const vc_jointattn_desc* desc) {
   return bwd_ws_bytes(desc, n);
 }
 
-vc_status vc_jointattn_fwd(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
-                           const int32_t* text_len, const uint8_t* key_mask, void* o, float* lse, void* workspace,
-                           size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Joint attention (frame_len 0) or the spatial branch (frame_len = tokens per frame).
+vc_status fwd_impl(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
+                   const int32_t* text_len, const uint8_t* key_mask, void* o, float* lse, void* workspace,
+                   size_t workspace_bytes, void* stream, bool spatial) {
   int64_t n = 0;
   vc_status st = check_desc(desc, &n);
   if (st != VC_OK) return st;
@@ -185,8 +190,25 @@ vc_status vc_jointattn_fwd(const vc_jointattn_desc* desc, const void* q, const v
   a.N = (int)n;
   a.T = desc->text_slot;
   a.ntile = ntiles(n);
+  a.frame_len = spatial ? desc->grid_h * desc->grid_w : 0;
   a.scale_log2 = scale_of(desc) * vcja::kLog2e;
   return vcja::launch_fwd(a, desc->head_dim, as_stream(stream)) == hipSuccess ? VC_OK : VC_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+vc_status vc_jointattn_fwd(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
+                           const int32_t* text_len, const uint8_t* key_mask, void* o, float* lse, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+  return fwd_impl(desc, q, k, v, text_len, key_mask, o, lse, workspace, workspace_bytes, stream, false);
+}
+
+vc_status vc_spatialattn_fwd(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
+                             const int32_t* text_len, const uint8_t* key_mask, void* o, float* lse, void* workspace,
+                             size_t workspace_bytes, void* stream) {
+  return fwd_impl(desc, q, k, v, text_len, key_mask, o, lse, workspace, workspace_bytes, stream, true);
 }
 
 vc_status vc_jointattn_bwd_prepare(const vc_jointattn_desc* desc, const void* q, const void* k, const void* o,
@@ -211,9 +233,13 @@ vc_status vc_jointattn_bwd_prepare(const vc_jointattn_desc* desc, const void* q,
   return VC_OK;
 }
 
-vc_status vc_jointattn_bwd_dkdv(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
-                                const void* dout, const int32_t* text_len, const uint8_t* key_mask, void* dk,
-                                void* dv, void* workspace, size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+vc_status dkdv_impl(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v, const void* dout,
+                    const int32_t* text_len, const uint8_t* key_mask, void* dk, void* dv, void* workspace,
+                    size_t workspace_bytes, void* stream, bool spatial) {
   int64_t n = 0;
   vc_status st = check_desc(desc, &n);
   if (st != VC_OK) return st;
@@ -242,14 +268,15 @@ vc_status vc_jointattn_bwd_dkdv(const vc_jointattn_desc* desc, const void* q, co
   a.N = (int)n;
   a.T = desc->text_slot;
   a.ntile = ntiles(n);
+  a.frame_len = spatial ? desc->grid_h * desc->grid_w : 0;
   a.scale = scale_of(desc);
   a.scale_log2 = a.scale * vcja::kLog2e;
   return vcja::launch_bwd_dkdv(a, desc->head_dim, as_stream(stream)) == hipSuccess ? VC_OK : VC_ERR_HIP;
 }
 
-vc_status vc_jointattn_bwd_dq(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
-                              const void* dout, const int32_t* text_len, const uint8_t* key_mask, void* dq,
-                              void* workspace, size_t workspace_bytes, void* stream) {
+vc_status dq_impl(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v, const void* dout,
+                  const int32_t* text_len, const uint8_t* key_mask, void* dq, void* workspace,
+                  size_t workspace_bytes, void* stream, bool spatial) {
   int64_t n = 0;
   vc_status st = check_desc(desc, &n);
   if (st != VC_OK) return st;
@@ -275,24 +302,56 @@ vc_status vc_jointattn_bwd_dq(const vc_jointattn_desc* desc, const void* q, cons
   a.N = (int)n;
   a.T = desc->text_slot;
   a.ntile = ntiles(n);
+  a.frame_len = spatial ? desc->grid_h * desc->grid_w : 0;
   a.scale = scale_of(desc);
   a.scale_log2 = a.scale * vcja::kLog2e;
   return vcja::launch_bwd_dq(a, desc->head_dim, as_stream(stream)) == hipSuccess ? VC_OK : VC_ERR_HIP;
 }
 
-vc_status vc_jointattn_bwd(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v, const void* o,
-                           const float* lse, const void* dout, const int32_t* text_len, const uint8_t* key_mask,
-                           void* dq, void* dk, void* dv, void* workspace, size_t workspace_bytes, void* stream) {
+vc_status bwd_impl(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v, const void* o,
+                   const float* lse, const void* dout, const int32_t* text_len, const uint8_t* key_mask, void* dq,
+                   void* dk, void* dv, void* workspace, size_t workspace_bytes, void* stream, bool spatial) {
   int64_t n = 0;
   vc_status st = check_desc(desc, &n);
   if (st != VC_OK) return st;
   if (!q || !k || !v || !o || !lse || !dout || !dq || !dk || !dv) return VC_ERR_NULL;
   if ((st = vc_jointattn_bwd_prepare(desc, q, k, o, lse, dout, workspace, workspace_bytes, stream)) != VC_OK)
     return st;
-  if ((st = vc_jointattn_bwd_dkdv(desc, q, k, v, dout, text_len, key_mask, dk, dv, workspace, workspace_bytes,
-                                  stream)) != VC_OK)
+  if ((st = dkdv_impl(desc, q, k, v, dout, text_len, key_mask, dk, dv, workspace, workspace_bytes, stream,
+                      spatial)) != VC_OK)
     return st;
-  return vc_jointattn_bwd_dq(desc, q, k, v, dout, text_len, key_mask, dq, workspace, workspace_bytes, stream);
+  return dq_impl(desc, q, k, v, dout, text_len, key_mask, dq, workspace, workspace_bytes, stream, spatial);
+}
+
+}  // namespace
+
+extern "C" {
+
+vc_status vc_jointattn_bwd_dkdv(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
+                                const void* dout, const int32_t* text_len, const uint8_t* key_mask, void* dk,
+                                void* dv, void* workspace, size_t workspace_bytes, void* stream) {
+  return dkdv_impl(desc, q, k, v, dout, text_len, key_mask, dk, dv, workspace, workspace_bytes, stream, false);
+}
+
+vc_status vc_jointattn_bwd_dq(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
+                              const void* dout, const int32_t* text_len, const uint8_t* key_mask, void* dq,
+                              void* workspace, size_t workspace_bytes, void* stream) {
+  return dq_impl(desc, q, k, v, dout, text_len, key_mask, dq, workspace, workspace_bytes, stream, false);
+}
+
+vc_status vc_jointattn_bwd(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v, const void* o,
+                           const float* lse, const void* dout, const int32_t* text_len, const uint8_t* key_mask,
+                           void* dq, void* dk, void* dv, void* workspace, size_t workspace_bytes, void* stream) {
+  return bwd_impl(desc, q, k, v, o, lse, dout, text_len, key_mask, dq, dk, dv, workspace, workspace_bytes, stream,
+                  false);
+}
+
+vc_status vc_spatialattn_bwd(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
+                             const void* o, const float* lse, const void* dout, const int32_t* text_len,
+                             const uint8_t* key_mask, void* dq, void* dk, void* dv, void* workspace,
+                             size_t workspace_bytes, void* stream) {
+  return bwd_impl(desc, q, k, v, o, lse, dout, text_len, key_mask, dq, dk, dv, workspace, workspace_bytes, stream,
+                  true);
 }
 
 vc_status vc_temporalattn_fwd(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,

@@ -74,7 +74,7 @@ __global__ __launch_bounds__(256) void bwd_prepare_kernel(const __bf16* __restri
   }
 }
 
-template <int D>
+template <int D, bool SPATIAL>
 __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a) {
   constexpr int RT = RowTile<D>::kBytes;      // row-major Q or dO tile bytes
   constexpr int RS = RowTile<D>::kStride;     // their row stride
@@ -98,10 +98,13 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
   const int npad = a.ntile * kBQ;
   const int key = blockIdx.x * kBKV + w * 32 + l32;  // this lane's key (accumulator column)
 
-  int tl = a.T;
-  if (a.text_len) tl = min(max(a.text_len[b], 0), a.T);
-  bool valid = (key < N) & ((key >= a.T) | (key < tl));
-  if (a.key_mask) valid = valid & (a.key_mask[(size_t)b * N + min(key, N - 1)] != 0);
+  AttendRule rule;
+  rule.N = N;
+  rule.T = a.T;
+  rule.tl = a.text_len ? min(max(a.text_len[b], 0), a.T) : a.T;
+  rule.L = SPATIAL ? a.frame_len : 0;
+  rule.km = a.key_mask ? a.key_mask + (size_t)b * N : nullptr;
+  const bool valid = rule.key_valid(key);
 
   if (!__syncthreads_or(valid)) {
     // No valid key in this workgroup: its dK, dV are zero.
@@ -152,12 +155,33 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
     dv_acc[i] = zero_f32x16();
   }
 
-  issue(0, 0);
-  for (int qt = 0; qt < a.ntile; ++qt) {
+  // Query tiles this workgroup visits (the same sequence for every wave): all of them in
+  // joint attention; in the spatial branch the video tiles its keys are attended from.
+  const int wk0 = blockIdx.x * kBKV, wk1 = min(wk0 + kBKV, N);
+  auto next_q = [&](int qt) {
+    if (SPATIAL)
+      while (qt < a.ntile && !rule.query_tile_needed(qt * kBQ, wk0, wk1)) ++qt;
+    return qt;
+  };
+  // Spatial branch: a tile needs the per-pair test unless this wave's keys are all text
+  // and the tile holds video queries only, or they all lie in one frame containing it.
+  const int kw0 = blockIdx.x * kBKV + w * 32, kw1 = kw0 + 31;
+  const bool wave_text_keys = kw1 < a.T;
+  const int wks = SPATIAL ? rule.frame_start(kw0) : 0;
+  const bool wave_one_frame = SPATIAL && kw0 >= a.T && kw1 < N && rule.frame_start(kw1) == wks;
+  const int2 kr = key_range(rule, key);  // spatial: queries attending to this lane's key
+
+  int qt = next_q(0);
+  if (qt < a.ntile) issue(qt, 0);
+  for (int pos = 0; qt < a.ntile; ++pos) {
+    const int qn = next_q(qt + 1);
     wait_all_memory();
-    __syncthreads();  // stage qt&1 holds tile qt; every wave is done with the other stage
-    if (qt + 1 < a.ntile) issue(qt + 1, (qt + 1) & 1);
-    const VC_LDS char* q_lds = (const VC_LDS char*)smem + (qt & 1) * STAGE;
+    __syncthreads();  // stage pos&1 holds tile qt; every wave is done with the other stage
+    if (qn < a.ntile) issue(qn, (pos + 1) & 1);
+    const int q0 = qt * kBQ;
+    const bool pair_mask = SPATIAL && !((wave_text_keys && q0 >= a.T) ||
+                                        (wave_one_frame && q0 >= wks && q0 + kBQ <= wks + rule.L));
+    const VC_LDS char* q_lds = (const VC_LDS char*)smem + (pos & 1) * STAGE;
     const VC_LDS char* do_lds = q_lds + RT;
     const VC_LDS char* qt_lds = q_lds + 2 * RT;
     const VC_LDS char* dot_lds = qt_lds + TT;
@@ -178,6 +202,9 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
         dp = mfma32(da, vf[ks], dp);
       }
       // Register r holds query row qb*32 + 8*(r/4) + 4*hi + r%4: four runs of 4 rows.
+      // Spatial branch: on tiles needing the per-pair test, queries outside [kr.x, kr.y)
+      // (this lane's key range) get probability zero.
+      const int row0 = pair_mask ? q0 + qb * 32 : kr.x;
       float p[16], ds[16];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
@@ -186,7 +213,12 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int r = 4 * j + i;
-          p[r] = valid ? fast_exp2(fmaf(s[r], a.scale_log2, -l2[i])) : 0.0f;
+          bool ok = valid;
+          if (SPATIAL) {
+            const int qrow = row0 + acc_row(r, hi);
+            ok = ok & (!pair_mask | ((qrow >= kr.x) & (qrow < kr.y)));
+          }
+          p[r] = ok ? fast_exp2(fmaf(s[r], a.scale_log2, -l2[i])) : 0.0f;
           ds[r] = p[r] * (dp[r] - d4[i]);
         }
       }
@@ -204,6 +236,7 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
         }
       }
     }
+    qt = qn;
   }
 
   if (key < N) {
@@ -261,12 +294,21 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
 #pragma unroll
   for (int i = 0; i < D / 32; ++i) dq_acc[i] = zero_f32x16();
 
-  int tl = a.T;
-  if (a.text_len) tl = min(max(a.text_len[b], 0), a.T);
-  const uint8_t* km = a.key_mask ? a.key_mask + (size_t)b * N : nullptr;
+  AttendRule rule;
+  rule.N = N;
+  rule.T = a.T;
+  rule.tl = a.text_len ? min(max(a.text_len[b], 0), a.T) : a.T;
+  rule.L = a.frame_len;
+  rule.km = a.key_mask ? a.key_mask + (size_t)b * N : nullptr;
+  const int qw0 = blockIdx.x * kDqBM + w * 32, qw1 = qw0 + 31;  // this wave's queries
+  const bool wave_all_video = qw0 >= a.T && qw1 < N;
+  const int wqs = a.frame_len ? rule.frame_start(qw0) : 0;
+  const bool wave_one_frame = wave_all_video && a.frame_len && rule.frame_start(qw1) == wqs;
+  const QueryRange qrange = query_range(rule, qi);
+  // Key tiles this workgroup visits (the same sequence for every wave).
+  const int wq0 = blockIdx.x * kDqBM, wq1 = min(wq0 + kDqBM, N);
   auto next_tile = [&](int kt) {
-    if (!km)
-      while (kt < a.ntile && kt * kBN >= tl && kt * kBN + kBN <= a.T) ++kt;
+    while (kt < a.ntile && !rule.key_tile_needed(kt * kBN, wq0, wq1)) ++kt;
     return kt;
   };
   auto issue = [&](int kt, int st) {
@@ -291,7 +333,15 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
     const VC_LDS char* v_lds = k_lds + RT;
     const VC_LDS char* kt_lds = k_lds + 2 * RT;
     const int k0 = kt * kBN;
-    const bool need_mask = km || (tl < a.T && k0 < a.T && k0 + kBN > tl) || (k0 + kBN > N);
+    bool need_mask;
+    if (rule.km || k0 + kBN > N)
+      need_mask = true;
+    else if (rule.L == 0)
+      need_mask = rule.tl < a.T && k0 < a.T && k0 + kBN > rule.tl;
+    else if (k0 + kBN <= rule.tl)
+      need_mask = !wave_all_video;
+    else
+      need_mask = !(wave_one_frame && k0 >= wqs && k0 + kBN <= wqs + rule.L);
 
 #pragma unroll
     for (int kb = 0; kb < kBN / 32; ++kb) {
@@ -314,8 +364,8 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int key = k0 + kb * 32 + acc_row(r, hi);
-          const uint8_t mv = km ? km[min(key, N - 1)] : (uint8_t)1;
-          const bool ok = (key < N) & ((key >= a.T) | (key < tl)) & (mv != 0);
+          bool ok = rule.key_valid(key);
+          if (rule.L) ok = ok & qrange.ok(key, a.T);
           ds[r] = ok ? ds[r] : 0.0f;
         }
       }
@@ -363,10 +413,15 @@ hipError_t launch_bwd_prepare(const __bf16* o, const float* lse, const __bf16* d
 
 hipError_t launch_bwd_dkdv(const DkdvArgs& a, int head_dim, hipStream_t s) {
   dim3 grid((a.N + kBKV - 1) / kBKV, a.H, a.B);
-  if (head_dim == 128)
-    hipLaunchKernelGGL(bwd_dkdv_kernel<128>, grid, dim3(64 * kDkdvWaves), 0, s, a);
+  const bool spatial = a.frame_len > 0;
+  if (head_dim == 128 && spatial)
+    hipLaunchKernelGGL((bwd_dkdv_kernel<128, true>), grid, dim3(64 * kDkdvWaves), 0, s, a);
+  else if (head_dim == 128)
+    hipLaunchKernelGGL((bwd_dkdv_kernel<128, false>), grid, dim3(64 * kDkdvWaves), 0, s, a);
+  else if (spatial)
+    hipLaunchKernelGGL((bwd_dkdv_kernel<64, true>), grid, dim3(64 * kDkdvWaves), 0, s, a);
   else
-    hipLaunchKernelGGL(bwd_dkdv_kernel<64>, grid, dim3(64 * kDkdvWaves), 0, s, a);
+    hipLaunchKernelGGL((bwd_dkdv_kernel<64, false>), grid, dim3(64 * kDkdvWaves), 0, s, a);
   return hipGetLastError();
 }
 

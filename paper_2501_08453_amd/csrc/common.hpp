@@ -145,6 +145,65 @@ __host__ __device__ constexpr int tok_pos(int t) {
   return (t & ~15) | (((t >> 2) & 3) == 1 ? 8 : ((t >> 2) & 3) == 2 ? 4 : ((t >> 2) & 3) * 4) | (t & 3);
 }
 
+// Which (query, key) pairs attend. Key j of a sample is *valid* if j < N, it is not padded
+// text (j >= T or j < tl) and key_mask keeps it. In joint attention every query sees every
+// valid key. In the spatial branch (frame length L > 0) only video queries attend, to the
+// valid text keys and to the valid keys of their own frame [T + f*L, T + (f+1)*L).
+struct AttendRule {
+  int N, T, tl, L;  // L = 0: joint attention
+  const uint8_t* km;
+  __device__ __forceinline__ int frame_start(int i) const { return T + ((i - T) / L) * L; }
+  __device__ __forceinline__ bool key_valid(int j) const {
+    bool ok = (j < N) & ((j >= T) | (j < tl));
+    if (km) ok = ok & (km[min(j, N - 1)] != 0);  // unconditional clamped load
+    return ok;
+  }
+  // Tiles [k0, k0+64) of keys a workgroup of queries [q0, q1) must visit; uniform across
+  // the workgroup. Joint: all but tiles of padded text only (when there is no key_mask).
+  // Spatial: the real text tiles and the tiles of the frames its video queries lie in.
+  __device__ __forceinline__ bool key_tile_needed(int k0, int q0, int q1) const {
+    if (L == 0) return km || !(k0 >= tl && k0 + kTileTok <= T);
+    const int v0 = max(q0, T);
+    if (v0 >= q1) return false;
+    const int lo = frame_start(v0), hi = min(N, frame_start(q1 - 1) + L);
+    const bool text = k0 < T && (km || k0 < tl);
+    return text || (k0 + kTileTok > lo && k0 < hi);
+  }
+  // Tiles of queries a workgroup of keys [k0, k1) must visit (key-stationary kernels).
+  // Spatial: all video query tiles if it holds real text keys, else the tiles of its
+  // keys' frames; never a tile of text queries only.
+  __device__ __forceinline__ bool query_tile_needed(int q0, int k0, int k1) const {
+    if (L == 0) return true;
+    if (q0 + kTileTok <= T) return false;
+    if (k0 < T && (km || k0 < tl)) return true;
+    const int v0 = max(k0, T);
+    if (v0 >= k1) return false;
+    const int lo = frame_start(v0), hi = min(N, frame_start(k1 - 1) + L);
+    return q0 + kTileTok > lo && q0 < hi;
+  }
+};
+
+// Spatial branch, query side: the keys query i attends to besides text, [lo, hi) (its own
+// frame), and whether it attends to text at all (only video queries do).
+struct QueryRange {
+  int lo, hi;
+  bool text;
+  __device__ __forceinline__ bool ok(int j, int T) const { return j < T ? text : ((j >= lo) & (j < hi)); }
+};
+__device__ __forceinline__ QueryRange query_range(const AttendRule& r, int i) {
+  if (r.L == 0 || i < r.T || i >= r.N) return QueryRange{0, 0, false};
+  const int f0 = r.frame_start(i);
+  return QueryRange{f0, f0 + r.L, true};
+}
+// Spatial branch, key side: the queries attending to key j, [lo, hi): every video query
+// for a text key, the queries of its frame for a video key.
+__device__ __forceinline__ int2 key_range(const AttendRule& r, int j) {
+  if (r.L == 0) return int2{0, 0};
+  if (j < r.T) return int2{r.T, r.N};
+  const int f0 = r.frame_start(min(j, r.N - 1));
+  return int2{f0, f0 + r.L};
+}
+
 // Kernel arguments. Token stride is H*D elements ([B, N, H, D] layout).
 struct FwdArgs {
   const __bf16* q;
@@ -155,6 +214,7 @@ struct FwdArgs {
   __bf16* o;
   float* lse;
   int B, H, N, T, ntile;  // ntile = tiles of 64 tokens per (sample, head)
+  int frame_len;          // 0: joint attention; > 0: spatial branch with frames of this many tokens
   float scale_log2;       // softmax scale times log2(e)
 };
 
@@ -173,6 +233,7 @@ struct DkdvArgs {
   __bf16* dk;
   __bf16* dv;
   int B, H, N, T, ntile;
+  int frame_len;        // 0: joint attention; > 0: spatial branch
   float scale;          // softmax scale
   float scale_log2;     // scale * log2(e)
 };
@@ -190,6 +251,7 @@ struct DqArgs {
   const uint8_t* key_mask;
   __bf16* dq;
   int B, H, N, T, ntile;
+  int frame_len;        // 0: joint attention; > 0: spatial branch
   float scale;
   float scale_log2;
 };

@@ -82,35 +82,33 @@ __device__ __forceinline__ void accumulate_pv(const VC_LDS char* vt_lds, const b
       }
 }
 
+// Masking of one wave's score tiles (lane = query qi).
 struct KeyMask {
-  int N, T, tl;
-  const uint8_t* km;
+  AttendRule rule;
+  QueryRange qr;        // spatial: keys this lane's query attends to
+  bool wave_all_video;  // spatial: every query of the wave is a video row (< N)
+  bool wave_one_frame;  // spatial: ... and they all lie in the frame starting at wqs
+  int wqs;
   __device__ __forceinline__ bool tile_needs_mask(int k0) const {
-    return km || (tl < T && k0 < T && k0 + kBN > tl) || (k0 + kBN > N);
+    const AttendRule& r = rule;
+    if (r.km || k0 + kBN > r.N) return true;
+    if (r.L == 0) return r.tl < r.T && k0 < r.T && k0 + kBN > r.tl;
+    if (k0 + kBN <= r.tl) return !wave_all_video;  // real text keys only
+    return !(wave_one_frame && k0 >= wqs && k0 + kBN <= wqs + r.L);
   }
-  // Sets scores of invalid keys to -inf. Branch-free per element: the validity test is
-  // plain arithmetic and the optional mask byte is loaded unconditionally (clamped index).
+  // Sets scores of keys this lane's query does not attend to to -inf. Branch-free per
+  // element: the tests are plain arithmetic and the optional mask byte is loaded
+  // unconditionally (clamped index).
   __device__ __forceinline__ void apply(f32x16* s, int k0, int hi) const {
-    if (km) {
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = k0 + kb * 32 + acc_row(r, hi);
-          const uint8_t mv = km[min(key, N - 1)];
-          const bool ok = (key < N) & ((key >= T) | (key < tl)) & (mv != 0);
-          s[kb][r] = ok ? s[kb][r] : -INFINITY;
-        }
-    } else {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = k0 + kb * 32 + acc_row(r, hi);
-          const bool ok = (key < N) & ((key >= T) | (key < tl));
-          s[kb][r] = ok ? s[kb][r] : -INFINITY;
-        }
-    }
+      for (int r = 0; r < 16; ++r) {
+        const int key = k0 + kb * 32 + acc_row(r, hi);
+        bool ok = rule.key_valid(key);
+        if (rule.L) ok = ok & qr.ok(key, rule.T);
+        s[kb][r] = ok ? s[kb][r] : -INFINITY;
+      }
   }
 };
 
@@ -197,14 +195,23 @@ __global__ __launch_bounds__(64 * kWaves, kWavesPerSimd * 4 / kWaves) void fwd_k
   }
 
   KeyMask mask;
-  mask.N = N;
-  mask.T = a.T;
-  mask.tl = a.text_len ? min(max(a.text_len[b], 0), a.T) : a.T;
-  mask.km = a.key_mask ? a.key_mask + (size_t)b * N : nullptr;
-  // A tile made only of padded text keys contributes nothing and is skipped.
+  mask.rule.N = N;
+  mask.rule.T = a.T;
+  mask.rule.tl = a.text_len ? min(max(a.text_len[b], 0), a.T) : a.T;
+  mask.rule.L = a.frame_len;
+  mask.rule.km = a.key_mask ? a.key_mask + (size_t)b * N : nullptr;
+  mask.qr = query_range(mask.rule, qi);
+  {
+    const int qw0 = blockIdx.x * kBM + w * 32, qw1 = qw0 + 31;  // this wave's queries
+    mask.wave_all_video = qw0 >= a.T && qw1 < N;
+    mask.wqs = a.frame_len ? mask.rule.frame_start(qw0) : 0;
+    mask.wave_one_frame = mask.wave_all_video && a.frame_len && mask.rule.frame_start(qw1) == mask.wqs;
+  }
+  // Key tiles this workgroup visits (the same sequence for every wave): all but tiles of
+  // padded text only in joint attention; text and own-frame tiles in the spatial branch.
+  const int wq0 = blockIdx.x * kBM, wq1 = min(wq0 + kBM, N);
   auto next_tile = [&](int kt) {
-    if (!mask.km)
-      while (kt < a.ntile && kt * kBN >= mask.tl && kt * kBN + kBN <= a.T) ++kt;
+    while (kt < a.ntile && !mask.rule.key_tile_needed(kt * kBN, wq0, wq1)) ++kt;
     return kt;
   };
   // Copies tile kt's K rows (rows past N repeat row N-1 and are masked) or V^T tile into
