@@ -9,6 +9,12 @@ stream. Inputs are resident in HBM before timing.
 Prints one JSON line. `value` is algorithmic TFLOP/s of the whole step:
 12 * H * N * N_kv * D per sample (forward 4, backward 8; the backward's
 recomputation of Q K^T is not counted).
+
+--branch spatial / temporal measure the other two attention branches of the
+block instead (same inputs, forward + backward): the spatial branch in
+algorithmic TFLOP/s (each video query against the valid text keys and its own
+frame), the temporal branch, which is bound by memory traffic, in algorithmic
+GB/s (bytes the step must move at least).
 """
 from __future__ import annotations
 
@@ -27,7 +33,10 @@ import numpy as np  # noqa: E402
 import workloads as W  # noqa: E402
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 matrix-core peak (published)
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E bandwidth (published)
 METRIC = "joint-attention fwd+bwd TFLOP/s and % bf16 MFMA peak at 57,856 tokens"
+METRIC_SPATIAL = "spatial-attention fwd+bwd TFLOP/s (per-frame text+frame keys)"
+METRIC_TEMPORAL = "temporal-attention fwd+bwd GB/s (algorithmic HBM bytes)"
 
 
 def valid_keys_per_sample(w, text_len):
@@ -41,6 +50,75 @@ def flops(w, text_len):
     nkv = valid_keys_per_sample(w, text_len)
     fwd = sum(4.0 * w.heads * w.tokens * n * w.head_dim for n in nkv)
     return fwd, 2.0 * fwd
+
+
+def spatial_flops(w, text_len):
+    """Forward, backward algorithmic flops of the spatial branch: each of the F*L video
+    queries against the valid text keys and the L keys of its frame."""
+    L = w.grid_h * w.grid_w
+    tl = [w.text_slot] * w.batch if text_len is None else np.clip(np.asarray(text_len), 0, w.text_slot)
+    fwd = sum(4.0 * w.heads * w.frames * L * (L + int(t)) * w.head_dim for t in tl)
+    return fwd, 2.0 * fwd
+
+
+def temporal_bytes(w):
+    """Forward, backward algorithmic HBM bytes of the temporal branch (bf16 tensors of the
+    video rows, fp32 LSE and D): forward reads q, k, v and writes o, lse; backward reads
+    q, k, v, o, dO, lse and writes dq, dk, dv (D kept on chip would save its round trip;
+    it is counted once as written and once as read)."""
+    rows = w.batch * w.frames * w.grid_h * w.grid_w * w.heads
+    t = rows * w.head_dim * 2.0
+    r = rows * 4.0
+    return 3 * t + t + r, 5 * t + r + 3 * t + 2 * r
+
+
+def cpu_baseline_branch(kind, w, g, text_len, target_s):
+    """The branch oracle timed on a bounded sample: whole frames of head 0 (spatial) or a
+    block of spatial positions of head 0 (temporal), forward + backward."""
+    import torch
+    import oracle.ref_branches as orb
+    T, F, L = w.text_slot, w.frames, w.grid_h * w.grid_w
+    tl = None if text_len is None else text_len[:1]
+    threads = __import__("oracle").host_threads()
+    if kind == "spatial":
+        # one frame of sample 0 with every head per round (the oracle's pool runs the heads
+        # in parallel), frames added until the target time is reached
+        done, fl, t = 0, 0.0, 0.0
+        while done < F and t < target_s:
+            def sl(name):
+                a = g[name][:1]
+                a = torch.cat([a[:, :T], a[:, T + done * L:T + (done + 1) * L]], dim=1)
+                return a.to(torch.float64).cpu().numpy()
+            q, k, v, do = (sl(n) for n in ("q", "k", "v", "do"))
+            t0 = time.perf_counter()
+            _, lse = orb.spatial_forward(q, k, v, T, 1, tl)
+            orb.spatial_backward(q, k, v, do, T, 1, tl, lse=lse)
+            t += time.perf_counter() - t0
+            tv = T if tl is None else int(min(max(tl[0], 0), T))
+            fl += 12.0 * w.heads * L * (L + tv) * w.head_dim
+            done += 1
+        return {"value": fl / t / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+                "sample": "%d frame(s) of sample 0, all %d heads (text + frame keys), fwd+bwd, %.1f s"
+                % (done, w.heads, t)}
+    h0 = lambda t: t[:1, :, :1].to(torch.float64).cpu().numpy()  # noqa: E731
+    q, k, v, do = (h0(g[n]) for n in ("q", "k", "v", "do"))
+    n_pos = 64
+    while True:
+        pos = np.arange(min(n_pos, L))
+        rows = (T + np.arange(F)[:, None] * L + pos[None, :]).reshape(-1)
+        sl = lambda a: a[:, rows]  # noqa: E731
+        t0 = time.perf_counter()
+        _, lse = orb.temporal_forward(sl(q), sl(k), sl(v), 0, F)
+        orb.temporal_backward(sl(q), sl(k), sl(v), sl(do), 0, F, lse=lse)
+        t = time.perf_counter() - t0
+        if t >= target_s / 4 or n_pos >= L:
+            break
+        n_pos *= 2
+    wsub = W.custom(1, 1, w.head_dim, 0, F, 1, len(pos))
+    bf, bb = temporal_bytes(wsub)
+    return {"value": (bf + bb) / t / 1e9, "unit": "GB/s", "cores": __import__("oracle").host_threads(),
+            "kind": "oracle", "sample": "%d spatial positions x %d frames of sample 0, head 0, fwd+bwd, %.1f s"
+            % (len(pos), F, t)}
 
 
 def cpu_baseline(w, g, text_len, target_s):
@@ -85,27 +163,30 @@ def cpu_baseline(w, g, text_len, target_s):
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_bwd_dkdv_long720p.json")
 KERNEL_SOURCES = ["paper_2501_08453_amd/csrc/bwd.hip", "paper_2501_08453_amd/csrc/common.hpp"]
+TEMPORAL_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_temporal_bwd_long720p.json")
+TEMPORAL_SOURCES = ["paper_2501_08453_amd/csrc/temporal.hip", "paper_2501_08453_amd/csrc/bwd.hip",
+                    "paper_2501_08453_amd/csrc/common.hpp"]
 
 
-def kernel_source_digest() -> str:
+def kernel_source_digest(sources=KERNEL_SOURCES) -> str:
     import hashlib
     h = hashlib.sha256()
-    for rel in KERNEL_SOURCES:
+    for rel in sources:
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
     return h.hexdigest()
 
 
-def traffic_record():
-    """HBM bytes per launch of the dK/dV kernel measured with hardware counters (FETCH_SIZE
-    + WRITE_SIZE, scaled by a plain copy of known size), if the record matches the current
-    kernel sources; None otherwise."""
+def traffic_record(path=TRAFFIC_FILE, sources=KERNEL_SOURCES):
+    """HBM bytes per launch measured with hardware counters (FETCH_SIZE + WRITE_SIZE,
+    scaled by a plain copy of known size), if the record matches the current kernel
+    sources; None otherwise."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(path) as f:
             rec = json.load(f)
     except (OSError, ValueError):
         return None
-    if rec.get("source_digest") != kernel_source_digest():
+    if rec.get("source_digest") != kernel_source_digest(sources):
         return None
     return rec.get("bytes_per_launch")
 
@@ -116,6 +197,8 @@ def main(argv=None):
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", type=int, default=W.HEADLINE, choices=sorted(W.WORKLOADS))
+    ap.add_argument("--branch", default="joint", choices=["joint", "spatial", "temporal"],
+                    help="attention branch to measure (joint = the headline)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the oracle timing")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -149,6 +232,8 @@ def main(argv=None):
     q, k, v, do = g["q"], g["k"], g["v"], g["do"]
     stream = torch.cuda.current_stream()
     sh = stream.cuda_stream
+    if args.branch != "joint":
+        return branch_main(args, w, g, text_len, tl, desc, o, lse, dq, dk, dv, fws, ws, stream)
 
     # Events bracket each stage on the stream the library launches on.
     def step(ev=None):
@@ -230,13 +315,95 @@ def main(argv=None):
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, g, text_len, args.cpu_seconds)
     print(json.dumps(line), flush=True)
-    if args.copy_calibration_mib:
-        n = args.copy_calibration_mib << 20
-        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
+    copy_calibration(args.copy_calibration_mib, dev)
+    return 0
+
+
+def copy_calibration(mib, dev):
+    """One plain device-to-device copy of `mib` MiB: the reference the hardware byte
+    counters are scaled by."""
+    if not mib:
+        return
+    import torch
+    n = mib << 20
+    src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+
+
+def branch_main(args, w, g, text_len, tl, desc, o, lse, dq, dk, dv, fws, ws, stream):
+    """Forward + backward of the spatial or temporal branch, events around each call."""
+    import torch
+    import paper_2501_08453_amd as vc
+    q, k, v, do = g["q"], g["k"], g["v"], g["do"]
+    sh = stream.cuda_stream
+    B, N, H, D = w.shape
+    if args.branch == "temporal":
+        tws = vc._workspace(vc.vc_temporalattn_bwd_workspace_bytes(desc), q.device)
+
+    def step(ev=None):
+        if ev:
+            ev[0].record(stream)
+        if args.branch == "spatial":
+            vc.vc_spatialattn_fwd(desc, q, k, v, tl, None, o, lse, fws, fws.numel(), sh)
+        else:
+            vc.vc_temporalattn_fwd(desc, q, k, v, None, o, lse, sh)
+        if ev:
+            ev[1].record(stream)
+        if args.branch == "spatial":
+            vc.vc_spatialattn_bwd(desc, q, k, v, o, lse, do, tl, None, dq, dk, dv, ws, ws.numel(), sh)
+        else:
+            vc.vc_temporalattn_bwd(desc, q, k, v, o, lse, do, None, dq, dk, dv, tws, tws.numel(), sh)
+        if ev:
+            ev[2].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    k_fwd = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    k_bwd = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    if args.branch == "spatial":
+        a_fwd, a_bwd = spatial_flops(w, text_len)
+        scale, unit, peak, bound, metric = 1e12, "TFLOP/s", PEAK_BF16_TFLOPS, "mfma", METRIC_SPATIAL
+    else:
+        a_fwd, a_bwd = temporal_bytes(w)
+        scale, unit, peak, bound, metric = 1e9, "GB/s", PEAK_HBM_GBS, "hbm", METRIC_TEMPORAL
+    value = (a_fwd + a_bwd) / (ms_step * 1e-3) / scale
+    # Dominant call: the backward (one call: preparation, dK/dV and dQ kernels).
+    bwd_rate = a_bwd / (k_bwd * 1e-3) / scale
+    line = {
+        "metric": metric, "value": round(value, 2), "unit": unit, "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) q, k, v, dO of the workload's shape)",
+        "config": {
+            "workload": "%s, %s branch: B=%d, H=%d, D=%d, %d text + %dx%dx%d video = %d tokens"
+                        % (w.name, args.branch, B, H, D, w.text_slot, w.frames, w.grid_h, w.grid_w, N),
+            "branch": args.branch, "batch": B, "heads": H, "head_dim": D, "tokens": N,
+            "text_slot": w.text_slot, "frames": w.frames, "grid": [w.grid_h, w.grid_w],
+        },
+        "kernels_ms": {"fwd": round(k_fwd, 4), "bwd": round(k_bwd, 4)},
+        "fwd_rate": round(a_fwd / (k_fwd * 1e-3) / scale, 2),
+        "roofline": {"bound": bound, "kernel": "%s backward (prepare + gradient kernels)" % args.branch,
+                     "achieved": round(bwd_rate, 2), "peak": peak, "unit": unit,
+                     "frac": round(bwd_rate / peak, 4), "traffic": None,
+                     "algorithmic_per_launch": a_bwd},
+    }
+    tr = traffic_record(TEMPORAL_TRAFFIC_FILE, TEMPORAL_SOURCES) if args.branch == "temporal" else None
+    if tr is not None:
+        line["roofline"]["traffic"] = tr
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline_branch(args.branch, w, g, text_len, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+    copy_calibration(args.copy_calibration_mib, q.device)
     return 0
 
 
