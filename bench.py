@@ -227,7 +227,7 @@ def main(argv=None):
     lse = torch.empty((B, H, N), dtype=torch.float32, device=dev)
     dq, dk, dv = (torch.empty_like(g["q"]) for _ in range(3))
     fws = vc.fwd_workspace(desc, dev)
-    ws = vc.workspace(desc, dev)
+    ws = vc.spatial_workspace(desc, dev) if args.branch == "spatial" else vc.workspace(desc, dev)
     fwsb, wsb = fws.numel(), ws.numel()
     q, k, v, do = g["q"], g["k"], g["v"], g["do"]
     stream = torch.cuda.current_stream()

@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define VC_JOINTATTN_ABI_VERSION 2
+#define VC_JOINTATTN_ABI_VERSION 3
 
 typedef enum vc_status {
   VC_OK = 0,
@@ -164,10 +164,17 @@ vc_status vc_jointattn_bwd_dq(const vc_jointattn_desc* desc,
  * keys and the valid keys of frame f, rows [T + f*L, T + (f+1)*L) (validity as
  * for the joint branch: text_len, key_mask). Text rows are not queries of this
  * branch: their o and dq are 0 and their lse -inf; text keys still receive dk,
- * dv from every frame. Same arguments, conventions and workspaces as
- * vc_jointattn_fwd / vc_jointattn_bwd (use their workspace-size queries); each
- * workgroup visits only the key tiles of the text and of its own frames.
+ * dv from every frame. Same arguments and conventions as vc_jointattn_fwd /
+ * vc_jointattn_bwd; the forward takes the joint forward workspace, the backward
+ * its own (vc_spatialattn_bwd_workspace_bytes: the joint backward workspace plus
+ * fp32 partial dk, dv of the text keys, whose work is split over several
+ * workgroups). Each workgroup visits only the key tiles of the text and of its
+ * own frames.
  * ------------------------------------------------------------------------- */
+
+/* Bytes of backward workspace vc_spatialattn_bwd needs for this descriptor (at
+ * least vc_jointattn_bwd_workspace_bytes), or 0 if the descriptor is invalid. */
+size_t vc_spatialattn_bwd_workspace_bytes(const vc_jointattn_desc* desc);
 
 /* Spatial forward: o [B,N,H,D] bf16 and lse [B,H,N] fp32 (natural log). */
 vc_status vc_spatialattn_fwd(const vc_jointattn_desc* desc,
@@ -177,7 +184,8 @@ vc_status vc_spatialattn_fwd(const vc_jointattn_desc* desc,
                              void* workspace, size_t workspace_bytes, void* stream);
 
 /* Spatial backward: dq, dk, dv from q, k, v, the spatial forward's o and lse, and
- * dout; workspace as for vc_jointattn_bwd. Bitwise reproducible, no atomics. */
+ * dout; workspace of vc_spatialattn_bwd_workspace_bytes (smaller: VC_ERR_WORKSPACE,
+ * nothing launched). Bitwise reproducible, no atomics. */
 vc_status vc_spatialattn_bwd(const vc_jointattn_desc* desc,
                              const void* q, const void* k, const void* v,
                              const void* o, const float* lse, const void* dout,

@@ -58,6 +58,7 @@ _SIGS = {
     "vc_jointattn_bwd_dkdv": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "vc_jointattn_bwd_dq": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "vc_spatialattn_fwd": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "vc_spatialattn_bwd_workspace_bytes": (ctypes.c_size_t, [_DP]),
     "vc_spatialattn_bwd": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "vc_temporalattn_fwd": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P]),
     "vc_temporalattn_bwd_workspace_bytes": (ctypes.c_size_t, [_DP]),
@@ -181,6 +182,10 @@ def vc_spatialattn_fwd(desc, q, k, v, text_len, key_mask, o, lse, workspace, wor
           _ptr(o), _ptr(lse), _ptr(workspace), int(workspace_bytes), _stream(stream))
 
 
+def vc_spatialattn_bwd_workspace_bytes(desc) -> int:
+    return _lib().vc_spatialattn_bwd_workspace_bytes(ctypes.byref(desc))
+
+
 def vc_spatialattn_bwd(desc, q, k, v, o, lse, dout, text_len, key_mask, dq, dk, dv, workspace, workspace_bytes,
                        stream=None):
     _call("vc_spatialattn_bwd", ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _ptr(dout),
@@ -233,6 +238,11 @@ def fwd_workspace(desc, device):
 def workspace(desc, device):
     """Backward workspace for a descriptor."""
     return _workspace(vc_jointattn_bwd_workspace_bytes(desc), device)
+
+
+def spatial_workspace(desc, device):
+    """Backward workspace of the spatial branch for a descriptor."""
+    return _workspace(vc_spatialattn_bwd_workspace_bytes(desc), device)
 
 
 def fwd(q, k, v, desc, text_len=None, key_mask=None, out=None, lse=None, ws=None):
@@ -300,7 +310,7 @@ def spatial_bwd(q, k, v, o, lse, dout, desc, text_len=None, key_mask=None, ws=No
     import torch
     B, N, H, D = _check_branch_inputs(desc, (("q", q), ("k", k), ("v", v), ("o", o), ("dout", dout)), key_mask)
     _check_tensor("lse", lse, (B, H, N), torch.float32)
-    ws = workspace(desc, q.device) if ws is None else ws
+    ws = spatial_workspace(desc, q.device) if ws is None else ws
     dq, dk, dv = (torch.empty_like(q) for _ in range(3))
     vc_spatialattn_bwd(desc, q, k, v, o, lse, dout, text_len, key_mask, dq, dk, dv, ws, ws.numel())
     return dq, dk, dv

@@ -4,6 +4,7 @@
 #include <math.h>
 #include <string.h>
 
+#include <algorithm>
 #include <mutex>
 
 #include "common.hpp"
@@ -90,6 +91,34 @@ BwdWorkspace split_bwd_ws(const vc_jointattn_desc* d, int64_t n, void* ws) {
                       reinterpret_cast<__bf16*>(p + 2 * rb + 2 * tb)};
 }
 
+// Spatial branch: split of the text key blocks' video query tiles into chunks of about one
+// frame (at least kMinTextSpan tiles), so that no dK/dV workgroup visits every video tile.
+constexpr int kMinTextSpan = 8;
+constexpr int kMaxTextChunks = 64;
+struct TextSplit {
+  int blocks, chunks, span;
+};
+TextSplit text_split(const vc_jointattn_desc* d, int64_t n) {
+  const int T = d->text_slot;
+  const int blocks = (T + vcja::kDkdvKeys - 1) / vcja::kDkdvKeys;
+  const int nvq = ntiles(n) - T / vcja::kTileTok;  // tiles holding video queries
+  const int L = d->grid_h * d->grid_w;
+  const int span = std::max((L + vcja::kTileTok - 1) / vcja::kTileTok + 1, kMinTextSpan);
+  const int chunks = blocks ? std::min(kMaxTextChunks, (nvq + span - 1) / span) : 1;
+  if (chunks < 2) return TextSplit{blocks, 1, nvq};
+  return TextSplit{blocks, chunks, (nvq + chunks - 1) / chunks};
+}
+// fp32 partial dK and dV of the split text blocks.
+size_t text_part_bytes(const vc_jointattn_desc* d, int64_t n) {
+  const TextSplit t = text_split(d, n);
+  if (t.chunks < 2) return 0;
+  return align256((size_t)2 * t.chunks * d->batch * d->heads * t.blocks * vcja::kDkdvKeys * d->head_dim *
+                  sizeof(float));
+}
+size_t spatial_bwd_ws_bytes(const vc_jointattn_desc* d, int64_t n) {
+  return bwd_ws_bytes(d, n) + text_part_bytes(d, n);
+}
+
 vc_status check_ws(void* ws, size_t have, size_t need) {
   if (!ws) return VC_ERR_WORKSPACE;
   if ((reinterpret_cast<uintptr_t>(ws) & 255u) != 0) return VC_ERR_ALIGN;
@@ -155,6 +184,12 @@ size_t vc_jointattn_bwd_workspace_bytes(const vc_jointattn_desc* desc) {
   int64_t n = 0;
   if (check_desc(desc, &n) != VC_OK) return 0;
   return bwd_ws_bytes(desc, n);
+}
+
+size_t vc_spatialattn_bwd_workspace_bytes(const vc_jointattn_desc* desc) {
+  int64_t n = 0;
+  if (check_desc(desc, &n) != VC_OK) return 0;
+  return spatial_bwd_ws_bytes(desc, n);
 }
 
 }  // extern "C"
@@ -247,10 +282,17 @@ vc_status dkdv_impl(const vc_jointattn_desc* desc, const void* q, const void* k,
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(dout) || !aligned16(dk) || !aligned16(dv) ||
       !aligned4(text_len))
     return VC_ERR_ALIGN;
-  if ((st = check_ws(workspace, workspace_bytes, bwd_ws_bytes(desc, n))) != VC_OK) return st;
+  if ((st = check_ws(workspace, workspace_bytes, spatial ? spatial_bwd_ws_bytes(desc, n) : bwd_ws_bytes(desc, n))) !=
+      VC_OK)
+    return st;
   if ((st = check_device()) != VC_OK) return st;
   const BwdWorkspace w = split_bwd_ws(desc, n, workspace);
   vcja::DkdvArgs a;
+  const TextSplit ts = spatial ? text_split(desc, n) : TextSplit{0, 1, 0};
+  a.text_part = reinterpret_cast<float*>(static_cast<char*>(workspace) + bwd_ws_bytes(desc, n));
+  a.text_blocks = ts.blocks;
+  a.text_chunks = ts.chunks;
+  a.text_span = ts.span;
   a.q = bf(q);
   a.k = bf(k);
   a.v = bf(v);
@@ -315,6 +357,7 @@ vc_status bwd_impl(const vc_jointattn_desc* desc, const void* q, const void* k, 
   vc_status st = check_desc(desc, &n);
   if (st != VC_OK) return st;
   if (!q || !k || !v || !o || !lse || !dout || !dq || !dk || !dv) return VC_ERR_NULL;
+  if (spatial && (st = check_ws(workspace, workspace_bytes, spatial_bwd_ws_bytes(desc, n))) != VC_OK) return st;
   if ((st = vc_jointattn_bwd_prepare(desc, q, k, o, lse, dout, workspace, workspace_bytes, stream)) != VC_OK)
     return st;
   if ((st = dkdv_impl(desc, q, k, v, dout, text_len, key_mask, dk, dv, workspace, workspace_bytes, stream,

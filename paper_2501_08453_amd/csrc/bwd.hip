@@ -29,6 +29,7 @@ namespace {
 
 constexpr int kDkdvWaves = 8;
 constexpr int kBKV = 32 * kDkdvWaves;  // keys per dK/dV workgroup
+static_assert(kBKV == kDkdvKeys, "dK/dV key block");
 constexpr int kBQ = kTileTok;  // queries per dK/dV tile
 constexpr int kDqWaves = 8;
 constexpr int kDqBM = 32 * kDqWaves;  // queries per dQ workgroup
@@ -89,14 +90,32 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index (uniform)
   const int l32 = lane & 31;
   const int hi = lane >> 5;
-  const int h = blockIdx.y;
-  const int b = blockIdx.z;
+  const int3 gp = xcd_grid_pos(SPATIAL);
+  const int h = gp.y;
+  const int b = gp.z;
   const int N = a.N;
   const size_t tok = (size_t)a.H * D;
   const size_t base = (size_t)b * N * tok + (size_t)h * D;
   const size_t bh = (size_t)b * a.H + h;
   const int npad = a.ntile * kBQ;
-  const int key = blockIdx.x * kBKV + w * 32 + l32;  // this lane's key (accumulator column)
+  // Spatial branch with split text blocks: workgroups [0, text_blocks*text_chunks) of a head
+  // take (text block, chunk of its query tiles) and come first in dispatch order, the rest
+  // the other key blocks in order.
+  int kb = gp.x, chunk = 0;
+  bool split = false;
+  if (SPATIAL && a.text_chunks > 1) {
+    const int nsplit = a.text_blocks * a.text_chunks;
+    split = gp.x < nsplit;
+    kb = split ? gp.x % a.text_blocks : gp.x - nsplit + a.text_blocks;
+    chunk = split ? gp.x / a.text_blocks : 0;
+  }
+  const int key = kb * kBKV + w * 32 + l32;  // this lane's key (accumulator column)
+  // Partial dK of this lane's key in its chunk (dV partials follow all dK partials); formed
+  // only where it is written, so that no register holds it across the main loop.
+  const size_t part_stride = (size_t)a.text_chunks * a.B * a.H * a.text_blocks * kBKV * D;
+  auto part_k = [&]() {
+    return a.text_part + ((((size_t)chunk * a.B + b) * a.H + h) * a.text_blocks * kBKV + key) * D;
+  };
 
   AttendRule rule;
   rule.N = N;
@@ -107,8 +126,15 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
   const bool valid = rule.key_valid(key);
 
   if (!__syncthreads_or(valid)) {
-    // No valid key in this workgroup: its dK, dV are zero.
-    if (key < N) {
+    // No valid key in this workgroup: its dK, dV (or partials) are zero.
+    if (split) {
+      const f32x4 z = {0.0f, 0.0f, 0.0f, 0.0f};
+      float* pk = part_k();
+      for (int c = 0; c < D / 4; ++c) {
+        *(f32x4*)(pk + 4 * c) = z;
+        *(f32x4*)(pk + part_stride + 4 * c) = z;
+      }
+    } else if (key < N) {
       const bf16x8 z = zero_bf16x8();
       for (int c = 0; c < D / 8; ++c) {
         *(bf16x8*)(a.dk + base + (size_t)key * tok + 8 * c) = z;
@@ -157,15 +183,18 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
 
   // Query tiles this workgroup visits (the same sequence for every wave): all of them in
   // joint attention; in the spatial branch the video tiles its keys are attended from.
-  const int wk0 = blockIdx.x * kBKV, wk1 = min(wk0 + kBKV, N);
-  auto next_q = [&](int qt) {
-    if (SPATIAL)
-      while (qt < a.ntile && !rule.query_tile_needed(qt * kBQ, wk0, wk1)) ++qt;
-    return qt;
-  };
+  const int wk0 = kb * kBKV;
+  TileRuns runs = rule.query_tiles(wk0, min(wk0 + kBKV, N), a.ntile);
+  if (split) {  // this chunk's part of the video query tiles
+    const int c0 = a.T / kBQ + chunk * a.text_span;
+    runs.b0 = max(runs.b0, c0);
+    runs.b1 = min(runs.b1, c0 + a.text_span);
+    if (runs.b0 >= runs.b1) runs.b1 = 0;
+  }
+  auto next_q = [&](int qt) { return SPATIAL ? runs.next(qt) : qt; };
   // Spatial branch: a tile needs the per-pair test unless this wave's keys are all text
   // and the tile holds video queries only, or they all lie in one frame containing it.
-  const int kw0 = blockIdx.x * kBKV + w * 32, kw1 = kw0 + 31;
+  const int kw0 = kb * kBKV + w * 32, kw1 = kw0 + 31;
   const bool wave_text_keys = kw1 < a.T;
   const int wks = SPATIAL ? rule.frame_start(kw0) : 0;
   const bool wave_one_frame = SPATIAL && kw0 >= a.T && kw1 < N && rule.frame_start(kw1) == wks;
@@ -239,7 +268,19 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
     qt = qn;
   }
 
-  if (key < N) {
+  if (split) {
+    float* pk = part_k();
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const f32x4 tk = {dk_acc[db][4 * j + 0] * a.scale, dk_acc[db][4 * j + 1] * a.scale,
+                          dk_acc[db][4 * j + 2] * a.scale, dk_acc[db][4 * j + 3] * a.scale};
+        const f32x4 tv = {dv_acc[db][4 * j + 0], dv_acc[db][4 * j + 1], dv_acc[db][4 * j + 2], dv_acc[db][4 * j + 3]};
+        *(f32x4*)(pk + db * 32 + 8 * j + 4 * hi) = tk;
+        *(f32x4*)(pk + part_stride + db * 32 + 8 * j + 4 * hi) = tv;
+      }
+  } else if (key < N) {
     __bf16* dkp = a.dk + base + (size_t)key * tok;
     __bf16* dvp = a.dv + base + (size_t)key * tok;
 #pragma unroll
@@ -254,6 +295,33 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
         *(bf16x4*)(dvp + db * 32 + 8 * j + 4 * hi) = tv;
       }
   }
+}
+
+// Spatial branch: dK, dV of the split text blocks' rows [0, min(rows, N)) as the sum of the
+// chunks' fp32 partials (rows = text_blocks * 256). One thread per 4 dims of one row.
+template <int D>
+__global__ void text_reduce_kernel(const float* part, __bf16* dk, __bf16* dv, int B, int H, int N, int rows,
+                                   int chunks) {
+  const int nrow = min(rows, N);
+  const size_t total = (size_t)B * H * nrow * (D / 4);
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= total) return;
+  const int d = (int)(i % (D / 4)) * 4;
+  size_t t = i / (D / 4);
+  const int row = (int)(t % nrow);
+  t /= nrow;
+  const int h = (int)(t % H);
+  const int b = (int)(t / H);
+  const size_t stride = (size_t)B * H * rows * D;  // one chunk
+  const size_t off = (((size_t)b * H + h) * rows + row) * D + d;
+  f32x4 sk = {0.0f, 0.0f, 0.0f, 0.0f}, sv = sk;
+  for (int c = 0; c < chunks; ++c) {
+    sk += *(const f32x4*)(part + c * stride + off);
+    sv += *(const f32x4*)(part + (size_t)chunks * stride + c * stride + off);
+  }
+  const size_t o = (((size_t)b * N + row) * H + h) * D + d;
+  *(bf16x4*)(dk + o) = bf16x4{(__bf16)sk[0], (__bf16)sk[1], (__bf16)sk[2], (__bf16)sk[3]};
+  *(bf16x4*)(dv + o) = bf16x4{(__bf16)sv[0], (__bf16)sv[1], (__bf16)sv[2], (__bf16)sv[3]};
 }
 
 template <int D>
@@ -271,13 +339,14 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index (uniform)
   const int l32 = lane & 31;
   const int hi = lane >> 5;
-  const int h = blockIdx.y;
-  const int b = blockIdx.z;
+  const int3 gp = xcd_grid_pos(a.frame_len != 0);
+  const int h = gp.y;
+  const int b = gp.z;
   const int N = a.N;
   const size_t tok = (size_t)a.H * D;
   const size_t base = (size_t)b * N * tok + (size_t)h * D;
   const size_t bh = (size_t)b * a.H + h;
-  const int qi = blockIdx.x * kDqBM + w * 32 + l32;  // this lane's query (accumulator column)
+  const int qi = gp.x * kDqBM + w * 32 + l32;  // this lane's query (accumulator column)
   const int qr = min(qi, N - 1);
 
   // Q^T and dO^T as B operands (dims 16*ks + 8*hi .. +7), LSE*log2e and D as scalars.
@@ -300,17 +369,15 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
   rule.tl = a.text_len ? min(max(a.text_len[b], 0), a.T) : a.T;
   rule.L = a.frame_len;
   rule.km = a.key_mask ? a.key_mask + (size_t)b * N : nullptr;
-  const int qw0 = blockIdx.x * kDqBM + w * 32, qw1 = qw0 + 31;  // this wave's queries
+  const int qw0 = gp.x * kDqBM + w * 32, qw1 = qw0 + 31;  // this wave's queries
   const bool wave_all_video = qw0 >= a.T && qw1 < N;
   const int wqs = a.frame_len ? rule.frame_start(qw0) : 0;
   const bool wave_one_frame = wave_all_video && a.frame_len && rule.frame_start(qw1) == wqs;
   const QueryRange qrange = query_range(rule, qi);
   // Key tiles this workgroup visits (the same sequence for every wave).
-  const int wq0 = blockIdx.x * kDqBM, wq1 = min(wq0 + kDqBM, N);
-  auto next_tile = [&](int kt) {
-    while (kt < a.ntile && !rule.key_tile_needed(kt * kBN, wq0, wq1)) ++kt;
-    return kt;
-  };
+  const int wq0 = gp.x * kDqBM;
+  const TileRuns runs = rule.key_tiles(wq0, min(wq0 + kDqBM, N), a.ntile);
+  auto next_tile = [&](int kt) { return runs.next(kt); };
   auto issue = [&](int kt, int st) {
     VC_LDS char* sk = (VC_LDS char*)smem + st * STAGE;
     for (int idx = w; idx < RCOPIES; idx += kDqWaves) {
@@ -412,8 +479,9 @@ hipError_t launch_bwd_prepare(const __bf16* o, const float* lse, const __bf16* d
 }
 
 hipError_t launch_bwd_dkdv(const DkdvArgs& a, int head_dim, hipStream_t s) {
-  dim3 grid((a.N + kBKV - 1) / kBKV, a.H, a.B);
   const bool spatial = a.frame_len > 0;
+  const bool split = spatial && a.text_chunks > 1;
+  dim3 grid((a.N + kBKV - 1) / kBKV + (split ? (a.text_chunks - 1) * a.text_blocks : 0), a.H, a.B);
   if (head_dim == 128 && spatial)
     hipLaunchKernelGGL((bwd_dkdv_kernel<128, true>), grid, dim3(64 * kDkdvWaves), 0, s, a);
   else if (head_dim == 128)
@@ -422,6 +490,17 @@ hipError_t launch_bwd_dkdv(const DkdvArgs& a, int head_dim, hipStream_t s) {
     hipLaunchKernelGGL((bwd_dkdv_kernel<64, true>), grid, dim3(64 * kDkdvWaves), 0, s, a);
   else
     hipLaunchKernelGGL((bwd_dkdv_kernel<64, false>), grid, dim3(64 * kDkdvWaves), 0, s, a);
+  if (split) {
+    const int rows = a.text_blocks * kBKV;
+    const size_t threads = (size_t)a.B * a.H * std::min(rows, a.N) * (head_dim / 4);
+    dim3 rgrid((unsigned)((threads + 255) / 256));
+    if (head_dim == 128)
+      hipLaunchKernelGGL(text_reduce_kernel<128>, rgrid, dim3(256), 0, s, a.text_part, a.dk, a.dv, a.B, a.H, a.N,
+                         rows, a.text_chunks);
+    else
+      hipLaunchKernelGGL(text_reduce_kernel<64>, rgrid, dim3(256), 0, s, a.text_part, a.dk, a.dv, a.B, a.H, a.N,
+                         rows, a.text_chunks);
+  }
   return hipGetLastError();
 }
 

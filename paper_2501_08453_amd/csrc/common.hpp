@@ -145,6 +145,33 @@ __host__ __device__ constexpr int tok_pos(int t) {
   return (t & ~15) | (((t >> 2) & 3) == 1 ? 8 : ((t >> 2) & 3) == 2 ? 4 : ((t >> 2) & 3) * 4) | (t & 3);
 }
 
+// The tiles a workgroup visits along the other token axis: [0, a1) and [b0, b1) (the runs
+// may overlap), so that the next tile is found without scanning the skipped ones.
+struct TileRuns {
+  int a1, b0, b1, n;
+  // First visited tile >= t, or n when there is none.
+  __device__ __forceinline__ int next(int t) const { return t < a1 ? t : (t < b1 ? max(t, b0) : n); }
+};
+
+// Workgroups are dispatched round-robin over the XCDs, each with its own L2. With `remap`,
+// renumber the flattened grid so that each XCD runs one contiguous range of it: in the
+// spatial branch the workgroups of one frame, which read the same key/value (or query)
+// tiles, then share an L2. Joint attention keeps the dispatch order: there every
+// workgroup of a head reads all of its tiles, and the XCDs working on the same head at the
+// same time share them through the memory-side cache (renumbering spreads the XCDs over
+// eight heads and costs ~7% in the key-stationary kernel). Returns (x, y, z).
+constexpr int kXcds = 8;
+__device__ __forceinline__ int3 xcd_grid_pos(bool remap) {
+  if (!remap) return int3{(int)blockIdx.x, (int)blockIdx.y, (int)blockIdx.z};
+  const int X = gridDim.x, Y = gridDim.y;
+  const int G = X * Y * gridDim.z;
+  const int i = blockIdx.x + X * (blockIdx.y + Y * blockIdx.z);
+  const int q = G / kXcds, r = G % kXcds;
+  const int xcd = i % kXcds, slot = i / kXcds;
+  const int l = xcd < r ? xcd * (q + 1) + slot : r * (q + 1) + (xcd - r) * q + slot;
+  return int3{l % X, (l / X) % Y, l / (X * Y)};
+}
+
 // Which (query, key) pairs attend. Key j of a sample is *valid* if j < N, it is not padded
 // text (j >= T or j < tl) and key_mask keeps it. In joint attention every query sees every
 // valid key. In the spatial branch (frame length L > 0) only video queries attend, to the
@@ -158,28 +185,27 @@ struct AttendRule {
     if (km) ok = ok & (km[min(j, N - 1)] != 0);  // unconditional clamped load
     return ok;
   }
-  // Tiles [k0, k0+64) of keys a workgroup of queries [q0, q1) must visit; uniform across
-  // the workgroup. Joint: all but tiles of padded text only (when there is no key_mask).
-  // Spatial: the real text tiles and the tiles of the frames its video queries lie in.
-  __device__ __forceinline__ bool key_tile_needed(int k0, int q0, int q1) const {
-    if (L == 0) return km || !(k0 >= tl && k0 + kTileTok <= T);
+  // Key tiles a workgroup of queries [q0, q1) visits; uniform across the workgroup. Joint:
+  // all but tiles of padded text only (when there is no key_mask). Spatial: the real text
+  // tiles and the tiles of the frames its video queries lie in.
+  __device__ __forceinline__ TileRuns key_tiles(int q0, int q1, int ntile) const {
+    const int text_tiles = ((km ? T : tl) + kTileTok - 1) / kTileTok;
+    if (L == 0) return km ? TileRuns{0, 0, ntile, ntile} : TileRuns{text_tiles, T / kTileTok, ntile, ntile};
     const int v0 = max(q0, T);
-    if (v0 >= q1) return false;
+    if (v0 >= q1) return TileRuns{0, 0, 0, ntile};
     const int lo = frame_start(v0), hi = min(N, frame_start(q1 - 1) + L);
-    const bool text = k0 < T && (km || k0 < tl);
-    return text || (k0 + kTileTok > lo && k0 < hi);
+    return TileRuns{text_tiles, lo / kTileTok, (hi + kTileTok - 1) / kTileTok, ntile};
   }
-  // Tiles of queries a workgroup of keys [k0, k1) must visit (key-stationary kernels).
-  // Spatial: all video query tiles if it holds real text keys, else the tiles of its
-  // keys' frames; never a tile of text queries only.
-  __device__ __forceinline__ bool query_tile_needed(int q0, int k0, int k1) const {
-    if (L == 0) return true;
-    if (q0 + kTileTok <= T) return false;
-    if (k0 < T && (km || k0 < tl)) return true;
+  // Query tiles a workgroup of keys [k0, k1) visits (key-stationary kernels). Spatial: all
+  // video query tiles if it holds real text keys, else the tiles of its keys' frames; never
+  // a tile of text queries only.
+  __device__ __forceinline__ TileRuns query_tiles(int k0, int k1, int ntile) const {
+    if (L == 0) return TileRuns{0, 0, ntile, ntile};
+    if (k0 < T && (km || k0 < tl)) return TileRuns{0, T / kTileTok, ntile, ntile};
     const int v0 = max(k0, T);
-    if (v0 >= k1) return false;
+    if (v0 >= k1) return TileRuns{0, 0, 0, ntile};
     const int lo = frame_start(v0), hi = min(N, frame_start(k1 - 1) + L);
-    return q0 + kTileTok > lo && q0 < hi;
+    return TileRuns{0, lo / kTileTok, (hi + kTileTok - 1) / kTileTok, ntile};
   }
 };
 
@@ -236,7 +262,15 @@ struct DkdvArgs {
   int frame_len;        // 0: joint attention; > 0: spatial branch
   float scale;          // softmax scale
   float scale_log2;     // scale * log2(e)
+  // Spatial branch, key blocks holding text keys (the first text_blocks): their video query
+  // tiles are split into text_chunks runs of text_span tiles, one workgroup each, writing
+  // fp32 partial dK, dV (scaled) to text_part, [2][text_chunks][B][H][text_blocks*256][D]
+  // (dK partials, then dV). text_chunks = 1: no split, text_part unused.
+  float* text_part;
+  int text_blocks, text_chunks, text_span;
 };
+
+constexpr int kDkdvKeys = 256;  // keys per dK/dV workgroup
 
 // Backward, query-stationary part: dQ.
 struct DqArgs {

@@ -178,13 +178,14 @@ __global__ __launch_bounds__(64 * kWaves, kWavesPerSimd * 4 / kWaves) void fwd_k
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index (uniform)
   const int l32 = lane & 31;
   const int hi = lane >> 5;
-  const int h = blockIdx.y;
-  const int b = blockIdx.z;
+  const int3 gp = xcd_grid_pos(a.frame_len != 0);
+  const int h = gp.y;
+  const int b = gp.z;
   const int N = a.N;
   const size_t tok = (size_t)a.H * D;
   const size_t base = (size_t)b * N * tok + (size_t)h * D;
   const __bf16* vt_bh = a.vt + ((size_t)b * a.H + h) * a.ntile * tile_elems(D);
-  const int qi = blockIdx.x * kBM + w * 32 + l32;
+  const int qi = gp.x * kBM + w * 32 + l32;
 
   // Q^T as the B operand: lane holds query qi, dims 16*ks + 8*hi .. +7.
   bf16x8 qf[D / 16];
@@ -202,18 +203,16 @@ __global__ __launch_bounds__(64 * kWaves, kWavesPerSimd * 4 / kWaves) void fwd_k
   mask.rule.km = a.key_mask ? a.key_mask + (size_t)b * N : nullptr;
   mask.qr = query_range(mask.rule, qi);
   {
-    const int qw0 = blockIdx.x * kBM + w * 32, qw1 = qw0 + 31;  // this wave's queries
+    const int qw0 = gp.x * kBM + w * 32, qw1 = qw0 + 31;  // this wave's queries
     mask.wave_all_video = qw0 >= a.T && qw1 < N;
     mask.wqs = a.frame_len ? mask.rule.frame_start(qw0) : 0;
     mask.wave_one_frame = mask.wave_all_video && a.frame_len && mask.rule.frame_start(qw1) == mask.wqs;
   }
   // Key tiles this workgroup visits (the same sequence for every wave): all but tiles of
   // padded text only in joint attention; text and own-frame tiles in the spatial branch.
-  const int wq0 = blockIdx.x * kBM, wq1 = min(wq0 + kBM, N);
-  auto next_tile = [&](int kt) {
-    while (kt < a.ntile && !mask.rule.key_tile_needed(kt * kBN, wq0, wq1)) ++kt;
-    return kt;
-  };
+  const int wq0 = gp.x * kBM;
+  const TileRuns runs = mask.rule.key_tiles(wq0, min(wq0 + kBM, N), a.ntile);
+  auto next_tile = [&](int kt) { return runs.next(kt); };
   // Copies tile kt's K rows (rows past N repeat row N-1 and are masked) or V^T tile into
   // ring slot `slot`.
   auto issue_k = [&](int kt, int slot) {

@@ -32,7 +32,7 @@ def test_exports_every_declared_function(lib):
 
 
 def test_version_and_strings(lib):
-    assert vc.vc_jointattn_abi_version() == 2
+    assert vc.vc_jointattn_abi_version() == 3
     for code in vc.STATUS:
         assert isinstance(vc.vc_status_string(code), str) and vc.vc_status_string(code)
     assert vc.vc_status_string(12345) == "unknown status"
@@ -52,6 +52,15 @@ def test_tokens_and_workspace():
     assert vc.vc_jointattn_bwd_workspace_bytes(d3) == 2 * rows + 3 * tiles
     assert vc.vc_jointattn_tokens(good_desc(head_dim=96)) == -3
     assert vc.vc_jointattn_bwd_workspace_bytes(good_desc(frames=0)) == 0
+    # spatial: the 900 video query tiles of the text key block split into 16 chunks of
+    # about one frame (57 tiles), fp32 partial dK and dV of its 256 keys per chunk
+    part = 2 * 16 * 24 * 256 * 128 * 4
+    assert vc.vc_spatialattn_bwd_workspace_bytes(d3) == 2 * rows + 3 * tiles + part
+    # no text, or too few video tiles to split: the joint size
+    for kw in (dict(text_slot=0), dict()):
+        dd = good_desc(**kw)
+        assert vc.vc_spatialattn_bwd_workspace_bytes(dd) == vc.vc_jointattn_bwd_workspace_bytes(dd)
+    assert vc.vc_spatialattn_bwd_workspace_bytes(good_desc(frames=0)) == 0
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -97,6 +106,14 @@ def test_workspace_checks(lib):
     fneed = vc.vc_jointattn_fwd_workspace_bytes(d)
     assert lib.vc_jointattn_fwd(ctypes.byref(d), p, p, p, None, None, p, p, None, fneed, None) == -5
     assert lib.vc_jointattn_fwd(ctypes.byref(d), p, p, p, None, None, p, p, p, fneed - 1, None) == -5
+    # the spatial backward needs more than the joint workspace when its text keys are split
+    # (long video: 16 chunks); rejected before anything runs
+    d3 = vc.make_desc(1, 24, 128, 256, 16, 45, 80)
+    joint, spatial = vc.vc_jointattn_bwd_workspace_bytes(d3), vc.vc_spatialattn_bwd_workspace_bytes(d3)
+    assert spatial > joint
+    assert lib.vc_spatialattn_bwd(ctypes.byref(d3), p, p, p, p, p, p, None, None, p, p, p, p, joint, None) == -5
+    assert lib.vc_spatialattn_bwd(ctypes.byref(d3), p, p, p, p, p, p, None, None, p, p, p, p, spatial - 1,
+                                  None) == -5
 
 
 def test_no_device_is_reported():

@@ -48,6 +48,12 @@ SMALL = [
     ("T256-F5-L64", 1, 2, 128, 256, 5, 8, 8, True, False),
     ("T40-F1-L200", 2, 1, 128, 40, 1, 10, 20, False, True),
     ("T8-F7-L33", 1, 2, 64, 8, 7, 3, 11, True, True),
+    # text key blocks whose video query tiles are split over several workgroups (fp32
+    # partials summed afterwards): 2 chunks; 2 text blocks, the second holding video keys
+    # of three frames; 3 chunks with a batch of 2
+    ("T100-F12-L60-split", 1, 2, 64, 100, 12, 6, 10, True, True),
+    ("T300-F9-L100-split", 1, 2, 128, 300, 9, 10, 10, True, False),
+    ("T64-F40-L30-split", 2, 1, 64, 64, 40, 5, 6, False, False),
 ]
 
 
@@ -62,6 +68,8 @@ def test_spatial_small_all_elements(case):
     km_np = W.random_key_mask(w, seed=88, keep=0.85) if masked else None
     km = None if km_np is None else torch.from_numpy(km_np).to("cuda")
     desc = vc.desc_for(w)
+    split = vc.vc_spatialattn_bwd_workspace_bytes(desc) > vc.vc_jointattn_bwd_workspace_bytes(desc)
+    assert split == name.endswith("-split")
     out = _run(desc, g, tl_d, km)
     o, lse = orb.spatial_forward(h["q"], h["k"], h["v"], T, F, tl, km_np)
     dq, dk, dv = orb.spatial_backward(h["q"], h["k"], h["v"], h["do"], T, F, tl, km_np, lse=lse)
