@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define VC_JOINTATTN_ABI_VERSION 3
+#define VC_JOINTATTN_ABI_VERSION 4
 
 typedef enum vc_status {
   VC_OK = 0,
@@ -68,7 +68,8 @@ typedef enum vc_status {
   VC_ERR_WORKSPACE = -5,   /* workspace NULL or smaller than required          */
   VC_ERR_DEVICE = -6,      /* no current HIP device, or it is not gfx950       */
   VC_ERR_HIP = -7,         /* a HIP launch reported an error                   */
-  VC_ERR_UNSUPPORTED = -8  /* a requested mode is not available                */
+  VC_ERR_UNSUPPORTED = -8, /* a requested mode is not available                */
+  VC_ERR_ALIAS = -9        /* an output is the same buffer as another output   */
 } vc_status;
 
 /* Problem descriptor (passed by pointer, read only during the call). */
@@ -213,6 +214,18 @@ vc_status vc_temporalattn_fwd(const vc_jointattn_desc* desc,
                               const uint8_t* key_mask,
                               void* o, float* lse, void* stream);
 
+/* Temporal forward with the branch sum fused into its epilogue: as
+ * vc_temporalattn_fwd, and in the same pass out = o_joint + o_spatial + o over
+ * every row (this branch's o is 0 on text rows), with the arithmetic of
+ * vc_branchsum, so `out` is bitwise what vc_branchsum(o_joint, o_spatial, o)
+ * would write. o_joint or o_spatial may be NULL (zero); out may be o_joint or
+ * o_spatial (in-place accumulation) but not o (VC_ERR_ALIAS). */
+vc_status vc_temporalattn_fwd_sum(const vc_jointattn_desc* desc,
+                                  const void* q, const void* k, const void* v,
+                                  const uint8_t* key_mask,
+                                  const void* o_joint, const void* o_spatial,
+                                  void* o, float* lse, void* out, void* stream);
+
 /* Bytes of device workspace the temporal backward needs: per row fp32 D and
  * LSE*log2(e) ([B,H,Npad]). 0 for an invalid descriptor. Host only. */
 size_t vc_temporalattn_bwd_workspace_bytes(const vc_jointattn_desc* desc);
@@ -226,6 +239,21 @@ vc_status vc_temporalattn_bwd(const vc_jointattn_desc* desc,
                               const uint8_t* key_mask,
                               void* dq, void* dk, void* dv,
                               void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Branch sum (Sec. III-B: the outputs of the spatial, temporal and
+ * full-sequence branches are added element-wise to form the block's attention
+ * output). The backward of the sum needs no kernel: every branch's backward
+ * takes the same dout.
+ * ------------------------------------------------------------------------- */
+
+/* out = o_joint + o_spatial + o_temporal, element-wise over [B,N,H,D] bf16: each
+ * element is summed in fp32 in that order and rounded once to bf16 (nearest
+ * even). Any input may be NULL (a branch the model does not run counts as
+ * zero), but not all three (VC_ERR_NULL); out may be one of the inputs. */
+vc_status vc_branchsum(const vc_jointattn_desc* desc,
+                       const void* o_joint, const void* o_spatial, const void* o_temporal,
+                       void* out, void* stream);
 
 #ifdef __cplusplus
 }

@@ -19,6 +19,7 @@ VC_OK = 0
 STATUS = {
     0: "VC_OK", -1: "VC_ERR_NULL", -2: "VC_ERR_SHAPE", -3: "VC_ERR_HEAD_DIM", -4: "VC_ERR_ALIGN",
     -5: "VC_ERR_WORKSPACE", -6: "VC_ERR_DEVICE", -7: "VC_ERR_HIP", -8: "VC_ERR_UNSUPPORTED",
+    -9: "VC_ERR_ALIAS",
 }
 
 
@@ -61,6 +62,8 @@ _SIGS = {
     "vc_spatialattn_bwd_workspace_bytes": (ctypes.c_size_t, [_DP]),
     "vc_spatialattn_bwd": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "vc_temporalattn_fwd": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P]),
+    "vc_temporalattn_fwd_sum": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
+    "vc_branchsum": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P]),
     "vc_temporalattn_bwd_workspace_bytes": (ctypes.c_size_t, [_DP]),
     "vc_temporalattn_bwd": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
 }
@@ -198,6 +201,16 @@ def vc_temporalattn_fwd(desc, q, k, v, key_mask, o, lse, stream=None):
           _stream(stream))
 
 
+def vc_temporalattn_fwd_sum(desc, q, k, v, key_mask, o_joint, o_spatial, o, lse, out, stream=None):
+    _call("vc_temporalattn_fwd_sum", ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(key_mask), _ptr(o_joint),
+          _ptr(o_spatial), _ptr(o), _ptr(lse), _ptr(out), _stream(stream))
+
+
+def vc_branchsum(desc, o_joint, o_spatial, o_temporal, out, stream=None):
+    _call("vc_branchsum", ctypes.byref(desc), _ptr(o_joint), _ptr(o_spatial), _ptr(o_temporal), _ptr(out),
+          _stream(stream))
+
+
 def vc_temporalattn_bwd_workspace_bytes(desc) -> int:
     return _lib().vc_temporalattn_bwd_workspace_bytes(ctypes.byref(desc))
 
@@ -324,6 +337,32 @@ def temporal_fwd(q, k, v, desc, key_mask=None, out=None, lse=None):
     lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device) if lse is None else lse
     vc_temporalattn_fwd(desc, q, k, v, key_mask, o, lse)
     return o, lse
+
+
+def temporal_fwd_sum(q, k, v, desc, o_joint=None, o_spatial=None, key_mask=None, out=None):
+    """Temporal branch (o, lse) and the block sum o_joint + o_spatial + o in one pass."""
+    import torch
+    B, N, H, D = _check_branch_inputs(desc, (("q", q), ("k", k), ("v", v)), key_mask)
+    for name, t in (("o_joint", o_joint), ("o_spatial", o_spatial)):
+        if t is not None:
+            _check_tensor(name, t, (B, N, H, D), torch.bfloat16)
+    o = torch.empty_like(q)
+    lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    out = torch.empty_like(q) if out is None else out
+    vc_temporalattn_fwd_sum(desc, q, k, v, key_mask, o_joint, o_spatial, o, lse, out)
+    return o, lse, out
+
+
+def branch_sum(desc, o_joint=None, o_spatial=None, o_temporal=None, out=None):
+    """Block output o_joint + o_spatial + o_temporal (bf16, summed in fp32, one rounding)."""
+    import torch
+    first = next(t for t in (o_joint, o_spatial, o_temporal) if t is not None)
+    for name, t in (("o_joint", o_joint), ("o_spatial", o_spatial), ("o_temporal", o_temporal)):
+        if t is not None:
+            _check_tensor(name, t, tuple(first.shape), torch.bfloat16)
+    out = torch.empty_like(first) if out is None else out
+    vc_branchsum(desc, o_joint, o_spatial, o_temporal, out)
+    return out
 
 
 def temporal_bwd(q, k, v, o, lse, dout, desc, key_mask=None, ws=None):

@@ -164,6 +164,7 @@ const char* vc_status_string(int status) {
     case VC_ERR_DEVICE: return "no current HIP device, or it is not gfx950";
     case VC_ERR_HIP: return "a HIP kernel launch failed";
     case VC_ERR_UNSUPPORTED: return "requested mode is not available";
+    case VC_ERR_ALIAS: return "an output is the same buffer as another output";
     default: return "unknown status";
   }
 }
@@ -397,14 +398,23 @@ vc_status vc_spatialattn_bwd(const vc_jointattn_desc* desc, const void* q, const
                   true);
 }
 
-vc_status vc_temporalattn_fwd(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
-                              const uint8_t* key_mask, void* o, float* lse, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Temporal forward; with `out`, also the branch sum out = o_joint + o_spatial + o.
+vc_status temporal_fwd_impl(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
+                            const uint8_t* key_mask, const void* o_joint, const void* o_spatial, void* o, float* lse,
+                            void* out, void* stream) {
   int64_t n = 0;
   vc_status st = check_desc(desc, &n);
   if (st != VC_OK) return st;
   if (desc->frames > kMaxTemporalFrames) return VC_ERR_SHAPE;
   if (!q || !k || !v || !o || !lse) return VC_ERR_NULL;
-  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse)) return VC_ERR_ALIGN;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse) || !aligned16(o_joint) ||
+      !aligned16(o_spatial) || !aligned16(out))
+    return VC_ERR_ALIGN;
+  if (out && out == o) return VC_ERR_ALIAS;
   if ((st = check_device()) != VC_OK) return st;
   vcja::TemporalArgs a = temporal_args(desc, n);
   a.q = bf(q);
@@ -413,11 +423,49 @@ vc_status vc_temporalattn_fwd(const vc_jointattn_desc* desc, const void* q, cons
   a.key_mask = key_mask;
   a.o = static_cast<__bf16*>(o);
   a.lse = lse;
+  a.sum_a = bf(o_joint);
+  a.sum_b = bf(o_spatial);
+  a.sum_out = static_cast<__bf16*>(out);
   hipStream_t s = as_stream(stream);
-  if (vcja::launch_text_rows(a.o, nullptr, nullptr, lse, a.B, a.H, a.N, a.T, desc->head_dim, s) != hipSuccess ||
-      vcja::launch_temporal_fwd(a, desc->head_dim, s) != hipSuccess)
+  if (vcja::launch_text_rows(a.o, nullptr, nullptr, lse, a.B, a.H, a.N, a.T, desc->head_dim, s) != hipSuccess)
     return VC_ERR_HIP;
+  // text rows of the sum: this branch contributes zero there
+  if (out && vcja::launch_branch_sum(a.sum_a, a.sum_b, nullptr, a.sum_out, a.B, a.N, a.T, a.H * desc->head_dim, s) !=
+                 hipSuccess)
+    return VC_ERR_HIP;
+  if (vcja::launch_temporal_fwd(a, desc->head_dim, s) != hipSuccess) return VC_ERR_HIP;
   return VC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+vc_status vc_temporalattn_fwd(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
+                              const uint8_t* key_mask, void* o, float* lse, void* stream) {
+  return temporal_fwd_impl(desc, q, k, v, key_mask, nullptr, nullptr, o, lse, nullptr, stream);
+}
+
+vc_status vc_temporalattn_fwd_sum(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
+                                  const uint8_t* key_mask, const void* o_joint, const void* o_spatial, void* o,
+                                  float* lse, void* out, void* stream) {
+  if (!out) return VC_ERR_NULL;
+  return temporal_fwd_impl(desc, q, k, v, key_mask, o_joint, o_spatial, o, lse, out, stream);
+}
+
+vc_status vc_branchsum(const vc_jointattn_desc* desc, const void* o_joint, const void* o_spatial,
+                       const void* o_temporal, void* out, void* stream) {
+  int64_t n = 0;
+  vc_status st = check_desc(desc, &n);
+  if (st != VC_OK) return st;
+  if (!out || (!o_joint && !o_spatial && !o_temporal)) return VC_ERR_NULL;
+  if (!aligned16(o_joint) || !aligned16(o_spatial) || !aligned16(o_temporal) || !aligned16(out)) return VC_ERR_ALIGN;
+  if ((st = check_device()) != VC_OK) return st;
+  const int rows = (int)n;
+  return vcja::launch_branch_sum(bf(o_joint), bf(o_spatial), bf(o_temporal), static_cast<__bf16*>(out),
+                                 desc->batch, rows, rows, desc->heads * desc->head_dim, as_stream(stream)) == hipSuccess
+             ? VC_OK
+             : VC_ERR_HIP;
 }
 
 size_t vc_temporalattn_bwd_workspace_bytes(const vc_jointattn_desc* desc) {

@@ -304,6 +304,11 @@ struct TemporalArgs {
   float* lse;           // forward output
   __bf16* dk;           // backward
   __bf16* dv;           // backward
+  // Forward with the branch sum fused into the epilogue (sum_out non-NULL): also writes
+  // sum_out = sum_a + sum_b + o for the video rows (a NULL input counts as zero).
+  const __bf16* sum_a;
+  const __bf16* sum_b;
+  __bf16* sum_out;
   int B, H, N, T, F, L, G, npad;
   float scale;
   float scale_log2;
@@ -322,6 +327,11 @@ hipError_t launch_bwd_dkdv(const DkdvArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_bwd_dq(const DqArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_temporal_fwd(const TemporalArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_temporal_bwd(const TemporalArgs& a, int head_dim, hipStream_t s);
+// out = a + b + c over rows [0, rows) of every sample of [B, N, H, D] tensors (row_elems =
+// H*D); each element summed in fp32 in that order and rounded once to bf16. A NULL input
+// counts as zero; out may be one of the inputs.
+hipError_t launch_branch_sum(const __bf16* a, const __bf16* b, const __bf16* c, __bf16* out, int B, int N, int rows,
+                             int row_elems, hipStream_t s);
 // Rows [0, T) of up to three [B, N, H, D] tensors set to zero and, if lse is given, their
 // LSE ([B, H, N]) to -inf.
 hipError_t launch_text_rows(__bf16* x0, __bf16* x1, __bf16* x2, float* lse, int B, int H, int N, int T, int head_dim,

@@ -39,7 +39,17 @@ __device__ __forceinline__ int acc_slot(int r, int hi) { return acc_row(r, hi); 
 // accumulator rows of 8 consecutive registers are numbered.
 __device__ __forceinline__ int op_slot(int st, int t, int hi) { return 16 * st + 8 * (t >> 2) + 4 * hi + (t & 3); }
 
-template <int D>
+// Sum of three bf16 values in fp32, in argument order, rounded once (a NULL source counts as
+// zero): the arithmetic shared by the branch-sum kernel and the fused epilogue.
+__device__ __forceinline__ void add_bf16x4(f32x4& acc, bf16x4 x) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) acc[i] += (float)x[i];
+}
+__device__ __forceinline__ void add_bf16x4(f32x4& acc, const __bf16* src) {
+  if (src) add_bf16x4(acc, *(const bf16x4*)src);
+}
+
+template <int D, bool SUM>
 __global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_fwd_kernel(TemporalArgs a) {
   const int lane = threadIdx.x & 63;
   const int l32 = lane & 31;
@@ -116,7 +126,16 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_fwd_kernel(Tempo
       for (int j = 0; j < 4; ++j) {
         bf16x4 o4 = {(__bf16)(oacc[4 * j + 0] * inv), (__bf16)(oacc[4 * j + 1] * inv),
                      (__bf16)(oacc[4 * j + 2] * inv), (__bf16)(oacc[4 * j + 3] * inv)};
-        *(bf16x4*)(op + db * 32 + 8 * j + 4 * hi) = o4;
+        const size_t e = db * 32 + 8 * j + 4 * hi;
+        *(bf16x4*)(op + e) = o4;
+        if (SUM) {  // branch sum: (a + b) + o, o as stored
+          const size_t off = base + (size_t)n * tok + e;
+          f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+          add_bf16x4(acc, a.sum_a ? a.sum_a + off : nullptr);
+          add_bf16x4(acc, a.sum_b ? a.sum_b + off : nullptr);
+          add_bf16x4(acc, o4);
+          *(bf16x4*)(a.sum_out + off) = bf16x4{(__bf16)acc[0], (__bf16)acc[1], (__bf16)acc[2], (__bf16)acc[3]};
+        }
       }
     }
   }
@@ -264,6 +283,22 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_bwd_kernel(Tempo
   }
 }
 
+// out = a + b + c (fp32, in that order, one rounding) over rows [0, rows) of each sample;
+// one thread per 4 elements.
+__global__ __launch_bounds__(256) void branch_sum_kernel(const __bf16* a, const __bf16* b, const __bf16* c,
+                                                         __bf16* out, int B, int N, int rows, int row_elems) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int per_row = row_elems / 4;
+  if (i >= (size_t)B * rows * per_row) return;
+  const size_t r = i / per_row;
+  const size_t off = ((r / rows) * N + r % rows) * row_elems + (i % per_row) * 4;
+  f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+  add_bf16x4(acc, a ? a + off : nullptr);
+  add_bf16x4(acc, b ? b + off : nullptr);
+  add_bf16x4(acc, c ? c + off : nullptr);
+  *(bf16x4*)(out + off) = bf16x4{(__bf16)acc[0], (__bf16)acc[1], (__bf16)acc[2], (__bf16)acc[3]};
+}
+
 // Zero rows [0, T) of up to three tensors and set their LSE to -inf.
 template <int D>
 __global__ __launch_bounds__(256) void text_rows_kernel(__bf16* x0, __bf16* x1, __bf16* x2, float* lse, int B, int H,
@@ -292,10 +327,24 @@ __global__ __launch_bounds__(256) void text_rows_kernel(__bf16* x0, __bf16* x1, 
 hipError_t launch_temporal_fwd(const TemporalArgs& a, int head_dim, hipStream_t s) {
   const int nblk = (a.L + a.G - 1) / a.G;
   dim3 grid((nblk + kWavesPerBlock - 1) / kWavesPerBlock, a.H, a.B);
-  if (head_dim == 128)
-    hipLaunchKernelGGL(temporal_fwd_kernel<128>, grid, dim3(64 * kWavesPerBlock), 0, s, a);
+  const bool sum = a.sum_out != nullptr;
+  if (head_dim == 128 && sum)
+    hipLaunchKernelGGL((temporal_fwd_kernel<128, true>), grid, dim3(64 * kWavesPerBlock), 0, s, a);
+  else if (head_dim == 128)
+    hipLaunchKernelGGL((temporal_fwd_kernel<128, false>), grid, dim3(64 * kWavesPerBlock), 0, s, a);
+  else if (sum)
+    hipLaunchKernelGGL((temporal_fwd_kernel<64, true>), grid, dim3(64 * kWavesPerBlock), 0, s, a);
   else
-    hipLaunchKernelGGL(temporal_fwd_kernel<64>, grid, dim3(64 * kWavesPerBlock), 0, s, a);
+    hipLaunchKernelGGL((temporal_fwd_kernel<64, false>), grid, dim3(64 * kWavesPerBlock), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_branch_sum(const __bf16* a, const __bf16* b, const __bf16* c, __bf16* out, int B, int N, int rows,
+                             int row_elems, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  const size_t threads = (size_t)B * rows * (row_elems / 4);
+  hipLaunchKernelGGL(branch_sum_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s, a, b, c, out, B, N,
+                     rows, row_elems);
   return hipGetLastError();
 }
 

@@ -32,7 +32,7 @@ def test_exports_every_declared_function(lib):
 
 
 def test_version_and_strings(lib):
-    assert vc.vc_jointattn_abi_version() == 3
+    assert vc.vc_jointattn_abi_version() == 4
     for code in vc.STATUS:
         assert isinstance(vc.vc_status_string(code), str) and vc.vc_status_string(code)
     assert vc.vc_status_string(12345) == "unknown status"
@@ -150,3 +150,18 @@ def test_temporal_argument_errors(lib):
     assert lib.vc_temporalattn_bwd(ctypes.byref(d), p, p, p, p, p, p, None, p, p, p, p, need - 1, None) == -5
     assert lib.vc_temporalattn_bwd(ctypes.byref(d), p, p, p, p, p, None, None, p, p, p, p, need, None) == -1
     assert vc.vc_temporalattn_bwd_workspace_bytes(good_desc(batch=0)) == 0
+
+
+def test_branch_sum_argument_errors(lib):
+    d = good_desc()
+    p = 1 << 20
+    # nothing to sum, or no output
+    assert lib.vc_branchsum(ctypes.byref(d), None, None, None, p, None) == -1
+    assert lib.vc_branchsum(ctypes.byref(d), p, p, p, None, None) == -1
+    assert lib.vc_branchsum(ctypes.byref(d), p, p + 8, None, p, None) == -4
+    assert lib.vc_branchsum(ctypes.byref(good_desc(heads=0)), p, p, p, p, None) == -2
+    # fused temporal forward + sum: out required, must not be this branch's o
+    assert lib.vc_temporalattn_fwd_sum(ctypes.byref(d), p, p, p, None, p, p, p, p, None, None) == -1
+    assert lib.vc_temporalattn_fwd_sum(ctypes.byref(d), p, p, p, None, p, p, p, p, p, None) == -9
+    assert lib.vc_temporalattn_fwd_sum(ctypes.byref(d), p, p, p, None, p + 2, None, p, p, p * 2, None) == -4
+    assert vc.vc_status_string(-9) == "an output is the same buffer as another output"
