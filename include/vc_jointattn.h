@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define VC_JOINTATTN_ABI_VERSION 4
+#define VC_JOINTATTN_ABI_VERSION 5
 
 typedef enum vc_status {
   VC_OK = 0,
@@ -254,6 +254,43 @@ vc_status vc_temporalattn_bwd(const vc_jointattn_desc* desc,
 vc_status vc_branchsum(const vc_jointattn_desc* desc,
                        const void* o_joint, const void* o_spatial, const void* o_temporal,
                        void* out, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Activation offload (Sec. V-B: saved activations swapped to host memory on a
+ * separate stream, overlapped with computation, as a substitute for
+ * recomputation in selected layers; compared in Sec. VI-D). An engine owns one
+ * copy stream (default priority) and two events; copies run on it and never
+ * block the host.
+ *  - Ordering: a store or load starts only after all work the caller queued on
+ *    `stream` before the call (so a tensor a kernel writes on `stream` can be
+ *    stored right after the launch). vc_offload_wait makes `stream` wait for
+ *    every copy issued so far: a stored device buffer may be overwritten, and a
+ *    loaded one read, on `stream` only after that wait.
+ *  - Memory: host buffers must be pinned (hipHostMalloc, or torch's
+ *    pin_memory); device buffers must be device memory of the engine's device.
+ *    Each [ptr, ptr + bytes) must lie inside one allocation. Otherwise
+ *    VC_ERR_UNSUPPORTED and nothing is issued. A call from another current
+ *    device than the engine's: VC_ERR_DEVICE.
+ *  - An engine is not thread-safe; use one per thread. bytes = 0 is a no-op.
+ * ------------------------------------------------------------------------- */
+typedef struct vc_offload vc_offload;
+
+/* Creates an engine on the current device; *out receives it (NULL on error). */
+vc_status vc_offload_create(vc_offload** out);
+
+/* Waits for the engine's copies to finish, then frees it. */
+vc_status vc_offload_destroy(vc_offload* h);
+
+/* Device -> pinned host copy of `bytes` bytes, ordered after `stream`'s work. */
+vc_status vc_offload_store(vc_offload* h, void* host_dst, const void* dev_src, size_t bytes,
+                           void* stream);
+
+/* Pinned host -> device copy of `bytes` bytes, ordered after `stream`'s work. */
+vc_status vc_offload_load(vc_offload* h, void* dev_dst, const void* host_src, size_t bytes,
+                          void* stream);
+
+/* Makes `stream` wait (on the device) for every copy issued so far. */
+vc_status vc_offload_wait(vc_offload* h, void* stream);
 
 #ifdef __cplusplus
 }

@@ -64,6 +64,11 @@ _SIGS = {
     "vc_temporalattn_fwd": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P]),
     "vc_temporalattn_fwd_sum": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
     "vc_branchsum": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P]),
+    "vc_offload_create": (ctypes.c_int, [ctypes.POINTER(ctypes.c_void_p)]),
+    "vc_offload_destroy": (ctypes.c_int, [ctypes.c_void_p]),
+    "vc_offload_store": (ctypes.c_int, [ctypes.c_void_p, _P, _P, ctypes.c_size_t, _P]),
+    "vc_offload_load": (ctypes.c_int, [ctypes.c_void_p, _P, _P, ctypes.c_size_t, _P]),
+    "vc_offload_wait": (ctypes.c_int, [ctypes.c_void_p, _P]),
     "vc_temporalattn_bwd_workspace_bytes": (ctypes.c_size_t, [_DP]),
     "vc_temporalattn_bwd": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
 }
@@ -363,6 +368,46 @@ def branch_sum(desc, o_joint=None, o_spatial=None, o_temporal=None, out=None):
     out = torch.empty_like(first) if out is None else out
     vc_branchsum(desc, o_joint, o_spatial, o_temporal, out)
     return out
+
+
+class Offload:
+    """Activation offload engine (C ABI vc_offload_*): device <-> pinned host copies on a
+    copy stream of its own, ordered after the caller's stream; `wait` makes the caller's
+    stream wait for them."""
+
+    def __init__(self):
+        h = ctypes.c_void_p()
+        _call("vc_offload_create", ctypes.byref(h))
+        self._h = h
+
+    @staticmethod
+    def _bytes(a, b):
+        n = a.numel() * a.element_size()
+        if b.numel() * b.element_size() != n:
+            raise ValueError("offload copy between tensors of different sizes")
+        return n
+
+    def store(self, host, dev, stream=None):
+        """host (pinned CPU tensor) <- dev (GPU tensor), after the stream's queued work."""
+        _call("vc_offload_store", self._h, _ptr(host), _ptr(dev), self._bytes(host, dev), _stream(stream))
+
+    def load(self, dev, host, stream=None):
+        """dev (GPU tensor) <- host (pinned CPU tensor), after the stream's queued work."""
+        _call("vc_offload_load", self._h, _ptr(dev), _ptr(host), self._bytes(dev, host), _stream(stream))
+
+    def wait(self, stream=None):
+        _call("vc_offload_wait", self._h, _stream(stream))
+
+    def close(self):
+        if self._h is not None and self._h.value:
+            _call("vc_offload_destroy", self._h)
+        self._h = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
 
 
 def temporal_bwd(q, k, v, o, lse, dout, desc, key_mask=None, ws=None):

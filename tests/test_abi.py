@@ -32,7 +32,7 @@ def test_exports_every_declared_function(lib):
 
 
 def test_version_and_strings(lib):
-    assert vc.vc_jointattn_abi_version() == 4
+    assert vc.vc_jointattn_abi_version() == 5
     for code in vc.STATUS:
         assert isinstance(vc.vc_status_string(code), str) and vc.vc_status_string(code)
     assert vc.vc_status_string(12345) == "unknown status"
@@ -165,3 +165,17 @@ def test_branch_sum_argument_errors(lib):
     assert lib.vc_temporalattn_fwd_sum(ctypes.byref(d), p, p, p, None, p, p, p, p, p, None) == -9
     assert lib.vc_temporalattn_fwd_sum(ctypes.byref(d), p, p, p, None, p + 2, None, p, p, p * 2, None) == -4
     assert vc.vc_status_string(-9) == "an output is the same buffer as another output"
+
+
+def test_offload_argument_errors(lib):
+    p = 1 << 20
+    assert lib.vc_offload_create(None) == -1
+    assert lib.vc_offload_destroy(None) == -1
+    assert lib.vc_offload_wait(None, None) == -1
+    assert lib.vc_offload_store(None, p, p, 16, None) == -1
+    assert lib.vc_offload_load(None, p, p, 16, None) == -1
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        h = ctypes.c_void_p(123)
+        assert lib.vc_offload_create(ctypes.byref(h)) == -6
+        assert h.value is None
