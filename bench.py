@@ -15,6 +15,12 @@ block instead (same inputs, forward + backward): the spatial branch in
 algorithmic TFLOP/s (each video query against the valid text keys and its own
 frame), the temporal branch, which is bound by memory traffic, in algorithmic
 GB/s (bytes the step must move at least).
+
+--branch block measures the whole attention of the parallel block (the three
+branches and their fused sum) over --layers stacked layers, forward through all
+of them and backward in reverse, with the branch outputs each layer saves for
+its backward kept in HBM, recomputed before its backward, or offloaded to
+pinned host memory and loaded back (the memory strategies of Sec. V-B / VI-D).
 """
 from __future__ import annotations
 
@@ -37,6 +43,8 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E bandwidth (published)
 METRIC = "joint-attention fwd+bwd TFLOP/s and % bf16 MFMA peak at 57,856 tokens"
 METRIC_SPATIAL = "spatial-attention fwd+bwd TFLOP/s (per-frame text+frame keys)"
 METRIC_TEMPORAL = "temporal-attention fwd+bwd GB/s (algorithmic HBM bytes)"
+METRIC_BLOCK = ("parallel-block attention (joint + spatial + temporal, summed) fwd+bwd TFLOP/s; saved branch "
+                "outputs kept, recomputed or offloaded")
 
 
 def valid_keys_per_sample(w, text_len):
@@ -197,8 +205,9 @@ def main(argv=None):
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", type=int, default=W.HEADLINE, choices=sorted(W.WORKLOADS))
-    ap.add_argument("--branch", default="joint", choices=["joint", "spatial", "temporal"],
-                    help="attention branch to measure (joint = the headline)")
+    ap.add_argument("--branch", default="joint", choices=["joint", "spatial", "temporal", "block"],
+                    help="attention branch to measure (joint = the headline; block = all three and their sum)")
+    ap.add_argument("--layers", type=int, default=4, help="stacked layers for --branch block")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the oracle timing")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -232,6 +241,9 @@ def main(argv=None):
     q, k, v, do = g["q"], g["k"], g["v"], g["do"]
     stream = torch.cuda.current_stream()
     sh = stream.cuda_stream
+    if args.branch == "block":
+        del o, lse, dq, dk, dv, ws
+        return block_main(args, w, g, text_len, tl, desc, fws, stream)
     if args.branch != "joint":
         return branch_main(args, w, g, text_len, tl, desc, o, lse, dq, dk, dv, fws, ws, stream)
 
@@ -404,6 +416,153 @@ def branch_main(args, w, g, text_len, tl, desc, o, lse, dq, dk, dv, fws, ws, str
         line["cpu_baseline"] = cpu_baseline_branch(args.branch, w, g, text_len, args.cpu_seconds)
     print(json.dumps(line), flush=True)
     copy_calibration(args.copy_calibration_mib, q.device)
+    return 0
+
+
+def pcie_rates(dev, mib=1024):
+    """Device -> pinned host and pinned host -> device copy rates (GB/s) of one large copy."""
+    import torch
+    n = mib << 20
+    d = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+    h = torch.empty(n, dtype=torch.uint8, pin_memory=True)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    h.copy_(d, non_blocking=True)  # warm
+    torch.cuda.synchronize()
+    ev[0].record()
+    h.copy_(d, non_blocking=True)
+    ev[1].record()
+    d.copy_(h, non_blocking=True)
+    ev[2].record()
+    torch.cuda.synchronize()
+    return n / (ev[0].elapsed_time(ev[1]) * 1e-3) / 1e9, n / (ev[1].elapsed_time(ev[2]) * 1e-3) / 1e9
+
+
+def block_main(args, w, g, text_len, tl, desc, fws, stream):
+    """`--layers` stacked attention blocks (joint, spatial and temporal branches with the
+    sum fused into the temporal forward), forward through every layer, then backward in
+    reverse, as in a training step. q, k, v, dO are shared by the layers. Each layer saves
+    the O and LSE of its three branches for its backward:
+      keep       every layer's set stays in HBM;
+      recompute  one scratch set; a layer's three forwards run again before its backward;
+      offload    a ring of two device sets; the set of layer i is stored to pinned host
+                 memory on the offload engine's stream while layer i+1 computes, and loaded
+                 back while layer i+2's backward runs (the last two layers stay resident).
+    """
+    import torch
+    import paper_2501_08453_amd as vc
+    q, k, v, do = g["q"], g["k"], g["v"], g["do"]
+    sh = stream.cuda_stream
+    B, N, H, D = w.shape
+    K = max(1, args.layers)
+    dev = q.device
+    ws_j = vc.workspace(desc, dev)
+    ws_s = vc.spatial_workspace(desc, dev)
+    ws_t = vc._workspace(vc.vc_temporalattn_bwd_workspace_bytes(desc), dev)
+    out = torch.empty_like(q)
+    grads = [tuple(torch.empty_like(q) for _ in range(3)) for _ in range(3)]
+
+    def new_set():  # O, LSE of the joint, spatial and temporal branches
+        sv = []
+        for _ in range(3):
+            sv += [torch.empty_like(q), torch.empty((B, H, N), dtype=torch.float32, device=dev)]
+        return sv
+
+    def forward(sv):
+        o_j, l_j, o_s, l_s, o_t, l_t = sv
+        vc.vc_jointattn_fwd(desc, q, k, v, tl, None, o_j, l_j, fws, fws.numel(), sh)
+        vc.vc_spatialattn_fwd(desc, q, k, v, tl, None, o_s, l_s, fws, fws.numel(), sh)
+        vc.vc_temporalattn_fwd_sum(desc, q, k, v, None, o_j, o_s, o_t, l_t, out, sh)
+
+    def backward(sv):
+        o_j, l_j, o_s, l_s, o_t, l_t = sv
+        vc.vc_jointattn_bwd(desc, q, k, v, o_j, l_j, do, tl, None, *grads[0], ws_j, ws_j.numel(), sh)
+        vc.vc_spatialattn_bwd(desc, q, k, v, o_s, l_s, do, tl, None, *grads[1], ws_s, ws_s.numel(), sh)
+        vc.vc_temporalattn_bwd(desc, q, k, v, o_t, l_t, do, None, *grads[2], ws_t, ws_t.numel(), sh)
+
+    keep_sets = [new_set() for _ in range(K)]
+    ring = keep_sets[:2] if K >= 2 else keep_sets
+    scratch = keep_sets[0]
+    n_off = max(0, K - 2)  # layers whose set leaves the device
+    host = [[torch.empty(t.shape, dtype=t.dtype, pin_memory=True) for t in ring[0]] for _ in range(n_off)]
+    off = vc.Offload()
+
+    def step_keep():
+        for i in range(K):
+            forward(keep_sets[i])
+        for i in reversed(range(K)):
+            backward(keep_sets[i])
+
+    def step_recompute():
+        for _ in range(K):
+            forward(scratch)
+        for _ in range(K):
+            forward(scratch)
+            backward(scratch)
+
+    def step_offload():
+        for i in range(K):
+            forward(ring[i % 2])
+            if i >= 1 and i - 1 < n_off:
+                off.wait()  # layer i+1 overwrites layer i-1's set: its store must be done
+            if i < n_off:
+                for hb, t in zip(host[i], ring[i % 2]):
+                    off.store(hb, t, sh)
+        for i in reversed(range(K)):
+            if 0 <= i - 1 < n_off:  # bring layer i-1 back while layer i's backward runs
+                for hb, t in zip(host[i - 1], ring[(i - 1) % 2]):
+                    off.load(t, hb, sh)
+            backward(ring[i % 2])
+            off.wait()
+
+    modes = {"keep": step_keep, "recompute": step_recompute, "offload": step_offload}
+    times = {}
+    for name, fn in modes.items():
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            fn()
+        torch.cuda.synchronize()
+        times[name] = (time.perf_counter() - t0) * 1e3 / args.steps
+    off.close()
+    d2h, h2d = pcie_rates(dev)
+
+    fj, bj = flops(w, text_len)
+    fs, bs = spatial_flops(w, text_len)
+    L = w.grid_h * w.grid_w
+    ft = 4.0 * w.batch * w.heads * L * w.frames * w.frames * w.head_dim  # every video query, F keys
+    block_flops = K * (fj + bj + fs + bs + 3.0 * ft)
+    value = block_flops / (times["keep"] * 1e-3) / 1e12
+    set_bytes = sum(t.numel() * t.element_size() for t in ring[0])
+    moved = 2 * n_off * set_bytes
+    line = {
+        "metric": METRIC_BLOCK, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(times["keep"], 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) q, k, v, dO of the workload's shape, shared by the layers)",
+        "config": {
+            "workload": "%s, parallel block x %d layers: B=%d, H=%d, D=%d, %d text + %dx%dx%d video = %d tokens"
+                        % (w.name, K, B, H, D, w.text_slot, w.frames, w.grid_h, w.grid_w, N),
+            "branch": "block", "layers": K, "batch": B, "heads": H, "head_dim": D, "tokens": N,
+            "text_slot": w.text_slot, "frames": w.frames, "grid": [w.grid_h, w.grid_w],
+        },
+        "roofline": {"bound": "mfma", "kernel": "whole block step (all kernels)", "achieved": round(value, 2),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(value / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None, "algorithmic_per_launch": block_flops},
+        "memory_strategies": {
+            "saved_bytes_per_layer": set_bytes,
+            "keep": {"ms_per_step": round(times["keep"], 3), "device_saved_bytes": K * set_bytes},
+            "recompute": {"ms_per_step": round(times["recompute"], 3), "device_saved_bytes": set_bytes,
+                          "overhead": round(times["recompute"] / times["keep"] - 1.0, 4)},
+            "offload": {"ms_per_step": round(times["offload"], 3), "device_saved_bytes": len(ring) * set_bytes,
+                        "host_bytes": n_off * set_bytes, "pcie_bytes_per_step": moved,
+                        "overhead": round(times["offload"] / times["keep"] - 1.0, 4)},
+            "pcie_GBps": {"d2h": round(d2h, 2), "h2d": round(h2d, 2)},
+        },
+        "cpu_baseline": None,
+    }
+    print(json.dumps(line), flush=True)
     return 0
 
 
