@@ -48,17 +48,20 @@ __device__ __forceinline__ void add_bf16x4(f32x4& acc, bf16x4 x) {
 __device__ __forceinline__ void add_bf16x4(f32x4& acc, const __bf16* src) {
   if (src) add_bf16x4(acc, *(const bf16x4*)src);
 }
+__device__ __forceinline__ void add_bf16x8(f32x4& lo, f32x4& hi, bf16x8 x) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    lo[i] += (float)x[i];
+    hi[i] += (float)x[4 + i];
+  }
+}
 
-template <int D, bool SUM>
-__global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_fwd_kernel(TemporalArgs a) {
+// One wave: attention of the G positions starting at sm.l0 (sm.l0 < L) of head h, sample b.
+template <int D>
+__device__ __forceinline__ void temporal_fwd_wave(const TemporalArgs& a, const SlotMap& sm, int h, int b) {
   const int lane = threadIdx.x & 63;
   const int l32 = lane & 31;
   const int hi = lane >> 5;
-  const int blk = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
-  const int h = blockIdx.y;
-  const int b = blockIdx.z;
-  SlotMap sm{a.T, a.F, a.L, a.G, blk * a.G};
-  if (sm.l0 >= a.L) return;  // whole wave
   const size_t tok = (size_t)a.H * D;
   const size_t base = (size_t)b * a.N * tok + (size_t)h * D;
 
@@ -126,21 +129,48 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_fwd_kernel(Tempo
       for (int j = 0; j < 4; ++j) {
         bf16x4 o4 = {(__bf16)(oacc[4 * j + 0] * inv), (__bf16)(oacc[4 * j + 1] * inv),
                      (__bf16)(oacc[4 * j + 2] * inv), (__bf16)(oacc[4 * j + 3] * inv)};
-        const size_t e = db * 32 + 8 * j + 4 * hi;
-        *(bf16x4*)(op + e) = o4;
-        if (SUM) {  // branch sum: (a + b) + o, o as stored
-          const size_t off = base + (size_t)n * tok + e;
-          f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-          add_bf16x4(acc, a.sum_a ? a.sum_a + off : nullptr);
-          add_bf16x4(acc, a.sum_b ? a.sum_b + off : nullptr);
-          add_bf16x4(acc, o4);
-          *(bf16x4*)(a.sum_out + off) = bf16x4{(__bf16)acc[0], (__bf16)acc[1], (__bf16)acc[2], (__bf16)acc[3]};
-        }
+        *(bf16x4*)(op + db * 32 + 8 * j + 4 * hi) = o4;
       }
     }
   }
   if (q_ok && hi == 0)
     a.lse[((size_t)b * a.H + h) * a.N + n] = sum > 0.0f ? (m2 + __log2f(sum)) * kLn2 : -INFINITY;
+}
+
+// Forward: one wave per G positions. With SUM, the workgroup then writes the branch sum
+// sum_out = (sum_a + sum_b) + o of the rows it produced, reading o back after a barrier
+// so that every access is a whole 16-byte chunk of a row (the accumulator layout would
+// scatter 8-byte pieces over 32 rows per instruction).
+template <int D, bool SUM>
+__global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_fwd_kernel(TemporalArgs a) {
+  const int h = blockIdx.y;
+  const int b = blockIdx.z;
+  SlotMap sm{a.T, a.F, a.L, a.G, (int)(blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6)) * a.G};
+  if (sm.l0 < a.L) temporal_fwd_wave<D>(a, sm, h, b);
+  if (SUM) {
+    __syncthreads();  // this workgroup's rows of o are written
+    const int wl0 = (int)blockIdx.x * kWavesPerBlock * a.G;  // first position of the workgroup
+    const int npos = min(kWavesPerBlock * a.G, a.L - wl0);
+    constexpr int kChunks = D / 8;  // 16-byte chunks per row
+    const size_t tok = (size_t)a.H * D;
+    const size_t base = (size_t)b * a.N * tok + (size_t)h * D;
+    for (int i = threadIdx.x; i < a.F * npos * kChunks; i += blockDim.x) {
+      const int r = i / kChunks;
+      const int f = r / npos;
+      const size_t off = base + (size_t)(a.T + f * a.L + wl0 + (r - f * npos)) * tok + (i % kChunks) * 8;
+      f32x4 lo = {0.0f, 0.0f, 0.0f, 0.0f}, hi = lo;
+      if (a.sum_a) add_bf16x8(lo, hi, *(const bf16x8*)(a.sum_a + off));
+      if (a.sum_b) add_bf16x8(lo, hi, *(const bf16x8*)(a.sum_b + off));
+      add_bf16x8(lo, hi, *(const bf16x8*)(a.o + off));
+      bf16x8 r8;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        r8[e] = (__bf16)lo[e];
+        r8[4 + e] = (__bf16)hi[e];
+      }
+      *(bf16x8*)(a.sum_out + off) = r8;
+    }
+  }
 }
 
 // Backward. LSE*log2(e) and D = rowsum(dO o O) per token come from the preparation pass
