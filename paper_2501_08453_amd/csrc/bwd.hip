@@ -253,15 +253,30 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
       }
       // Operand element t of k-step st2 is query 16*st2 + 8*(t/4) + 4*hi + t%4, stored by
       // the transposed tiles as 8 consecutive elements at position 16*st2 + 8*hi.
+      // Operands of the 2 * D/32 products in order (k-step st2 major, dim block db minor),
+      // each read one product ahead: the read is in flight while the previous pair runs.
+      constexpr int NB = D / 32;
+      const int obase = (l32 * kTileRow + qb * 32 + 8 * hi) * 2;
+      auto opnd = [&](int idx, const VC_LDS char* bp) {
+        return *(const VC_LDS bf16x8*)(bp + obase + ((idx % NB) * 32 * kTileRow + 16 * (idx / NB)) * 2);
+      };
+      bf16x8 av = opnd(0, dot_lds), ak = opnd(0, qt_lds);
 #pragma unroll
       for (int st2 = 0; st2 < 2; ++st2) {
         const bf16x8 pb = to_bf16x8(&p[8 * st2]);
         const bf16x8 sb = to_bf16x8(&ds[8 * st2]);
 #pragma unroll
-        for (int db = 0; db < D / 32; ++db) {
-          const int off = ((db * 32 + l32) * kTileRow + qb * 32 + 16 * st2 + 8 * hi) * 2;
-          dv_acc[db] = mfma32(*(const VC_LDS bf16x8*)(dot_lds + off), pb, dv_acc[db]);
-          dk_acc[db] = mfma32(*(const VC_LDS bf16x8*)(qt_lds + off), sb, dk_acc[db]);
+        for (int db = 0; db < NB; ++db) {
+          const int nx = st2 * NB + db + 1;
+          bf16x8 vn = av, kn = ak;
+          if (nx < 2 * NB) {
+            vn = opnd(nx, dot_lds);
+            kn = opnd(nx, qt_lds);
+          }
+          dv_acc[db] = mfma32(av, pb, dv_acc[db]);
+          dk_acc[db] = mfma32(ak, sb, dk_acc[db]);
+          av = vn;
+          ak = kn;
         }
       }
     }
