@@ -226,7 +226,7 @@ vc_status vc_temporalattn_fwd_sum(const vc_jointattn_desc* desc,
                                   const void* o_joint, const void* o_spatial,
                                   void* o, float* lse, void* out, void* stream);
 
-/* Bytes of device workspace the temporal backward needs: per row fp32 D and
+/* Bytes of device workspace the temporal backward needs: per row fp32 -D and
  * LSE*log2(e) ([B,H,Npad]). 0 for an invalid descriptor. Host only. */
 size_t vc_temporalattn_bwd_workspace_bytes(const vc_jointattn_desc* desc);
 

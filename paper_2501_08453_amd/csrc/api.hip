@@ -72,7 +72,7 @@ size_t rows_bytes(const vc_jointattn_desc* d, int64_t n) {
   return align256((size_t)d->batch * d->heads * (size_t)ntiles(n) * vcja::kTileTok * sizeof(float));
 }
 
-// Backward workspace: D | LSE*log2(e) | Q^T tiles | dO^T tiles | K^T tiles.
+// Backward workspace: -D | LSE*log2(e) | Q^T tiles | dO^T tiles | K^T tiles.
 struct BwdWorkspace {
   float* dd;
   float* lse2;

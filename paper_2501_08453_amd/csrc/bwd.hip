@@ -1,21 +1,22 @@
 // Backward joint text-video attention for gfx950, without atomics.
 //
-// Prepare: per query row, D_i = <dO_i, O_i> and LSE_i*log2(e) in fp32, padded
+// Prepare: per query row, -D_i = -<dO_i, O_i> and LSE_i*log2(e) in fp32, padded
 //   to whole tiles of 64 rows (padding rows get LSE = +inf so that their
 //   probabilities vanish, and D = 0); transposed token tiles of Q, dO and K
-//   come from the reformatting pass.
+//   come from the reformatting pass. D is stored negated so that dP - D is
+//   what the dP accumulator holds when it starts from -D.
 // dK/dV (key-stationary): one workgroup of eight waves owns 256 keys of one
 //   (sample, head), each wave 32, with K and V of its keys in registers and
 //   dK^T, dV^T accumulated in registers. It walks over all query tiles of 64,
 //   whose row-major Q and dO tiles, transposed Q^T and dO^T tiles, LSE and D
 //   are copied asynchronously global -> LDS into a two-stage ring one tile
 //   ahead; one barrier per tile. Per tile it recomputes S = Q K^T and
-//   P = exp2(S c log2(e) - LSE log2(e)), forms dP = dO V^T and
+//   P = exp2(S c log2(e) - LSE log2(e)), forms dP - D = -D + dO V^T and
 //   dS = P o (dP - D) with the matrix cores, and accumulates dV^T += dO^T P and
 //   dK^T += Q^T dS straight from the accumulator layout (lane column = key).
 // dQ (query-stationary): one workgroup of eight waves owns 256 queries, each
 //   wave 32, with Q^T and dO^T of its queries in registers and the lane's
-//   LSE and D as scalars. It walks over the key tiles like the forward,
+//   LSE and -D as scalars. It walks over the key tiles like the forward,
 //   computing S^T = K Q^T and dP^T = V dO^T, dS^T, and dQ^T += K^T dS^T with
 //   dS^T taken straight from the accumulator layout (lane column = query).
 // Splitting the gradient this way recomputes S and dP once more instead of
@@ -62,7 +63,7 @@ __global__ __launch_bounds__(256) void bwd_prepare_kernel(const __bf16* __restri
     const int b = (int)(bn / N);
     const size_t bh = (size_t)b * H + h;
     const float x = lse[bh * N + n];
-    dd[bh * Npad + n] = sum;
+    dd[bh * Npad + n] = -sum;
     lse2[bh * Npad + n] = (x == -INFINITY) ? INFINITY : x * kLog2e;
   }
   // Padding rows [N, Npad) of every (sample, head).
@@ -219,7 +220,13 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
 
 #pragma unroll 1
     for (int qb = 0; qb < kBQ / 32; ++qb) {
-      f32x16 s = zero_f32x16(), dp = zero_f32x16();
+      f32x16 s = zero_f32x16(), dp;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {  // dP accumulates on top of -D of its query rows
+        const f32x4 nd = *(const VC_LDS f32x4*)(dd_lds + qb * 32 + 8 * j + 4 * hi);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) dp[4 * j + i] = nd[i];
+      }
 #pragma unroll
       for (int ks = 0; ks < D / 16; ++ks) {
         const bf16x8 qa = *(const VC_LDS bf16x8*)(q_lds + (qb * 32 + l32) * RS + (2 * ks + hi) * 16);
@@ -238,7 +245,6 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const f32x4 l2 = *(const VC_LDS f32x4*)(lse_lds + qb * 32 + 8 * j + 4 * hi);
-        const f32x4 d4 = *(const VC_LDS f32x4*)(dd_lds + qb * 32 + 8 * j + 4 * hi);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int r = 4 * j + i;
@@ -248,7 +254,7 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
             ok = ok & (!pair_mask | ((qrow >= kr.x) & (qrow < kr.y)));
           }
           p[r] = ok ? fast_exp2(fmaf(s[r], a.scale_log2, -l2[i])) : 0.0f;
-          ds[r] = p[r] * (dp[r] - d4[i]);
+          ds[r] = p[r] * dp[r];
         }
       }
       // Operand element t of k-step st2 is query 16*st2 + 8*(t/4) + 4*hi + t%4, stored by
@@ -364,7 +370,7 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
   const int qi = gp.x * kDqBM + w * 32 + l32;  // this lane's query (accumulator column)
   const int qr = min(qi, N - 1);
 
-  // Q^T and dO^T as B operands (dims 16*ks + 8*hi .. +7), LSE*log2e and D as scalars.
+  // Q^T and dO^T as B operands (dims 16*ks + 8*hi .. +7), LSE*log2e and -D as scalars.
   bf16x8 qf[D / 16], dof[D / 16];
 #pragma unroll
   for (int ks = 0; ks < D / 16; ++ks) {
@@ -452,7 +458,7 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
         }
       }
 #pragma unroll
-      for (int r = 0; r < 16; ++r) ds[r] = ds[r] * (dp[r] - dd);
+      for (int r = 0; r < 16; ++r) ds[r] = ds[r] * (dp[r] + dd);
 #pragma unroll
       for (int st2 = 0; st2 < 2; ++st2) {
         const bf16x8 sb = to_bf16x8(&ds[8 * st2]);

@@ -253,7 +253,7 @@ struct DkdvArgs {
   const __bf16* qt;     // Q as transposed token tiles
   const __bf16* dot;    // dO as transposed token tiles
   const float* lse2;    // LSE * log2(e), +inf for rows without keys and padding, [B, H, Npad]
-  const float* dd;      // D = rowsum(dO o O), 0 on padding, [B, H, Npad]
+  const float* dd;      // -D = -rowsum(dO o O), 0 on padding, [B, H, Npad]
   const int32_t* text_len;
   const uint8_t* key_mask;
   __bf16* dk;
@@ -299,7 +299,7 @@ struct TemporalArgs {
   const __bf16* dout;   // backward only
   const uint8_t* key_mask;
   const float* lse2;    // backward: LSE * log2(e) per token, +inf where there is none, [B, H, Npad]
-  const float* dd;      // backward: D = rowsum(dO o O), [B, H, Npad]
+  const float* dd;      // backward: -D = -rowsum(dO o O), [B, H, Npad]
   __bf16* o;            // forward output / backward dQ
   float* lse;           // forward output
   __bf16* dk;           // backward

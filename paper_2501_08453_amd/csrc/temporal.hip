@@ -173,7 +173,7 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_fwd_kernel(Tempo
   }
 }
 
-// Backward. LSE*log2(e) and D = rowsum(dO o O) per token come from the preparation pass
+// Backward. LSE*log2(e) and -D = -rowsum(dO o O) per token come from the preparation pass
 // ([B, H, npad], +inf / 0 where a row has no key). Two orientations of the same block:
 // lane = query (S^T, dP^T, dS^T) gives dQ^T = c K^T dS^T; lane = key (S, dP, dS) gives
 // dV^T = dO^T P and dK^T = c Q^T dS. The transposed A operands are gathered in the slot
@@ -230,7 +230,7 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_bwd_kernel(Tempo
       bool ok = s_ok & (j >= lo) & (j < lo + a.F);
       if (km) ok = ok & (km[sm.token(j)] != 0);
       const float p = ok ? fast_exp2(fmaf(sacc[r], a.scale_log2, -l2)) : 0.0f;
-      ds[r] = p * (pacc[r] - d);
+      ds[r] = p * (pacc[r] + d);
     }
     bf16x8 sb[2];
     sb[0] = to_bf16x8(&ds[0]);
@@ -275,7 +275,7 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_bwd_kernel(Tempo
       const float l2 = a.lse2[rbase + ni];
       const float d = a.dd[rbase + ni];
       p[r] = ok ? fast_exp2(fmaf(sacc[r], a.scale_log2, -l2)) : 0.0f;
-      ds[r] = p[r] * (pacc[r] - d);
+      ds[r] = p[r] * (pacc[r] + d);
     }
     bf16x8 pb[2], sb[2];
     pb[0] = to_bf16x8(&p[0]);
