@@ -248,12 +248,13 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int r = 4 * j + i;
-          bool ok = valid;
+          p[r] = fast_exp2(fmaf(s[r], a.scale_log2, -l2[i]));
           if (SPATIAL) {
             const int qrow = row0 + acc_row(r, hi);
-            ok = ok & (!pair_mask | ((qrow >= kr.x) & (qrow < kr.y)));
+            p[r] = (valid & (!pair_mask | ((qrow >= kr.x) & (qrow < kr.y)))) ? p[r] : 0.0f;
           }
-          p[r] = ok ? fast_exp2(fmaf(s[r], a.scale_log2, -l2[i])) : 0.0f;
+          // Joint attention needs no test here: the probabilities of an invalid key reach
+          // only its own lane's dK, dV, which are written as zero at the end.
           ds[r] = p[r] * dp[r];
         }
       }
@@ -304,14 +305,17 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
   } else if (key < N) {
     __bf16* dkp = a.dk + base + (size_t)key * tok;
     __bf16* dvp = a.dv + base + (size_t)key * tok;
+    // An invalid key gets exactly zero (its accumulators may hold anything, even inf).
+    auto kv = [&](float x) { return (__bf16)(valid ? x * a.scale : 0.0f); };
+    auto vv = [&](float x) { return (__bf16)(valid ? x : 0.0f); };
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        bf16x4 tk = {(__bf16)(dk_acc[db][4 * j + 0] * a.scale), (__bf16)(dk_acc[db][4 * j + 1] * a.scale),
-                     (__bf16)(dk_acc[db][4 * j + 2] * a.scale), (__bf16)(dk_acc[db][4 * j + 3] * a.scale)};
-        bf16x4 tv = {(__bf16)dv_acc[db][4 * j + 0], (__bf16)dv_acc[db][4 * j + 1], (__bf16)dv_acc[db][4 * j + 2],
-                     (__bf16)dv_acc[db][4 * j + 3]};
+        bf16x4 tk = {kv(dk_acc[db][4 * j + 0]), kv(dk_acc[db][4 * j + 1]), kv(dk_acc[db][4 * j + 2]),
+                     kv(dk_acc[db][4 * j + 3])};
+        bf16x4 tv = {vv(dv_acc[db][4 * j + 0]), vv(dv_acc[db][4 * j + 1]), vv(dv_acc[db][4 * j + 2]),
+                     vv(dv_acc[db][4 * j + 3])};
         *(bf16x4*)(dkp + db * 32 + 8 * j + 4 * hi) = tk;
         *(bf16x4*)(dvp + db * 32 + 8 * j + 4 * hi) = tv;
       }
