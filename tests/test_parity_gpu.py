@@ -204,13 +204,17 @@ def test_masked_key_values_have_no_effect():
     a = run_gpu(desc, g["q"], g["k"], g["v"], g["do"], g["text_len"], kmg)
     valid = ora.key_validity(2, w.tokens, w.text_slot, x["text_len"], km)
     inv = torch.from_numpy(~valid).to("cuda")[:, :, None, None]
-    noise = torch.randn(g["k"].shape, device="cuda", generator=torch.Generator("cuda").manual_seed(1)) * 30
-    k2 = torch.where(inv, noise.to(torch.bfloat16), g["k"]).contiguous()
-    v2 = torch.where(inv, (-noise).to(torch.bfloat16), g["v"]).contiguous()
-    b = run_gpu(desc, g["q"], k2, v2, g["do"], g["text_len"], kmg)
-    assert np.array_equal(a["o"], b["o"]) and np.array_equal(a["lse"], b["lse"])
-    assert np.all(b["dk"][~valid] == 0) and np.all(b["dv"][~valid] == 0)
-    assert np.array_equal(a["dq"], b["dq"])
+    # 30: large finite probabilities at the masked keys; 3000: their exponentials
+    # overflow (inf, and NaN in dS), which must stay confined to those keys
+    for mag in (30.0, 3000.0):
+        noise = torch.randn(g["k"].shape, device="cuda", generator=torch.Generator("cuda").manual_seed(1)) * mag
+        k2 = torch.where(inv, noise.to(torch.bfloat16), g["k"]).contiguous()
+        v2 = torch.where(inv, (-noise).to(torch.bfloat16), g["v"]).contiguous()
+        b = run_gpu(desc, g["q"], k2, v2, g["do"], g["text_len"], kmg)
+        assert np.array_equal(a["o"], b["o"]) and np.array_equal(a["lse"], b["lse"])
+        assert np.all(b["dk"][~valid] == 0) and np.all(b["dv"][~valid] == 0)
+        assert np.array_equal(a["dk"][valid], b["dk"][valid]) and np.array_equal(a["dv"][valid], b["dv"][valid])
+        assert np.array_equal(a["dq"], b["dq"])
 
 
 def test_forward_is_deterministic_and_batch_independent():
