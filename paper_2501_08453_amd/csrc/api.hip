@@ -228,6 +228,10 @@ vc_status fwd_impl(const vc_jointattn_desc* desc, const void* q, const void* k, 
   a.ntile = ntiles(n);
   a.frame_len = spatial ? desc->grid_h * desc->grid_w : 0;
   a.scale_log2 = scale_of(desc) * vcja::kLog2e;
+  // Spatial branch: text rows are not queries; their o and lse are written here.
+  if (spatial && vcja::launch_text_rows(a.o, nullptr, nullptr, lse, a.B, a.H, a.N, a.T, desc->head_dim,
+                                        as_stream(stream)) != hipSuccess)
+    return VC_ERR_HIP;
   return vcja::launch_fwd(a, desc->head_dim, as_stream(stream)) == hipSuccess ? VC_OK : VC_ERR_HIP;
 }
 
@@ -348,6 +352,10 @@ vc_status dq_impl(const vc_jointattn_desc* desc, const void* q, const void* k, c
   a.frame_len = spatial ? desc->grid_h * desc->grid_w : 0;
   a.scale = scale_of(desc);
   a.scale_log2 = a.scale * vcja::kLog2e;
+  // Spatial branch: text rows are not queries; their dq is zero.
+  if (spatial && vcja::launch_text_rows(a.dq, nullptr, nullptr, nullptr, a.B, a.H, a.N, a.T, desc->head_dim,
+                                        as_stream(stream)) != hipSuccess)
+    return VC_ERR_HIP;
   return vcja::launch_bwd_dq(a, desc->head_dim, as_stream(stream)) == hipSuccess ? VC_OK : VC_ERR_HIP;
 }
 

@@ -110,7 +110,10 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
     kb = split ? gp.x % a.text_blocks : gp.x - nsplit + a.text_blocks;
     chunk = split ? gp.x / a.text_blocks : 0;
   }
-  const int key = kb * kBKV + w * 32 + l32;  // this lane's key (accumulator column)
+  // This workgroup's keys (spatial branch: text keys, or keys of one frame).
+  const RowBlock rb = row_block(kb, N, a.T, SPATIAL ? a.frame_len : 0, kBKV, true);
+  const int key = rb.r0 + w * 32 + l32;  // this lane's key (accumulator column)
+  const bool key_in = key < rb.r1;
   // Partial dK of this lane's key in its chunk (dV partials follow all dK partials); formed
   // only where it is written, so that no register holds it across the main loop.
   const size_t part_stride = (size_t)a.text_chunks * a.B * a.H * a.text_blocks * kBKV * D;
@@ -124,7 +127,7 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
   rule.tl = a.text_len ? min(max(a.text_len[b], 0), a.T) : a.T;
   rule.L = SPATIAL ? a.frame_len : 0;
   rule.km = a.key_mask ? a.key_mask + (size_t)b * N : nullptr;
-  const bool valid = rule.key_valid(key);
+  const bool valid = key_in && rule.key_valid(key);
 
   if (!__syncthreads_or(valid)) {
     // No valid key in this workgroup: its dK, dV (or partials) are zero.
@@ -135,7 +138,7 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
         *(f32x4*)(pk + 4 * c) = z;
         *(f32x4*)(pk + part_stride + 4 * c) = z;
       }
-    } else if (key < N) {
+    } else if (key_in) {
       const bf16x8 z = zero_bf16x8();
       for (int c = 0; c < D / 8; ++c) {
         *(bf16x8*)(a.dk + base + (size_t)key * tok + 8 * c) = z;
@@ -167,7 +170,7 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
   // K, V of this lane's key as B operands (dims 16*ks + 8*hi .. +7).
   bf16x8 kf[D / 16], vf[D / 16];
   {
-    const size_t kr = base + (size_t)min(key, N - 1) * tok + 8 * hi;
+    const size_t kr = base + (size_t)min(key, rb.r1 - 1) * tok + 8 * hi;
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) {
       kf[ks] = *(const bf16x8*)(a.k + kr + 16 * ks);
@@ -184,8 +187,7 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
 
   // Query tiles this workgroup visits (the same sequence for every wave): all of them in
   // joint attention; in the spatial branch the video tiles its keys are attended from.
-  const int wk0 = kb * kBKV;
-  TileRuns runs = rule.query_tiles(wk0, min(wk0 + kBKV, N), a.ntile);
+  TileRuns runs = rule.query_tiles(rb.r0, rb.r1, a.ntile);
   if (split) {  // this chunk's part of the video query tiles
     const int c0 = a.T / kBQ + chunk * a.text_span;
     runs.b0 = max(runs.b0, c0);
@@ -195,7 +197,8 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
   auto next_q = [&](int qt) { return SPATIAL ? runs.next(qt) : qt; };
   // Spatial branch: a tile needs the per-pair test unless this wave's keys are all text
   // and the tile holds video queries only, or they all lie in one frame containing it.
-  const int kw0 = kb * kBKV + w * 32, kw1 = kw0 + 31;
+  // (a wave past the end of a short block takes its last row)
+  const int kw0 = min(rb.r0 + w * 32, rb.r1 - 1), kw1 = min(rb.r0 + w * 32 + 31, rb.r1 - 1);
   const bool wave_text_keys = kw1 < a.T;
   const int wks = SPATIAL ? rule.frame_start(kw0) : 0;
   const bool wave_one_frame = SPATIAL && kw0 >= a.T && kw1 < N && rule.frame_start(kw1) == wks;
@@ -302,7 +305,7 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
         *(f32x4*)(pk + db * 32 + 8 * j + 4 * hi) = tk;
         *(f32x4*)(pk + part_stride + db * 32 + 8 * j + 4 * hi) = tv;
       }
-  } else if (key < N) {
+  } else if (key_in) {
     __bf16* dkp = a.dk + base + (size_t)key * tok;
     __bf16* dvp = a.dv + base + (size_t)key * tok;
     // An invalid key gets exactly zero (its accumulators may hold anything, even inf).
@@ -322,12 +325,11 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
   }
 }
 
-// Spatial branch: dK, dV of the split text blocks' rows [0, min(rows, N)) as the sum of the
-// chunks' fp32 partials (rows = text_blocks * 256). One thread per 4 dims of one row.
+// Spatial branch: dK, dV of the text rows [0, nrow) as the sum of the chunks' fp32
+// partials (rows = text_blocks * 256 per partial). One thread per 4 dims of one row.
 template <int D>
 __global__ void text_reduce_kernel(const float* part, __bf16* dk, __bf16* dv, int B, int H, int N, int rows,
-                                   int chunks) {
-  const int nrow = min(rows, N);
+                                   int nrow, int chunks) {
   const size_t total = (size_t)B * H * nrow * (D / 4);
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= total) return;
@@ -371,8 +373,11 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
   const size_t tok = (size_t)a.H * D;
   const size_t base = (size_t)b * N * tok + (size_t)h * D;
   const size_t bh = (size_t)b * a.H + h;
-  const int qi = gp.x * kDqBM + w * 32 + l32;  // this lane's query (accumulator column)
-  const int qr = min(qi, N - 1);
+  // This workgroup's queries (spatial branch: inside one frame; text rows of dQ are written
+  // by the caller's text-rows pass).
+  const RowBlock rb = row_block(gp.x, N, a.T, a.frame_len, kDqBM, false);
+  const int qi = rb.r0 + w * 32 + l32;  // this lane's query (accumulator column)
+  const int qr = min(qi, rb.r1 - 1);
 
   // Q^T and dO^T as B operands (dims 16*ks + 8*hi .. +7), LSE*log2e and -D as scalars.
   bf16x8 qf[D / 16], dof[D / 16];
@@ -394,14 +399,14 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
   rule.tl = a.text_len ? min(max(a.text_len[b], 0), a.T) : a.T;
   rule.L = a.frame_len;
   rule.km = a.key_mask ? a.key_mask + (size_t)b * N : nullptr;
-  const int qw0 = gp.x * kDqBM + w * 32, qw1 = qw0 + 31;  // this wave's queries
+  // This wave's queries (past the end of a short block: its last row).
+  const int qw0 = min(rb.r0 + w * 32, rb.r1 - 1), qw1 = min(rb.r0 + w * 32 + 31, rb.r1 - 1);
   const bool wave_all_video = qw0 >= a.T && qw1 < N;
   const int wqs = a.frame_len ? rule.frame_start(qw0) : 0;
   const bool wave_one_frame = wave_all_video && a.frame_len && rule.frame_start(qw1) == wqs;
   const QueryRange qrange = query_range(rule, qi);
   // Key tiles this workgroup visits (the same sequence for every wave).
-  const int wq0 = gp.x * kDqBM;
-  const TileRuns runs = rule.key_tiles(wq0, min(wq0 + kDqBM, N), a.ntile);
+  const TileRuns runs = rule.key_tiles(rb.r0, rb.r1, a.ntile);
   auto next_tile = [&](int kt) { return runs.next(kt); };
   auto issue = [&](int kt, int st) {
     VC_LDS char* sk = (VC_LDS char*)smem + st * STAGE;
@@ -477,7 +482,7 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
     kt = kn;
   }
 
-  if (qi < N) {
+  if (qi < rb.r1) {
     __bf16* qp = a.dq + base + (size_t)qi * tok;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
@@ -506,7 +511,9 @@ hipError_t launch_bwd_prepare(const __bf16* o, const float* lse, const __bf16* d
 hipError_t launch_bwd_dkdv(const DkdvArgs& a, int head_dim, hipStream_t s) {
   const bool spatial = a.frame_len > 0;
   const bool split = spatial && a.text_chunks > 1;
-  dim3 grid((a.N + kBKV - 1) / kBKV + (split ? (a.text_chunks - 1) * a.text_blocks : 0), a.H, a.B);
+  dim3 grid(row_blocks(a.N, a.T, spatial ? a.frame_len : 0, kBKV, true) +
+                (split ? (a.text_chunks - 1) * a.text_blocks : 0),
+            a.H, a.B);
   if (head_dim == 128 && spatial)
     hipLaunchKernelGGL((bwd_dkdv_kernel<128, true>), grid, dim3(64 * kDkdvWaves), 0, s, a);
   else if (head_dim == 128)
@@ -517,20 +524,21 @@ hipError_t launch_bwd_dkdv(const DkdvArgs& a, int head_dim, hipStream_t s) {
     hipLaunchKernelGGL((bwd_dkdv_kernel<64, false>), grid, dim3(64 * kDkdvWaves), 0, s, a);
   if (split) {
     const int rows = a.text_blocks * kBKV;
-    const size_t threads = (size_t)a.B * a.H * std::min(rows, a.N) * (head_dim / 4);
+    const int nrow = std::min(a.T, a.N);  // the text keys
+    const size_t threads = (size_t)a.B * a.H * nrow * (head_dim / 4);
     dim3 rgrid((unsigned)((threads + 255) / 256));
     if (head_dim == 128)
       hipLaunchKernelGGL(text_reduce_kernel<128>, rgrid, dim3(256), 0, s, a.text_part, a.dk, a.dv, a.B, a.H, a.N,
-                         rows, a.text_chunks);
+                         rows, nrow, a.text_chunks);
     else
       hipLaunchKernelGGL(text_reduce_kernel<64>, rgrid, dim3(256), 0, s, a.text_part, a.dk, a.dv, a.B, a.H, a.N,
-                         rows, a.text_chunks);
+                         rows, nrow, a.text_chunks);
   }
   return hipGetLastError();
 }
 
 hipError_t launch_bwd_dq(const DqArgs& a, int head_dim, hipStream_t s) {
-  dim3 grid((a.N + kDqBM - 1) / kDqBM, a.H, a.B);
+  dim3 grid(row_blocks(a.N, a.T, a.frame_len, kDqBM, false), a.H, a.B);
   if (head_dim == 128)
     hipLaunchKernelGGL(bwd_dq_kernel<128>, grid, dim3(64 * kDqWaves), 0, s, a);
   else

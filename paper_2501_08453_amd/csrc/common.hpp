@@ -123,11 +123,6 @@ __device__ __forceinline__ float swap_halves(float x) { return __shfl_xor(x, 32,
 __device__ __forceinline__ float halves_max(float x) { return fmaxf(x, swap_halves(x)); }
 __device__ __forceinline__ float halves_sum(float x) { return x + swap_halves(x); }
 
-// Wave issue priority: raised around matrix-core phases so that a wave's MFMAs issue back
-// to back while the other wave on the SIMD fills the gaps with vector work.
-__device__ __forceinline__ void prio_high() { __builtin_amdgcn_s_setprio(1); }
-__device__ __forceinline__ void prio_low() { __builtin_amdgcn_s_setprio(0); }
-
 // Keeps the compiler from moving any instruction across this point.
 __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 
@@ -143,6 +138,28 @@ __host__ __device__ constexpr size_t tile_elems(int d) { return (size_t)d * kTil
 // Position of token t (0..63) inside a transposed tile row.
 __host__ __device__ constexpr int tok_pos(int t) {
   return (t & ~15) | (((t >> 2) & 3) == 1 ? 8 : ((t >> 2) & 3) == 2 ? 4 : ((t >> 2) & 3) * 4) | (t & 3);
+}
+
+// The rows (queries or keys) a workgroup owns, [r0, r1), at most `per` of them. Joint
+// attention: uniform blocks over [0, N). Spatial branch: no block straddles a frame or the
+// text slot (a straddling block would visit the key tiles of two frames, each wave masking
+// half of them): first the text rows [0, T) in blocks (with `text`: the key side), then
+// ceil(L / per) blocks per frame, the last one shorter when `per` does not divide L.
+struct RowBlock {
+  int r0, r1;
+};
+__host__ __device__ inline int row_blocks(int N, int T, int L, int per, bool text) {
+  if (L == 0) return (N + per - 1) / per;
+  return (text ? (T + per - 1) / per : 0) + ((N - T) / L) * ((L + per - 1) / per);
+}
+__device__ __forceinline__ RowBlock row_block(int x, int N, int T, int L, int per, bool text) {
+  if (L == 0) return RowBlock{x * per, min(N, (x + 1) * per)};
+  const int tb = text ? (T + per - 1) / per : 0;
+  if (x < tb) return RowBlock{x * per, min(T, (x + 1) * per)};
+  const int nb = (L + per - 1) / per;
+  const int f = (x - tb) / nb, j = x - tb - f * nb;
+  const int s = T + f * L;
+  return RowBlock{s + j * per, s + min(L, (j + 1) * per)};
 }
 
 // The tiles a workgroup visits along the other token axis: [0, a1) and [b0, b1) (the runs

@@ -185,12 +185,16 @@ __global__ __launch_bounds__(64 * kWaves, kWavesPerSimd * 4 / kWaves) void fwd_k
   const size_t tok = (size_t)a.H * D;
   const size_t base = (size_t)b * N * tok + (size_t)h * D;
   const __bf16* vt_bh = a.vt + ((size_t)b * a.H + h) * a.ntile * tile_elems(D);
-  const int qi = gp.x * kBM + w * 32 + l32;
+  // This workgroup's queries (spatial branch: inside one frame; text rows are written
+  // by the caller's text-rows pass).
+  const RowBlock rb = row_block(gp.x, N, a.T, a.frame_len, kBM, false);
+  const int qi = rb.r0 + w * 32 + l32;
+  const bool q_in = qi < rb.r1;
 
   // Q^T as the B operand: lane holds query qi, dims 16*ks + 8*hi .. +7.
   bf16x8 qf[D / 16];
   {
-    const __bf16* qp = a.q + base + (size_t)min(qi, N - 1) * tok + 8 * hi;
+    const __bf16* qp = a.q + base + (size_t)min(qi, rb.r1 - 1) * tok + 8 * hi;
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) qf[ks] = *(const bf16x8*)(qp + 16 * ks);
   }
@@ -203,15 +207,16 @@ __global__ __launch_bounds__(64 * kWaves, kWavesPerSimd * 4 / kWaves) void fwd_k
   mask.rule.km = a.key_mask ? a.key_mask + (size_t)b * N : nullptr;
   mask.qr = query_range(mask.rule, qi);
   {
-    const int qw0 = gp.x * kBM + w * 32, qw1 = qw0 + 31;  // this wave's queries
+    // This wave's queries; a wave past the end of a short block takes its last row, so that
+    // it follows the same tile path as the others.
+    const int qw0 = min(rb.r0 + w * 32, rb.r1 - 1), qw1 = min(rb.r0 + w * 32 + 31, rb.r1 - 1);
     mask.wave_all_video = qw0 >= a.T && qw1 < N;
     mask.wqs = a.frame_len ? mask.rule.frame_start(qw0) : 0;
     mask.wave_one_frame = mask.wave_all_video && a.frame_len && mask.rule.frame_start(qw1) == mask.wqs;
   }
   // Key tiles this workgroup visits (the same sequence for every wave): all but tiles of
   // padded text only in joint attention; text and own-frame tiles in the spatial branch.
-  const int wq0 = gp.x * kBM;
-  const TileRuns runs = mask.rule.key_tiles(wq0, min(wq0 + kBM, N), a.ntile);
+  const TileRuns runs = mask.rule.key_tiles(rb.r0, rb.r1, a.ntile);
   auto next_tile = [&](int kt) { return runs.next(kt); };
   // Copies tile kt's K rows (rows past N repeat row N-1 and are masked) or V^T tile into
   // ring slot `slot`.
@@ -313,7 +318,7 @@ __global__ __launch_bounds__(64 * kWaves, kWavesPerSimd * 4 / kWaves) void fwd_k
 
   const float lt = halves_sum(l);
   const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
-  if (qi < N) {
+  if (q_in) {
     __bf16* op = a.o + base + (size_t)qi * tok;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
@@ -331,7 +336,7 @@ __global__ __launch_bounds__(64 * kWaves, kWavesPerSimd * 4 / kWaves) void fwd_k
 }  // namespace
 
 hipError_t launch_fwd(const FwdArgs& a, int head_dim, hipStream_t s) {
-  dim3 grid((a.N + kBM - 1) / kBM, a.H, a.B);
+  dim3 grid(row_blocks(a.N, a.T, a.frame_len, kBM, false), a.H, a.B);
   if (head_dim == 128)
     hipLaunchKernelGGL(fwd_kernel<128>, grid, dim3(64 * kWaves), 0, s, a);
   else
