@@ -5,10 +5,11 @@
 // Sequences are short (F <= 32), so one wave packs G = floor(32/F) consecutive
 // positions of one (sample, head) into the 32 slots of a 32x32x16 matrix-core
 // block: slot s holds frame s % F of position l0 + s / F; slots past G*F are
-// padding. Every operand is read straight from global memory (no LDS): rows of
-// Q, K (and dO, V in the backward) as 16-byte chunks, and the transposed operands
-// (V^T, K^T, Q^T, dO^T) gathered element by element in the key order the
-// accumulator layout produces. A key is valid for a query if it belongs to the
+// padding. Rows of Q, K (and dO, V in the backward) are read as 16-byte chunks, one
+// slot per lane; the rows whose transposes are MFMA operands (V^T in the forward,
+// K^T, Q^T, dO^T in the backward) are also written to LDS, and the transposed
+// fragments read from there element by element in the key order the accumulator
+// layout produces. A key is valid for a query if it belongs to the
 // same position (same group of F slots) and key_mask keeps it. The work is small
 // and bound by memory traffic.
 #include "common.hpp"
@@ -18,6 +19,12 @@ namespace {
 
 constexpr int kSlots = 32;
 constexpr int kWavesPerBlock = 4;
+// Rows of a wave's 32 slots staged in LDS (row-major, padded by 8 elements so that the
+// rows of a 16-byte write fall in different banks): transposed operands are read from
+// there two bytes at a time instead of being gathered from memory.
+constexpr int kRowPad = 8;
+template <int D>
+constexpr int stage_elems() { return kSlots * (D + kRowPad); }
 
 // Token row of slot s in the block starting at position l0 (clamped into range for
 // padding slots, whose probabilities are zero).
@@ -58,7 +65,8 @@ __device__ __forceinline__ void add_bf16x8(f32x4& lo, f32x4& hi, bf16x8 x) {
 
 // One wave: attention of the G positions starting at sm.l0 (sm.l0 < L) of head h, sample b.
 template <int D>
-__device__ __forceinline__ void temporal_fwd_wave(const TemporalArgs& a, const SlotMap& sm, int h, int b) {
+__device__ __forceinline__ void temporal_fwd_wave(const TemporalArgs& a, const SlotMap& sm, int h, int b,
+                                                  VC_LDS __bf16* vs) {
   const int lane = threadIdx.x & 63;
   const int l32 = lane & 31;
   const int hi = lane >> 5;
@@ -75,6 +83,8 @@ __device__ __forceinline__ void temporal_fwd_wave(const TemporalArgs& a, const S
   for (int ks = 0; ks < D / 16; ++ks) {
     qf[ks] = *(const bf16x8*)(a.q + base + (size_t)n * tok + 16 * ks + 8 * hi);
     kf[ks] = *(const bf16x8*)(a.k + base + (size_t)n * tok + 16 * ks + 8 * hi);
+    *(VC_LDS bf16x8*)(vs + s * (D + kRowPad) + 16 * ks + 8 * hi) =
+        *(const bf16x8*)(a.v + base + (size_t)n * tok + 16 * ks + 8 * hi);
   }
   // S^T = K Q^T: lane column = query slot s, register r = key slot acc_slot(r, hi).
   f32x16 sacc = zero_f32x16();
@@ -107,11 +117,11 @@ __device__ __forceinline__ void temporal_fwd_wave(const TemporalArgs& a, const S
   bf16x8 pb[2];
   pb[0] = to_bf16x8(&p[0]);
   pb[1] = to_bf16x8(&p[8]);
-  size_t vrow[2][8];
+  int vrow[2][8];  // LDS rows of the key slots of operand element t, k-step st
 #pragma unroll
   for (int st = 0; st < 2; ++st)
 #pragma unroll
-    for (int t = 0; t < 8; ++t) vrow[st][t] = base + (size_t)sm.token(op_slot(st, t, hi)) * tok;
+    for (int t = 0; t < 8; ++t) vrow[st][t] = op_slot(st, t, hi) * (D + kRowPad);
   const float inv = sum > 0.0f ? 1.0f / sum : 0.0f;
   __bf16* op = a.o + base + (size_t)n * tok;
 #pragma unroll
@@ -121,7 +131,7 @@ __device__ __forceinline__ void temporal_fwd_wave(const TemporalArgs& a, const S
     for (int st = 0; st < 2; ++st) {
       bf16x8 vt;
 #pragma unroll
-      for (int t = 0; t < 8; ++t) vt[t] = a.v[vrow[st][t] + db * 32 + l32];
+      for (int t = 0; t < 8; ++t) vt[t] = vs[vrow[st][t] + db * 32 + l32];
       oacc = mfma32(vt, pb[st], oacc);
     }
     if (q_ok) {
@@ -145,8 +155,10 @@ template <int D, bool SUM>
 __global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_fwd_kernel(TemporalArgs a) {
   const int h = blockIdx.y;
   const int b = blockIdx.z;
-  SlotMap sm{a.T, a.F, a.L, a.G, (int)(blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6)) * a.G};
-  if (sm.l0 < a.L) temporal_fwd_wave<D>(a, sm, h, b);
+  __shared__ __attribute__((aligned(16))) __bf16 stage[kWavesPerBlock * stage_elems<D>()];
+  const int wave = threadIdx.x >> 6;
+  SlotMap sm{a.T, a.F, a.L, a.G, (int)(blockIdx.x * kWavesPerBlock + wave) * a.G};
+  if (sm.l0 < a.L) temporal_fwd_wave<D>(a, sm, h, b, (VC_LDS __bf16*)stage + wave * stage_elems<D>());
   if (SUM) {
     __syncthreads();  // this workgroup's rows of o are written
     const int wl0 = (int)blockIdx.x * kWavesPerBlock * a.G;  // first position of the workgroup
@@ -180,10 +192,20 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_fwd_kernel(Tempo
 // order the accumulator layout produces.
 template <int D>
 __global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_bwd_kernel(TemporalArgs a) {
+  // Per wave: K rows of its 32 slots (the dQ part), later Q rows in the same place (the
+  // dK/dV part), dO rows; then LSE*log2e and -D of the slots. Two workgroups fit a CU.
+  __shared__ __attribute__((aligned(16))) __bf16 stage[kWavesPerBlock * 2 * stage_elems<D>()];
+  __shared__ float stat[kWavesPerBlock * 2 * kSlots];
   const int lane = threadIdx.x & 63;
   const int l32 = lane & 31;
   const int hi = lane >> 5;
-  const int blk = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+  const int wave = threadIdx.x >> 6;
+  VC_LDS __bf16* k_rows = (VC_LDS __bf16*)stage + wave * 2 * stage_elems<D>();
+  VC_LDS __bf16* q_rows = k_rows;  // once the dQ part has read K
+  VC_LDS __bf16* do_rows = k_rows + stage_elems<D>();
+  VC_LDS float* lse_slot = (VC_LDS float*)stat + wave * 2 * kSlots;
+  VC_LDS float* nd_slot = lse_slot + kSlots;
+  const int blk = blockIdx.x * kWavesPerBlock + wave;
   const int h = blockIdx.y;
   const int b = blockIdx.z;
   SlotMap sm{a.T, a.F, a.L, a.G, blk * a.G};
@@ -205,13 +227,20 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_bwd_kernel(Tempo
     kf[ks] = *(const bf16x8*)(a.k + off);
     vf[ks] = *(const bf16x8*)(a.v + off);
     dof[ks] = *(const bf16x8*)(a.dout + off);
+    const int e = s * (D + kRowPad) + 16 * ks + 8 * hi;
+    *(VC_LDS bf16x8*)(k_rows + e) = kf[ks];
+    *(VC_LDS bf16x8*)(do_rows + e) = dof[ks];
   }
-  // Rows of the slots an operand element t of k-step st refers to (gathers).
-  size_t grow[2][8];
+  if (hi == 0) {
+    lse_slot[s] = a.lse2[rbase + n];
+    nd_slot[s] = a.dd[rbase + n];
+  }
+  // LDS rows of the slots an operand element t of k-step st refers to.
+  int grow[2][8];
 #pragma unroll
   for (int st = 0; st < 2; ++st)
 #pragma unroll
-    for (int t = 0; t < 8; ++t) grow[st][t] = base + (size_t)sm.token(op_slot(st, t, hi)) * tok;
+    for (int t = 0; t < 8; ++t) grow[st][t] = op_slot(st, t, hi) * (D + kRowPad);
 
   // ---- lane = query: dQ ----
   {
@@ -243,7 +272,7 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_bwd_kernel(Tempo
       for (int st = 0; st < 2; ++st) {
         bf16x8 kt;
 #pragma unroll
-        for (int t = 0; t < 8; ++t) kt[t] = a.k[grow[st][t] + db * 32 + l32];
+        for (int t = 0; t < 8; ++t) kt[t] = k_rows[grow[st][t] + db * 32 + l32];
         acc = mfma32(kt, sb[st], acc);
       }
       if (s_ok) {
@@ -257,6 +286,10 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_bwd_kernel(Tempo
     }
   }
   // ---- lane = key: dK, dV ----
+  // Q rows replace the K rows (LDS operations of a wave complete in order, so every read
+  // of K above precedes these writes).
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) *(VC_LDS bf16x8*)(q_rows + s * (D + kRowPad) + 16 * ks + 8 * hi) = qf[ks];
   {
     f32x16 sacc = zero_f32x16(), pacc = zero_f32x16();
 #pragma unroll
@@ -271,9 +304,8 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_bwd_kernel(Tempo
     for (int r = 0; r < 16; ++r) {
       const int i = acc_slot(r, hi);  // query slot
       const bool ok = k_ok & (i >= lo) & (i < lo + a.F) & sm.ok(i);
-      const int ni = sm.token(i);
-      const float l2 = a.lse2[rbase + ni];
-      const float d = a.dd[rbase + ni];
+      const float l2 = lse_slot[i];
+      const float d = nd_slot[i];
       p[r] = ok ? fast_exp2(fmaf(sacc[r], a.scale_log2, -l2)) : 0.0f;
       ds[r] = p[r] * (pacc[r] + d);
     }
@@ -292,8 +324,8 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_bwd_kernel(Tempo
         bf16x8 dot, qt;
 #pragma unroll
         for (int t = 0; t < 8; ++t) {
-          dot[t] = a.dout[grow[st][t] + db * 32 + l32];
-          qt[t] = a.q[grow[st][t] + db * 32 + l32];
+          dot[t] = do_rows[grow[st][t] + db * 32 + l32];
+          qt[t] = q_rows[grow[st][t] + db * 32 + l32];
         }
         vacc = mfma32(dot, pb[st], vacc);
         kacc = mfma32(qt, sb[st], kacc);
