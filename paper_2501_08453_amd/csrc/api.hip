@@ -17,6 +17,7 @@ constexpr int kMaxDevices = 64;
 struct DeviceInfo {
   std::once_flag once;
   bool is_gfx950 = false;
+  int cus = 0;  // compute units
 };
 DeviceInfo g_devices[kMaxDevices];
 
@@ -26,10 +27,19 @@ vc_status check_device() {
   DeviceInfo& di = g_devices[dev];
   std::call_once(di.once, [&] {
     hipDeviceProp_t prop;
-    if (hipGetDeviceProperties(&prop, dev) == hipSuccess)
+    if (hipGetDeviceProperties(&prop, dev) == hipSuccess) {
       di.is_gfx950 = strncmp(prop.gcnArchName, "gfx950", 6) == 0;
+      di.cus = prop.multiProcessorCount;
+    }
   });
   return di.is_gfx950 ? VC_OK : VC_ERR_DEVICE;
+}
+
+// Compute units of the current device (after check_device succeeded).
+int device_cus() {
+  int dev = 0;
+  (void)hipGetDevice(&dev);
+  return g_devices[dev].cus;
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -72,7 +82,36 @@ size_t rows_bytes(const vc_jointattn_desc* d, int64_t n) {
   return align256((size_t)d->batch * d->heads * (size_t)ntiles(n) * vcja::kTileTok * sizeof(float));
 }
 
-// Backward workspace: -D | LSE*log2(e) | Q^T tiles | dO^T tiles | K^T tiles.
+// Joint attention: split of the last, partial round of a kernel's dispatch. With W items
+// (256-row blocks x heads x samples) on `cus` compute units, the R = W mod cus items of the
+// last round are each split into C = cus / R workgroups over runs of `span` tiles along the
+// other token axis, so that the round ends after about 1/C of an item's time. At most
+// kTailMaxWgs split workgroups (the workspace is planned for that many).
+constexpr int kTailMaxWgs = 256;
+constexpr int kRowsPerItem = 256;
+struct TailPlan {
+  int items, chunks, span;
+};
+TailPlan tail_plan(int64_t work_items, int ntile, int cus) {
+  cus = std::min(cus, kTailMaxWgs);
+  if (cus < 2 || work_items <= cus) return TailPlan{0, 1, 0};
+  const int r = (int)(work_items % cus);
+  if (r == 0 || cus / r < 2) return TailPlan{0, 1, 0};
+  const int span = (ntile + cus / r - 1) / (cus / r);
+  return TailPlan{r, (ntile + span - 1) / span, span};
+}
+// Items of the joint kernels (256-row blocks x heads x samples).
+int64_t joint_items(const vc_jointattn_desc* d, int64_t n) {
+  return ((n + kRowsPerItem - 1) / kRowsPerItem) * d->heads * d->batch;
+}
+// fp32 partials of the split tail: dK and dV of up to kTailMaxWgs workgroups of 256 keys
+// (the dQ pass reuses the region for its single tensor).
+size_t tail_part_bytes(const vc_jointattn_desc* d, int64_t n) {
+  const int64_t wgs = std::min<int64_t>(kTailMaxWgs, joint_items(d, n));
+  return align256((size_t)2 * wgs * kRowsPerItem * d->head_dim * sizeof(float));
+}
+
+// Backward workspace: -D | LSE*log2(e) | Q^T tiles | dO^T tiles | K^T tiles | tail partials.
 struct BwdWorkspace {
   float* dd;
   float* lse2;
@@ -81,7 +120,12 @@ struct BwdWorkspace {
   __bf16* kt;
 };
 
-size_t bwd_ws_bytes(const vc_jointattn_desc* d, int64_t n) { return 2 * rows_bytes(d, n) + 3 * tiles_bytes(d, n); }
+size_t bwd_ws_bytes(const vc_jointattn_desc* d, int64_t n) {
+  return 2 * rows_bytes(d, n) + 3 * tiles_bytes(d, n) + tail_part_bytes(d, n);
+}
+float* tail_part_of(const vc_jointattn_desc* d, int64_t n, void* ws) {
+  return reinterpret_cast<float*>(static_cast<char*>(ws) + 2 * rows_bytes(d, n) + 3 * tiles_bytes(d, n));
+}
 
 BwdWorkspace split_bwd_ws(const vc_jointattn_desc* d, int64_t n, void* ws) {
   char* p = static_cast<char*>(ws);
@@ -298,6 +342,11 @@ vc_status dkdv_impl(const vc_jointattn_desc* desc, const void* q, const void* k,
   a.text_blocks = ts.blocks;
   a.text_chunks = ts.chunks;
   a.text_span = ts.span;
+  const TailPlan tp = spatial ? TailPlan{0, 1, 0} : tail_plan(joint_items(desc, n), ntiles(n), device_cus());
+  a.tail_part = tail_part_of(desc, n, workspace);
+  a.tail_blocks = tp.items;
+  a.tail_chunks = tp.chunks;
+  a.tail_span = tp.span;
   a.q = bf(q);
   a.k = bf(k);
   a.v = bf(v);

@@ -91,9 +91,22 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index (uniform)
   const int l32 = lane & 31;
   const int hi = lane >> 5;
-  const int3 gp = xcd_grid_pos(SPATIAL);
-  const int h = gp.y;
-  const int b = gp.z;
+  // Spatial branch: 3-D grid (key block slot, head, sample), renumbered by XCD. Joint: 1-D
+  // grid of items with the split tail dispatched last.
+  int gx, h, b;
+  TailItem ti{0, 0, 0, -1, 0};
+  if (SPATIAL) {
+    const int3 gp = xcd_grid_pos(true);
+    gx = gp.x;
+    h = gp.y;
+    b = gp.z;
+  } else {
+    ti = tail_item(blockIdx.x, (a.N + kBKV - 1) / kBKV, a.H, a.B, a.tail_blocks);
+    gx = ti.blk;
+    h = ti.h;
+    b = ti.b;
+  }
+  const bool tail = !SPATIAL && ti.chunk >= 0;
   const int N = a.N;
   const size_t tok = (size_t)a.H * D;
   const size_t base = (size_t)b * N * tok + (size_t)h * D;
@@ -102,13 +115,13 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
   // Spatial branch with split text blocks: workgroups [0, text_blocks*text_chunks) of a head
   // take (text block, chunk of its query tiles) and come first in dispatch order, the rest
   // the other key blocks in order.
-  int kb = gp.x, chunk = 0;
+  int kb = gx, chunk = 0;
   bool split = false;
   if (SPATIAL && a.text_chunks > 1) {
     const int nsplit = a.text_blocks * a.text_chunks;
-    split = gp.x < nsplit;
-    kb = split ? gp.x % a.text_blocks : gp.x - nsplit + a.text_blocks;
-    chunk = split ? gp.x / a.text_blocks : 0;
+    split = gx < nsplit;
+    kb = split ? gx % a.text_blocks : gx - nsplit + a.text_blocks;
+    chunk = split ? gx / a.text_blocks : 0;
   }
   // This workgroup's keys (spatial branch: text keys, or keys of one frame).
   const RowBlock rb = row_block(kb, N, a.T, SPATIAL ? a.frame_len : 0, kBKV, true);
@@ -119,6 +132,11 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
   const size_t part_stride = (size_t)a.text_chunks * a.B * a.H * a.text_blocks * kBKV * D;
   auto part_k = [&]() {
     return a.text_part + ((((size_t)chunk * a.B + b) * a.H + h) * a.text_blocks * kBKV + key) * D;
+  };
+  // Joint tail: partial dK of this lane's key (dV partials follow all dK partials).
+  const size_t tail_stride = (size_t)a.tail_blocks * a.tail_chunks * kBKV * D;
+  auto tail_k = [&]() {
+    return a.tail_part + (((size_t)ti.slot * a.tail_chunks + ti.chunk) * kBKV + (key - rb.r0)) * D;
   };
 
   AttendRule rule;
@@ -131,7 +149,14 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
 
   if (!__syncthreads_or(valid)) {
     // No valid key in this workgroup: its dK, dV (or partials) are zero.
-    if (split) {
+    if (tail) {
+      const f32x4 z = {0.0f, 0.0f, 0.0f, 0.0f};
+      float* pk = tail_k();
+      for (int c = 0; c < D / 4; ++c) {
+        *(f32x4*)(pk + 4 * c) = z;
+        *(f32x4*)(pk + tail_stride + 4 * c) = z;
+      }
+    } else if (split) {
       const f32x4 z = {0.0f, 0.0f, 0.0f, 0.0f};
       float* pk = part_k();
       for (int c = 0; c < D / 4; ++c) {
@@ -194,7 +219,12 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
     runs.b1 = min(runs.b1, c0 + a.text_span);
     if (runs.b0 >= runs.b1) runs.b1 = 0;
   }
-  auto next_q = [&](int qt) { return SPATIAL ? runs.next(qt) : qt; };
+  if (tail) {  // this chunk's run of query tiles
+    runs.b0 = ti.chunk * a.tail_span;
+    runs.b1 = min(a.ntile, runs.b0 + a.tail_span);
+    if (runs.b0 >= runs.b1) runs.b1 = 0;
+  }
+  auto next_q = [&](int qt) { return (SPATIAL || tail) ? runs.next(qt) : qt; };
   // Spatial branch: a tile needs the per-pair test unless this wave's keys are all text
   // and the tile holds video queries only, or they all lie in one frame containing it.
   // (a wave past the end of a short block takes its last row)
@@ -293,7 +323,23 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
     qt = qn;
   }
 
-  if (split) {
+  if (tail) {
+    // An invalid key's partials are zero (its accumulators may hold anything).
+    float* pk = tail_k();
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        f32x4 tk, tv;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          tk[e] = valid ? dk_acc[db][4 * j + e] * a.scale : 0.0f;
+          tv[e] = valid ? dv_acc[db][4 * j + e] : 0.0f;
+        }
+        *(f32x4*)(pk + db * 32 + 8 * j + 4 * hi) = tk;
+        *(f32x4*)(pk + tail_stride + db * 32 + 8 * j + 4 * hi) = tv;
+      }
+  } else if (split) {
     float* pk = part_k();
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
@@ -345,6 +391,34 @@ __global__ void text_reduce_kernel(const float* part, __bf16* dk, __bf16* dv, in
   for (int c = 0; c < chunks; ++c) {
     sk += *(const f32x4*)(part + c * stride + off);
     sv += *(const f32x4*)(part + (size_t)chunks * stride + c * stride + off);
+  }
+  const size_t o = (((size_t)b * N + row) * H + h) * D + d;
+  *(bf16x4*)(dk + o) = bf16x4{(__bf16)sk[0], (__bf16)sk[1], (__bf16)sk[2], (__bf16)sk[3]};
+  *(bf16x4*)(dv + o) = bf16x4{(__bf16)sv[0], (__bf16)sv[1], (__bf16)sv[2], (__bf16)sv[3]};
+}
+
+// Joint tail of the dK/dV kernel: dK, dV of the split items as the sum of their chunks'
+// fp32 partials. One thread per 4 dims of one key row.
+template <int D>
+__global__ void tail_reduce_kernel(const float* part, __bf16* dk, __bf16* dv, int B, int H, int N, int items,
+                                   int chunks) {
+  const int nblk = (N + kBKV - 1) / kBKV;
+  const size_t total = (size_t)items * kBKV * (D / 4);
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= total) return;
+  const int d = (int)(i % (D / 4)) * 4;
+  const int k = (int)((i / (D / 4)) % kBKV);
+  const int slot = (int)(i / ((size_t)(D / 4) * kBKV));
+  const int item = nblk * H * B - items + slot;
+  const int row = (item % nblk) * kBKV + k;
+  if (row >= N) return;
+  const int h = (item / nblk) % H, b = item / (nblk * H);
+  const size_t stride = (size_t)items * chunks * kBKV * D;  // dK partials, then dV
+  f32x4 sk = {0.0f, 0.0f, 0.0f, 0.0f}, sv = sk;
+  for (int c = 0; c < chunks; ++c) {
+    const size_t off = (((size_t)slot * chunks + c) * kBKV + k) * D + d;
+    sk += *(const f32x4*)(part + off);
+    sv += *(const f32x4*)(part + stride + off);
   }
   const size_t o = (((size_t)b * N + row) * H + h) * D + d;
   *(bf16x4*)(dk + o) = bf16x4{(__bf16)sk[0], (__bf16)sk[1], (__bf16)sk[2], (__bf16)sk[3]};
@@ -511,9 +585,10 @@ hipError_t launch_bwd_prepare(const __bf16* o, const float* lse, const __bf16* d
 hipError_t launch_bwd_dkdv(const DkdvArgs& a, int head_dim, hipStream_t s) {
   const bool spatial = a.frame_len > 0;
   const bool split = spatial && a.text_chunks > 1;
-  dim3 grid(row_blocks(a.N, a.T, spatial ? a.frame_len : 0, kBKV, true) +
-                (split ? (a.text_chunks - 1) * a.text_blocks : 0),
-            a.H, a.B);
+  const int nblk = row_blocks(a.N, a.T, spatial ? a.frame_len : 0, kBKV, true);
+  // Spatial: 3-D grid renumbered by XCD. Joint: 1-D grid of items, the split tail last.
+  dim3 grid = spatial ? dim3(nblk + (split ? (a.text_chunks - 1) * a.text_blocks : 0), a.H, a.B)
+                      : dim3(nblk * a.H * a.B + a.tail_blocks * (a.tail_chunks - 1));
   if (head_dim == 128 && spatial)
     hipLaunchKernelGGL((bwd_dkdv_kernel<128, true>), grid, dim3(64 * kDkdvWaves), 0, s, a);
   else if (head_dim == 128)
@@ -522,6 +597,16 @@ hipError_t launch_bwd_dkdv(const DkdvArgs& a, int head_dim, hipStream_t s) {
     hipLaunchKernelGGL((bwd_dkdv_kernel<64, true>), grid, dim3(64 * kDkdvWaves), 0, s, a);
   else
     hipLaunchKernelGGL((bwd_dkdv_kernel<64, false>), grid, dim3(64 * kDkdvWaves), 0, s, a);
+  if (!spatial && a.tail_blocks > 0) {
+    const size_t threads = (size_t)a.tail_blocks * kBKV * (head_dim / 4);
+    dim3 rgrid((unsigned)((threads + 255) / 256));
+    if (head_dim == 128)
+      hipLaunchKernelGGL(tail_reduce_kernel<128>, rgrid, dim3(256), 0, s, a.tail_part, a.dk, a.dv, a.B, a.H, a.N,
+                         a.tail_blocks, a.tail_chunks);
+    else
+      hipLaunchKernelGGL(tail_reduce_kernel<64>, rgrid, dim3(256), 0, s, a.tail_part, a.dk, a.dv, a.B, a.H, a.N,
+                         a.tail_blocks, a.tail_chunks);
+  }
   if (split) {
     const int rows = a.text_blocks * kBKV;
     const int nrow = std::min(a.T, a.N);  // the text keys

@@ -140,6 +140,26 @@ __host__ __device__ constexpr int tok_pos(int t) {
   return (t & ~15) | (((t >> 2) & 3) == 1 ? 8 : ((t >> 2) & 3) == 2 ? 4 : ((t >> 2) & 3) * 4) | (t & 3);
 }
 
+// Joint attention runs a 1-D grid of items (row block, head, sample), row block fastest.
+// The last `tail_items` items, those of the last, partial round of dispatch, are replaced by
+// tail_chunks workgroups each, dispatched after all others, every one over a run of tiles
+// along the other token axis; the round then ends after about 1/tail_chunks of the time.
+struct TailItem {
+  int blk, h, b;  // row block, head, sample
+  int chunk;      // -1: a whole item; else the run of tiles [chunk*span, (chunk+1)*span)
+  int slot;       // tail: index of the item among the split ones
+};
+__device__ __forceinline__ TailItem tail_item(int x, int nblk, int H, int B, int tail_items) {
+  const int regular = nblk * H * B - tail_items;
+  int item = x, chunk = -1, slot = 0;
+  if (x >= regular) {
+    slot = (x - regular) % tail_items;
+    chunk = (x - regular) / tail_items;
+    item = regular + slot;
+  }
+  return TailItem{item % nblk, (item / nblk) % H, item / (nblk * H), chunk, slot};
+}
+
 // The rows (queries or keys) a workgroup owns, [r0, r1), at most `per` of them. Joint
 // attention: uniform blocks over [0, N). Spatial branch: no block straddles a frame or the
 // text slot (a straddling block would visit the key tiles of two frames, each wave masking
@@ -285,6 +305,11 @@ struct DkdvArgs {
   // (dK partials, then dV). text_chunks = 1: no split, text_part unused.
   float* text_part;
   int text_blocks, text_chunks, text_span;
+  // Joint attention: the tail_blocks items of the last, partial round of dispatch are each
+  // split into tail_chunks workgroups over runs of tail_span query tiles, dispatched last,
+  // writing fp32 partial dK, dV (scaled) to tail_part, [2][tail_blocks][tail_chunks][256][D].
+  float* tail_part;
+  int tail_blocks, tail_chunks, tail_span;
 };
 
 constexpr int kDkdvKeys = 256;  // keys per dK/dV workgroup
