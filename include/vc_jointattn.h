@@ -98,7 +98,10 @@ const char* vc_status_string(int status);
 int64_t vc_jointattn_tokens(const vc_jointattn_desc* desc);
 
 /* Bytes of device workspace the forward needs: a token-major copy of V
- * ([B,H,ceil(N/64)] tiles of D x 72 bf16). 0 for an invalid descriptor. */
+ * ([B,H,ceil(N/64)] tiles of D x 72 bf16), then room for the fp32 partial
+ * results of up to 256 workgroups of 256 query rows (O, exponent base, sum),
+ * used when the work's last round of workgroups on the device is split over
+ * several workgroups to end early. 0 for an invalid descriptor. Host only. */
 size_t vc_jointattn_fwd_workspace_bytes(const vc_jointattn_desc* desc);
 
 /* Forward: o = softmax(c q k^T, masked) v and lse, as defined above.
@@ -112,9 +115,11 @@ vc_status vc_jointattn_fwd(const vc_jointattn_desc* desc,
                            void* o, float* lse,
                            void* workspace, size_t workspace_bytes, void* stream);
 
-/* Bytes of device workspace the backward needs: per query row fp32 D and
- * LSE*log2(e) ([B,H,Npad], Npad = N rounded up to 64), and token-major copies of
- * Q, dO and K (as for the forward's V). 0 for an invalid descriptor. Host only. */
+/* Bytes of device workspace the backward needs: per query row fp32 -D and
+ * LSE*log2(e) ([B,H,Npad], Npad = N rounded up to 64), token-major copies of
+ * Q, dO and K (as for the forward's V), and room for fp32 partial dK, dV (or
+ * dQ) of up to 256 workgroups of 256 rows, used as in the forward. 0 for an
+ * invalid descriptor. Host only. */
 size_t vc_jointattn_bwd_workspace_bytes(const vc_jointattn_desc* desc);
 
 /* Backward: dq, dk, dv (bf16 [B,N,H,D]) from q, k, v, the forward's o and lse,
@@ -122,8 +127,10 @@ size_t vc_jointattn_bwd_workspace_bytes(const vc_jointattn_desc* desc);
  * order. `workspace` is caller-owned device memory of at least
  * vc_jointattn_bwd_workspace_bytes(desc) bytes, 256-byte aligned; its contents
  * on entry do not matter. Masked keys get dk = dv = 0 exactly. No atomics are
- * used: the result is bitwise reproducible for either value of
- * desc->deterministic. */
+ * used: the result is bitwise reproducible run to run for either value of
+ * desc->deterministic (on devices with a different number of compute units the
+ * split of the last round of workgroups, and so the summation order of its
+ * rows, differs). */
 vc_status vc_jointattn_bwd(const vc_jointattn_desc* desc,
                            const void* q, const void* k, const void* v,
                            const void* o, const float* lse, const void* dout,

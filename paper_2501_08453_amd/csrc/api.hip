@@ -111,6 +111,13 @@ size_t tail_part_bytes(const vc_jointattn_desc* d, int64_t n) {
   return align256((size_t)2 * wgs * kRowsPerItem * d->head_dim * sizeof(float));
 }
 
+// Forward workspace: V^T tiles | split-tail partials (unnormalised O, base, sum per row).
+size_t fwd_tail_bytes(const vc_jointattn_desc* d, int64_t n) {
+  const int64_t wgs = std::min<int64_t>(kTailMaxWgs, joint_items(d, n));
+  return align256((size_t)wgs * kRowsPerItem * (d->head_dim + 2) * sizeof(float));
+}
+size_t fwd_ws_bytes(const vc_jointattn_desc* d, int64_t n) { return tiles_bytes(d, n) + fwd_tail_bytes(d, n); }
+
 // Backward workspace: -D | LSE*log2(e) | Q^T tiles | dO^T tiles | K^T tiles | tail partials.
 struct BwdWorkspace {
   float* dd;
@@ -222,7 +229,7 @@ int64_t vc_jointattn_tokens(const vc_jointattn_desc* desc) {
 size_t vc_jointattn_fwd_workspace_bytes(const vc_jointattn_desc* desc) {
   int64_t n = 0;
   if (check_desc(desc, &n) != VC_OK) return 0;
-  return tiles_bytes(desc, n);
+  return fwd_ws_bytes(desc, n);
 }
 
 size_t vc_jointattn_bwd_workspace_bytes(const vc_jointattn_desc* desc) {
@@ -251,7 +258,7 @@ vc_status fwd_impl(const vc_jointattn_desc* desc, const void* q, const void* k, 
   if (!q || !k || !v || !o || !lse) return VC_ERR_NULL;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse) || !aligned4(text_len))
     return VC_ERR_ALIGN;
-  if ((st = check_ws(workspace, workspace_bytes, tiles_bytes(desc, n))) != VC_OK) return st;
+  if ((st = check_ws(workspace, workspace_bytes, fwd_ws_bytes(desc, n))) != VC_OK) return st;
   if ((st = check_device()) != VC_OK) return st;
   __bf16* vt = static_cast<__bf16*>(workspace);
   if (vcja::launch_token_tiles(bf(v), vt, desc->batch, desc->heads, (int)n, desc->head_dim, as_stream(stream)) !=
@@ -272,6 +279,11 @@ vc_status fwd_impl(const vc_jointattn_desc* desc, const void* q, const void* k, 
   a.ntile = ntiles(n);
   a.frame_len = spatial ? desc->grid_h * desc->grid_w : 0;
   a.scale_log2 = scale_of(desc) * vcja::kLog2e;
+  const TailPlan tp = spatial ? TailPlan{0, 1, 0} : tail_plan(joint_items(desc, n), ntiles(n), device_cus());
+  a.tail_part = reinterpret_cast<float*>(static_cast<char*>(workspace) + tiles_bytes(desc, n));
+  a.tail_blocks = tp.items;
+  a.tail_chunks = tp.chunks;
+  a.tail_span = tp.span;
   // Spatial branch: text rows are not queries; their o and lse are written here.
   if (spatial && vcja::launch_text_rows(a.o, nullptr, nullptr, lse, a.B, a.H, a.N, a.T, desc->head_dim,
                                         as_stream(stream)) != hipSuccess)
@@ -393,6 +405,11 @@ vc_status dq_impl(const vc_jointattn_desc* desc, const void* q, const void* k, c
   a.text_len = text_len;
   a.key_mask = key_mask;
   a.dq = static_cast<__bf16*>(dq);
+  const TailPlan tp = spatial ? TailPlan{0, 1, 0} : tail_plan(joint_items(desc, n), ntiles(n), device_cus());
+  a.tail_part = tail_part_of(desc, n, workspace);
+  a.tail_blocks = tp.items;
+  a.tail_chunks = tp.chunks;
+  a.tail_span = tp.span;
   a.B = desc->batch;
   a.H = desc->heads;
   a.N = (int)n;

@@ -440,16 +440,28 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index (uniform)
   const int l32 = lane & 31;
   const int hi = lane >> 5;
-  const int3 gp = xcd_grid_pos(a.frame_len != 0);
-  const int h = gp.y;
-  const int b = gp.z;
+  // Spatial branch: 3-D grid renumbered by XCD. Joint: 1-D grid of items, split tail last.
+  int gx, h, b;
+  TailItem ti{0, 0, 0, -1, 0};
+  if (a.frame_len) {
+    const int3 gp = xcd_grid_pos(true);
+    gx = gp.x;
+    h = gp.y;
+    b = gp.z;
+  } else {
+    ti = tail_item(blockIdx.x, (a.N + kDqBM - 1) / kDqBM, a.H, a.B, a.tail_blocks);
+    gx = ti.blk;
+    h = ti.h;
+    b = ti.b;
+  }
+  const bool tail = ti.chunk >= 0;
   const int N = a.N;
   const size_t tok = (size_t)a.H * D;
   const size_t base = (size_t)b * N * tok + (size_t)h * D;
   const size_t bh = (size_t)b * a.H + h;
   // This workgroup's queries (spatial branch: inside one frame; text rows of dQ are written
   // by the caller's text-rows pass).
-  const RowBlock rb = row_block(gp.x, N, a.T, a.frame_len, kDqBM, false);
+  const RowBlock rb = row_block(gx, N, a.T, a.frame_len, kDqBM, false);
   const int qi = rb.r0 + w * 32 + l32;  // this lane's query (accumulator column)
   const int qr = min(qi, rb.r1 - 1);
 
@@ -480,7 +492,12 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
   const bool wave_one_frame = wave_all_video && a.frame_len && rule.frame_start(qw1) == wqs;
   const QueryRange qrange = query_range(rule, qi);
   // Key tiles this workgroup visits (the same sequence for every wave).
-  const TileRuns runs = rule.key_tiles(rb.r0, rb.r1, a.ntile);
+  TileRuns runs = rule.key_tiles(rb.r0, rb.r1, a.ntile);
+  const int kt0 = tail ? ti.chunk * a.tail_span : 0;  // joint tail: this chunk's key tiles
+  if (tail) {
+    runs.a1 = min(runs.a1, kt0 + a.tail_span);
+    runs.b1 = min(runs.b1, kt0 + a.tail_span);
+  }
   auto next_tile = [&](int kt) { return runs.next(kt); };
   auto issue = [&](int kt, int st) {
     VC_LDS char* sk = (VC_LDS char*)smem + st * STAGE;
@@ -492,7 +509,7 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
     for (int idx = w; idx < TCOPIES; idx += kDqWaves) copy16_to_lds(tsrc + idx * 512 + lane * 8, sk + 2 * RT + idx * 1024);
   };
 
-  int kt = next_tile(0);
+  int kt = next_tile(kt0);
   if (kt < a.ntile) issue(kt, 0);
   int st = 0;
   while (kt < a.ntile) {
@@ -556,7 +573,17 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
     kt = kn;
   }
 
-  if (qi < rb.r1) {
+  if (tail) {  // partial dQ of this lane's query row
+    float* pq = a.tail_part + (((size_t)ti.slot * a.tail_chunks + ti.chunk) * kDqBM + (qi - rb.r0)) * D;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const f32x4 t = {dq_acc[db][4 * j + 0] * a.scale, dq_acc[db][4 * j + 1] * a.scale,
+                         dq_acc[db][4 * j + 2] * a.scale, dq_acc[db][4 * j + 3] * a.scale};
+        *(f32x4*)(pq + db * 32 + 8 * j + 4 * hi) = t;
+      }
+  } else if (qi < rb.r1) {
     __bf16* qp = a.dq + base + (size_t)qi * tok;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
@@ -567,6 +594,25 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
         *(bf16x4*)(qp + db * 32 + 8 * j + 4 * hi) = t;
       }
   }
+}
+
+// Joint tail of the dQ kernel: dQ of the split items as the sum of their chunks' partials.
+template <int D>
+__global__ void tail_reduce_dq_kernel(const float* part, __bf16* dq, int B, int H, int N, int items, int chunks) {
+  const int nblk = (N + kDqBM - 1) / kDqBM;
+  const size_t total = (size_t)items * kDqBM * (D / 4);
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= total) return;
+  const int d = (int)(i % (D / 4)) * 4;
+  const int k = (int)((i / (D / 4)) % kDqBM);
+  const int slot = (int)(i / ((size_t)(D / 4) * kDqBM));
+  const int item = nblk * H * B - items + slot;
+  const int row = (item % nblk) * kDqBM + k;
+  if (row >= N) return;
+  const int h = (item / nblk) % H, b = item / (nblk * H);
+  f32x4 s = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int c = 0; c < chunks; ++c) s += *(const f32x4*)(part + (((size_t)slot * chunks + c) * kDqBM + k) * D + d);
+  *(bf16x4*)(dq + (((size_t)b * N + row) * H + h) * D + d) = bf16x4{(__bf16)s[0], (__bf16)s[1], (__bf16)s[2], (__bf16)s[3]};
 }
 
 }  // namespace
@@ -623,11 +669,23 @@ hipError_t launch_bwd_dkdv(const DkdvArgs& a, int head_dim, hipStream_t s) {
 }
 
 hipError_t launch_bwd_dq(const DqArgs& a, int head_dim, hipStream_t s) {
-  dim3 grid(row_blocks(a.N, a.T, a.frame_len, kDqBM, false), a.H, a.B);
+  const int nblk = row_blocks(a.N, a.T, a.frame_len, kDqBM, false);
+  // Spatial: 3-D grid renumbered by XCD. Joint: 1-D grid of items, the split tail last.
+  dim3 grid = a.frame_len ? dim3(nblk, a.H, a.B) : dim3(nblk * a.H * a.B + a.tail_blocks * (a.tail_chunks - 1));
   if (head_dim == 128)
     hipLaunchKernelGGL(bwd_dq_kernel<128>, grid, dim3(64 * kDqWaves), 0, s, a);
   else
     hipLaunchKernelGGL(bwd_dq_kernel<64>, grid, dim3(64 * kDqWaves), 0, s, a);
+  if (!a.frame_len && a.tail_blocks > 0) {
+    const size_t threads = (size_t)a.tail_blocks * kDqBM * (head_dim / 4);
+    dim3 rgrid((unsigned)((threads + 255) / 256));
+    if (head_dim == 128)
+      hipLaunchKernelGGL(tail_reduce_dq_kernel<128>, rgrid, dim3(256), 0, s, a.tail_part, a.dq, a.B, a.H, a.N,
+                         a.tail_blocks, a.tail_chunks);
+    else
+      hipLaunchKernelGGL(tail_reduce_dq_kernel<64>, rgrid, dim3(256), 0, s, a.tail_part, a.dq, a.B, a.H, a.N,
+                         a.tail_blocks, a.tail_chunks);
+  }
   return hipGetLastError();
 }
 

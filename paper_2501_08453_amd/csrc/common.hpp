@@ -279,6 +279,11 @@ struct FwdArgs {
   int B, H, N, T, ntile;  // ntile = tiles of 64 tokens per (sample, head)
   int frame_len;          // 0: joint attention; > 0: spatial branch with frames of this many tokens
   float scale_log2;       // softmax scale times log2(e)
+  // Joint attention: split tail over runs of tail_span key tiles. Per split workgroup row,
+  // tail_part holds the unnormalised fp32 O ([tail_blocks][tail_chunks][256][D]), then the
+  // exponent base m (log2 units) and the probability sum l ([tail_blocks][tail_chunks][256]).
+  float* tail_part;
+  int tail_blocks, tail_chunks, tail_span;
 };
 
 // Backward, key-stationary part: dK and dV.
@@ -330,6 +335,10 @@ struct DqArgs {
   int frame_len;        // 0: joint attention; > 0: spatial branch
   float scale;
   float scale_log2;
+  // Joint attention: split tail as for dK/dV, over runs of tail_span key tiles; fp32
+  // partial dQ (scaled) in tail_part, [tail_blocks][tail_chunks][256][D].
+  float* tail_part;
+  int tail_blocks, tail_chunks, tail_span;
 };
 
 // Temporal branch: attention of each spatial position across the F frames. Video token

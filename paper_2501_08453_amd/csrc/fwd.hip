@@ -178,16 +178,28 @@ __global__ __launch_bounds__(64 * kWaves, kWavesPerSimd * 4 / kWaves) void fwd_k
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index (uniform)
   const int l32 = lane & 31;
   const int hi = lane >> 5;
-  const int3 gp = xcd_grid_pos(a.frame_len != 0);
-  const int h = gp.y;
-  const int b = gp.z;
+  // Spatial branch: 3-D grid renumbered by XCD. Joint: 1-D grid of items, split tail last.
+  int gx, h, b;
+  TailItem ti{0, 0, 0, -1, 0};
+  if (a.frame_len) {
+    const int3 gp = xcd_grid_pos(true);
+    gx = gp.x;
+    h = gp.y;
+    b = gp.z;
+  } else {
+    ti = tail_item(blockIdx.x, (a.N + kBM - 1) / kBM, a.H, a.B, a.tail_blocks);
+    gx = ti.blk;
+    h = ti.h;
+    b = ti.b;
+  }
+  const bool tail = ti.chunk >= 0;
   const int N = a.N;
   const size_t tok = (size_t)a.H * D;
   const size_t base = (size_t)b * N * tok + (size_t)h * D;
   const __bf16* vt_bh = a.vt + ((size_t)b * a.H + h) * a.ntile * tile_elems(D);
   // This workgroup's queries (spatial branch: inside one frame; text rows are written
   // by the caller's text-rows pass).
-  const RowBlock rb = row_block(gp.x, N, a.T, a.frame_len, kBM, false);
+  const RowBlock rb = row_block(gx, N, a.T, a.frame_len, kBM, false);
   const int qi = rb.r0 + w * 32 + l32;
   const bool q_in = qi < rb.r1;
 
@@ -216,7 +228,12 @@ __global__ __launch_bounds__(64 * kWaves, kWavesPerSimd * 4 / kWaves) void fwd_k
   }
   // Key tiles this workgroup visits (the same sequence for every wave): all but tiles of
   // padded text only in joint attention; text and own-frame tiles in the spatial branch.
-  const TileRuns runs = mask.rule.key_tiles(rb.r0, rb.r1, a.ntile);
+  TileRuns runs = mask.rule.key_tiles(rb.r0, rb.r1, a.ntile);
+  const int kt0 = tail ? ti.chunk * a.tail_span : 0;  // joint tail: this chunk's key tiles
+  if (tail) {
+    runs.a1 = min(runs.a1, kt0 + a.tail_span);
+    runs.b1 = min(runs.b1, kt0 + a.tail_span);
+  }
   auto next_tile = [&](int kt) { return runs.next(kt); };
   // Copies tile kt's K rows (rows past N repeat row N-1 and are masked) or V^T tile into
   // ring slot `slot`.
@@ -239,7 +256,7 @@ __global__ __launch_bounds__(64 * kWaves, kWavesPerSimd * 4 / kWaves) void fwd_k
   float l = 0.0f;       // running sum of this lane's half
   bf16x8 pb[4];         // probabilities of the current tile as PV operands
 
-  int cur = next_tile(0);
+  int cur = next_tile(kt0);
   if (cur < a.ntile) {
     int nxt = next_tile(cur + 1);
     int par = 0;  // ring slot of tile `cur`
@@ -318,7 +335,22 @@ __global__ __launch_bounds__(64 * kWaves, kWavesPerSimd * 4 / kWaves) void fwd_k
 
   const float lt = halves_sum(l);
   const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
-  if (q_in) {
+  if (tail) {  // this chunk's unnormalised O, base and sum for the merge
+    const size_t rows = (size_t)a.tail_blocks * a.tail_chunks * kBM;
+    const size_t row = ((size_t)ti.slot * a.tail_chunks + ti.chunk) * kBM + (qi - rb.r0);
+    float* po = a.tail_part + row * D;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const f32x4 t = {oacc[db][4 * j + 0], oacc[db][4 * j + 1], oacc[db][4 * j + 2], oacc[db][4 * j + 3]};
+        *(f32x4*)(po + db * 32 + 8 * j + 4 * hi) = t;
+      }
+    if (hi == 0) {
+      a.tail_part[rows * D + row] = m;
+      a.tail_part[rows * D + rows + row] = lt;
+    }
+  } else if (q_in) {
     __bf16* op = a.o + base + (size_t)qi * tok;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
@@ -333,14 +365,68 @@ __global__ __launch_bounds__(64 * kWaves, kWavesPerSimd * 4 / kWaves) void fwd_k
   }
 }
 
+// Joint tail: O and LSE of the split items from their chunks' partials,
+// O = sum_c 2^(m_c - M) O_c / sum_c 2^(m_c - M) l_c over the chunks that saw a valid key
+// (M the largest of their bases). One thread per 4 dims of one query row.
+template <int D>
+__global__ void tail_merge_kernel(const float* part, __bf16* o, float* lse, int B, int H, int N, int items,
+                                  int chunks) {
+  const int nblk = (N + kBM - 1) / kBM;
+  const size_t total = (size_t)items * kBM * (D / 4);
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= total) return;
+  const int d = (int)(i % (D / 4)) * 4;
+  const int k = (int)((i / (D / 4)) % kBM);
+  const int slot = (int)(i / ((size_t)(D / 4) * kBM));
+  const int item = nblk * H * B - items + slot;
+  const int row = (item % nblk) * kBM + k;
+  if (row >= N) return;
+  const int h = (item / nblk) % H, b = item / (nblk * H);
+  const size_t rows = (size_t)items * chunks * kBM;
+  const float* pm = part + rows * D;
+  const float* pl = pm + rows;
+  float mx = -INFINITY;
+  for (int c = 0; c < chunks; ++c) {
+    const size_t r = ((size_t)slot * chunks + c) * kBM + k;
+    if (pl[r] > 0.0f) mx = fmaxf(mx, pm[r]);
+  }
+  float sum = 0.0f;
+  f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int c = 0; c < chunks; ++c) {
+    const size_t r = ((size_t)slot * chunks + c) * kBM + k;
+    if (pl[r] > 0.0f) {
+      const float wgt = exp2f(pm[r] - mx);
+      sum += wgt * pl[r];
+      acc += wgt * *(const f32x4*)(part + r * D + d);
+    }
+  }
+  const float inv = sum > 0.0f ? 1.0f / sum : 0.0f;
+  const size_t off = (((size_t)b * N + row) * H + h) * D + d;
+  *(bf16x4*)(o + off) = bf16x4{(__bf16)(acc[0] * inv), (__bf16)(acc[1] * inv), (__bf16)(acc[2] * inv),
+                               (__bf16)(acc[3] * inv)};
+  if (d == 0) lse[((size_t)b * H + h) * N + row] = sum > 0.0f ? (mx + log2f(sum)) * kLn2 : -INFINITY;
+}
+
 }  // namespace
 
 hipError_t launch_fwd(const FwdArgs& a, int head_dim, hipStream_t s) {
-  dim3 grid(row_blocks(a.N, a.T, a.frame_len, kBM, false), a.H, a.B);
+  const int nblk = row_blocks(a.N, a.T, a.frame_len, kBM, false);
+  // Spatial: 3-D grid renumbered by XCD. Joint: 1-D grid of items, the split tail last.
+  dim3 grid = a.frame_len ? dim3(nblk, a.H, a.B) : dim3(nblk * a.H * a.B + a.tail_blocks * (a.tail_chunks - 1));
   if (head_dim == 128)
     hipLaunchKernelGGL(fwd_kernel<128>, grid, dim3(64 * kWaves), 0, s, a);
   else
     hipLaunchKernelGGL(fwd_kernel<64>, grid, dim3(64 * kWaves), 0, s, a);
+  if (!a.frame_len && a.tail_blocks > 0) {
+    const size_t threads = (size_t)a.tail_blocks * kBM * (head_dim / 4);
+    dim3 rgrid((unsigned)((threads + 255) / 256));
+    if (head_dim == 128)
+      hipLaunchKernelGGL(tail_merge_kernel<128>, rgrid, dim3(256), 0, s, a.tail_part, a.o, a.lse, a.B, a.H, a.N,
+                         a.tail_blocks, a.tail_chunks);
+    else
+      hipLaunchKernelGGL(tail_merge_kernel<64>, rgrid, dim3(256), 0, s, a.tail_part, a.o, a.lse, a.B, a.H, a.N,
+                         a.tail_blocks, a.tail_chunks);
+  }
   return hipGetLastError();
 }
 

@@ -48,7 +48,8 @@ def test_tokens_and_workspace():
     al = lambda x: (x + 255) // 256 * 256  # noqa: E731
     rows = al(24 * npad * 4)
     tiles = al(24 * (npad // 64) * 128 * 72 * 2)
-    assert vc.vc_jointattn_fwd_workspace_bytes(d3) == tiles
+    # V^T tiles, then per row of up to 256 split workgroups: fp32 O, base and sum
+    assert vc.vc_jointattn_fwd_workspace_bytes(d3) == tiles + 256 * 256 * (128 + 2) * 4
     # fp32 partial dK, dV of up to 256 split workgroups of 256 keys (the last, partial round
     # of the 5,424 workgroups)
     tail = 2 * 256 * 256 * 128 * 4
