@@ -59,6 +59,20 @@ def _full_compare(w, x, scale=None, key_mask=None, use_bf16_oracle=True, heads=N
     return out, valid
 
 
+def test_split_tail_of_last_round():
+    """Joint kernels split the items of their last, partial round of workgroups over several
+    workgroups (fp32 partials merged or summed afterwards). 9 heads x 30 blocks of 256 rows
+    = 270 items: on 256 compute units the last 14 items (blocks 16-29 of head 8) are split
+    into 18 chunks each. Head 8 (and head 0, unsplit) on every element, with ragged text and a
+    key mask so that split items hold masked keys too."""
+    w = W.custom(1, 9, 64, 100, 4, 43, 43, name="tail", ragged_text=True)
+    assert (w.tokens + 255) // 256 == 30
+    x = W.make_inputs(w, seed=71)
+    km = W.random_key_mask(w, seed=72, keep=0.9)
+    log("split tail: 270 items of 256 rows", w.shape)
+    _full_compare(w, x, key_mask=km, heads=[0, 8])
+
+
 def test_tiny_workload_fp32_oracle():
     """Workload 1 (144 tokens): oracle on the fp32 draws, GPU on their bf16 casts."""
     w = W.WORKLOADS[1]
