@@ -210,6 +210,9 @@ def main(argv=None):
     ap.add_argument("--layers", type=int, default=4, help="stacked layers for --branch block")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the oracle timing")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--deterministic", action="store_true",
+                    help="joint backward as separate dK/dV and dQ passes (bitwise reproducible) instead of "
+                         "the fused pass")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after the run, copy this many MiB device-to-device with one plain copy "
                          "kernel (reference for hardware byte counters)")
@@ -230,7 +233,7 @@ def main(argv=None):
     text_len = x["text_len"]
     tl = None if text_len is None else torch.from_numpy(text_len).to(dev)
     del x
-    desc = vc.desc_for(w)
+    desc = vc.desc_for(w, deterministic=args.deterministic)
     B, N, H, D = w.shape
     o = torch.empty_like(g["q"])
     lse = torch.empty((B, H, N), dtype=torch.float32, device=dev)
@@ -247,7 +250,11 @@ def main(argv=None):
     if args.branch != "joint":
         return branch_main(args, w, g, text_len, tl, desc, o, lse, dq, dk, dv, fws, ws, stream)
 
-    # Events bracket each stage on the stream the library launches on.
+    # Events bracket each stage on the stream the library launches on. Default: the fused
+    # backward (stage 1; the key-stationary pass for dK, dV and, for the leading key
+    # blocks, their dQ share: the accumulator fill, the kernel, the split tail's sum; the
+    # dQ pass over the other keys); --deterministic: stage 1 with all token-major copies,
+    # the dK/dV pass, the dQ pass over all keys.
     def step(ev=None):
         if ev:
             ev[0].record(stream)
@@ -257,7 +264,10 @@ def main(argv=None):
         vc.vc_jointattn_bwd_prepare(desc, q, k, o, lse, do, ws, wsb, sh)
         if ev:
             ev[2].record(stream)
-        vc.vc_jointattn_bwd_dkdv(desc, q, k, v, do, tl, None, dk, dv, ws, wsb, sh)
+        if args.deterministic:
+            vc.vc_jointattn_bwd_dkdv(desc, q, k, v, do, tl, None, dk, dv, ws, wsb, sh)
+        else:
+            vc.vc_jointattn_bwd_fused(desc, q, k, v, do, tl, None, dk, dv, ws, wsb, sh)
         if ev:
             ev[3].record(stream)
         vc.vc_jointattn_bwd_dq(desc, q, k, v, do, tl, None, dq, ws, wsb, sh)
@@ -281,9 +291,12 @@ def main(argv=None):
 
     f_fwd, f_bwd = flops(w, text_len)
     value = (f_fwd + f_bwd) / (ms_step * 1e-3) / 1e12
-    # The dK/dV kernel carries 3/4 of the backward's algorithmic flops (dP, dV, dK of
-    # dP, dV, dK, dQ); the dQ kernel the remaining dQ product (plus its recomputation).
-    dkdv_flops = 0.75 * f_bwd
+    # The dominant kernel is the key-stationary backward pass: it carries 3/4 of the
+    # backward's algorithmic flops (the dP, dV, dK products of dP, dV, dK, dQ) and, fused,
+    # the dQ product of its leading keys too (with text_len ragged the count is approximate
+    # by the masked text keys); the dQ pass the rest of the dQ product (plus recomputation).
+    fused_share = 0.0 if args.deterministic else vc.vc_jointattn_fused_dq_keys(desc) / N
+    dkdv_flops = (0.75 + 0.25 * fused_share) * f_bwd
     dkdv_tflops = dkdv_flops / (k_dkdv * 1e-3) / 1e12
     line = {
         "metric": METRIC,
@@ -306,13 +319,17 @@ def main(argv=None):
         },
         "pct_of_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
         "algorithmic_tflop_per_step": round((f_fwd + f_bwd) / 1e12, 4),
-        "kernels_ms": {"fwd": round(k_fwd, 4), "bwd_prepare": round(k_prep, 4), "bwd_dkdv": round(k_dkdv, 4),
+        "backward": "deterministic (separate dK/dV and dQ passes)" if args.deterministic
+                    else "fused (dQ of the leading %.0f%% of keys by fp32 atomics in the dK/dV pass)"
+                    % (100 * fused_share),
+        "kernels_ms": {"fwd": round(k_fwd, 4), "bwd_prepare": round(k_prep, 4),
+                       ("bwd_dkdv" if args.deterministic else "bwd_fused"): round(k_dkdv, 4),
                        "bwd_dq": round(k_dq, 4)},
         "fwd_tflops": round(f_fwd / (k_fwd * 1e-3) / 1e12, 2),
         "bwd_tflops": round(f_bwd / ((k_prep + k_dkdv + k_dq) * 1e-3) / 1e12, 2),
         "roofline": {
             "bound": "mfma",
-            "kernel": "bwd_dkdv_kernel",
+            "kernel": "bwd_dkdv_kernel" + ("" if args.deterministic else " (dQ fused)"),
             "achieved": round(dkdv_tflops, 2),
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
@@ -321,7 +338,7 @@ def main(argv=None):
             "algorithmic_flops_per_launch": dkdv_flops,
         },
     }
-    tr = traffic_record()
+    tr = None if args.deterministic else traffic_record()  # the record is the fused kernel's
     if tr is not None:
         line["roofline"]["traffic"] = tr
     if not args.no_cpu_baseline:

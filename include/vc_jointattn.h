@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define VC_JOINTATTN_ABI_VERSION 5
+#define VC_JOINTATTN_ABI_VERSION 6
 
 typedef enum vc_status {
   VC_OK = 0,
@@ -82,9 +82,11 @@ typedef struct vc_jointattn_desc {
   int32_t grid_h;         /* Hp >= 1: patch rows per frame                      */
   int32_t grid_w;         /* Wp >= 1: patch columns per frame                   */
   float softmax_scale;    /* c; <= 0 selects 1/sqrt(D)                          */
-  int32_t deterministic;  /* 0 or 1. Both give the same bitwise reproducible
-                             results (no atomics anywhere); kept so callers can
-                             state the requirement explicitly                  */
+  int32_t deterministic;  /* 0: the joint backward computes dQ inside the
+                             key-stationary kernel, adding it up with fp32
+                             atomics (fastest; dQ may differ from run to run
+                             by rounding). 1: a separate dQ pass, bitwise
+                             reproducible. Other results never use atomics. */
 } vc_jointattn_desc;
 
 /* Version of this ABI (VC_JOINTATTN_ABI_VERSION). */
@@ -117,20 +119,23 @@ vc_status vc_jointattn_fwd(const vc_jointattn_desc* desc,
 
 /* Bytes of device workspace the backward needs: per query row fp32 -D and
  * LSE*log2(e) ([B,H,Npad], Npad = N rounded up to 64), token-major copies of
- * Q, dO and K (as for the forward's V), and room for fp32 partial dK, dV (or
- * dQ) of up to 256 workgroups of 256 rows, used as in the forward. 0 for an
- * invalid descriptor. Host only. */
+ * Q, dO and K (as for the forward's V; with desc->deterministic = 0 the same
+ * region holds the fp32 dQ accumulator [B,N,H,D] instead), and room for fp32
+ * partial dK, dV (or dQ) of up to 256 workgroups of 256 rows, used as in the
+ * forward. 0 for an invalid descriptor. Host only. */
 size_t vc_jointattn_bwd_workspace_bytes(const vc_jointattn_desc* desc);
 
 /* Backward: dq, dk, dv (bf16 [B,N,H,D]) from q, k, v, the forward's o and lse,
- * and the upstream gradient dout. Equivalent to the three stage calls below in
- * order. `workspace` is caller-owned device memory of at least
- * vc_jointattn_bwd_workspace_bytes(desc) bytes, 256-byte aligned; its contents
- * on entry do not matter. Masked keys get dk = dv = 0 exactly. No atomics are
- * used: the result is bitwise reproducible run to run for either value of
- * desc->deterministic (on devices with a different number of compute units the
- * split of the last round of workgroups, and so the summation order of its
- * rows, differs). */
+ * and the upstream gradient dout. `workspace` is caller-owned device memory of
+ * at least vc_jointattn_bwd_workspace_bytes(desc) bytes, 256-byte aligned; its
+ * contents on entry do not matter. Masked keys get dk = dv = 0 exactly.
+ * desc->deterministic = 1: equivalent to the three stage calls below in order;
+ * no atomics, the result is bitwise reproducible run to run (on devices with a
+ * different number of compute units the split of the last round of
+ * workgroups, and so the summation order of its rows, differs).
+ * desc->deterministic = 0: stage 1 (token-major copy of k only),
+ * vc_jointattn_bwd_fused, then stage 3 over the remaining keys; dk, dv are
+ * reproducible run to run, dq only up to the rounding of its fp32 sums. */
 vc_status vc_jointattn_bwd(const vc_jointattn_desc* desc,
                            const void* q, const void* k, const void* v,
                            const void* o, const float* lse, const void* dout,
@@ -139,15 +144,17 @@ vc_status vc_jointattn_bwd(const vc_jointattn_desc* desc,
                            void* workspace, size_t workspace_bytes, void* stream);
 
 /* Backward stage 1: per query row, D_i = sum_d dO_id O_id and LSE_i*log2(e)
- * (fp32, padding rows made inert), and the token-major copies of q, dout and k,
- * all into the workspace. Memory-bound. */
+ * (fp32, padding rows made inert), the token-major copy of k and, when
+ * desc->deterministic = 1, those of q and dout, all into the workspace.
+ * Memory-bound. */
 vc_status vc_jointattn_bwd_prepare(const vc_jointattn_desc* desc,
                                    const void* q, const void* k,
                                    const void* o, const float* lse, const void* dout,
                                    void* workspace, size_t workspace_bytes, void* stream);
 
 /* Backward stage 2 (key-stationary): recompute P from the stage-1 LSE and write
- * dk = c dS^T Q and dv = P^T dO. Needs stage 1 on the same workspace. */
+ * dk = c dS^T Q and dv = P^T dO. Needs stage 1 on the same workspace, run with
+ * desc->deterministic = 1; VC_ERR_UNSUPPORTED if desc->deterministic is 0. */
 vc_status vc_jointattn_bwd_dkdv(const vc_jointattn_desc* desc,
                                 const void* q, const void* k, const void* v,
                                 const void* dout,
@@ -156,13 +163,37 @@ vc_status vc_jointattn_bwd_dkdv(const vc_jointattn_desc* desc,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
 /* Backward stage 3 (query-stationary): recompute P and dP and write
- * dq = c dS K. Needs stage 1 on the same workspace; independent of stage 2. */
+ * dq = c dS K. desc->deterministic = 1: over all keys; needs stage 1 on the
+ * same workspace, independent of stage 2. desc->deterministic = 0: completes
+ * the fused backward (stage 1, then vc_jointattn_bwd_fused, on the same
+ * workspace): over the keys whose blocks did not add their share of dQ in the
+ * fused pass, plus that pass's fp32 accumulator. */
 vc_status vc_jointattn_bwd_dq(const vc_jointattn_desc* desc,
                               const void* q, const void* k, const void* v,
                               const void* dout,
                               const int32_t* text_len, const uint8_t* key_mask,
                               void* dq,
                               void* workspace, size_t workspace_bytes, void* stream);
+
+/* Backward stage 2 of the fused backward (what vc_jointattn_bwd runs for
+ * desc->deterministic = 0; this call does not read the flag): one
+ * key-stationary pass recomputes P and dP and writes dk = c dS^T Q and
+ * dv = P^T dO; the key blocks of a fixed leading fraction also add their share
+ * of dq / c, dS K, to an fp32 accumulator in the workspace with atomics, so
+ * that S and dP of those keys are computed once. Needs stage 1 on the same
+ * workspace; stage 3 (vc_jointattn_bwd_dq with desc->deterministic = 0)
+ * completes dq. */
+/* Keys [0, K) whose share of dq the fused pass adds (vc_jointattn_bwd_fused);
+ * stage 3 covers keys [K, N). Returns K, or a negative vc_status if the
+ * descriptor is invalid. Host only. */
+int64_t vc_jointattn_fused_dq_keys(const vc_jointattn_desc* desc);
+
+vc_status vc_jointattn_bwd_fused(const vc_jointattn_desc* desc,
+                                 const void* q, const void* k, const void* v,
+                                 const void* dout,
+                                 const int32_t* text_len, const uint8_t* key_mask,
+                                 void* dk, void* dv,
+                                 void* workspace, size_t workspace_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
  * Spatial attention branch (Sec. III-B: the video sequence [B, F, L, ...]

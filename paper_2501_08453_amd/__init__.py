@@ -58,6 +58,8 @@ _SIGS = {
     "vc_jointattn_bwd_prepare": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "vc_jointattn_bwd_dkdv": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "vc_jointattn_bwd_dq": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "vc_jointattn_fused_dq_keys": (ctypes.c_int64, [_DP]),
+    "vc_jointattn_bwd_fused": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "vc_spatialattn_fwd": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "vc_spatialattn_bwd_workspace_bytes": (ctypes.c_size_t, [_DP]),
     "vc_spatialattn_bwd": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
@@ -183,6 +185,17 @@ def vc_jointattn_bwd_dkdv(desc, q, k, v, dout, text_len, key_mask, dk, dv, works
 def vc_jointattn_bwd_dq(desc, q, k, v, dout, text_len, key_mask, dq, workspace, workspace_bytes, stream=None):
     _call("vc_jointattn_bwd_dq", ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(dout),
           _ptr(text_len), _ptr(key_mask), _ptr(dq), _ptr(workspace), int(workspace_bytes), _stream(stream))
+
+
+def vc_jointattn_fused_dq_keys(desc) -> int:
+    return _lib().vc_jointattn_fused_dq_keys(ctypes.byref(desc))
+
+
+def vc_jointattn_bwd_fused(desc, q, k, v, dout, text_len, key_mask, dk, dv, workspace, workspace_bytes,
+                           stream=None):
+    _call("vc_jointattn_bwd_fused", ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(dout),
+          _ptr(text_len), _ptr(key_mask), _ptr(dk), _ptr(dv), _ptr(workspace), int(workspace_bytes),
+          _stream(stream))
 
 
 def vc_spatialattn_fwd(desc, q, k, v, text_len, key_mask, o, lse, workspace, workspace_bytes, stream=None):

@@ -111,6 +111,17 @@ size_t tail_part_bytes(const vc_jointattn_desc* d, int64_t n) {
   return align256((size_t)2 * wgs * kRowsPerItem * d->head_dim * sizeof(float));
 }
 
+// Fused backward: the key blocks [0, fused_dq_blocks) add their dQ share with atomics in
+// the key-stationary pass; the dQ pass covers the others. Per key block, the atomics (an
+// fp32 dQ tile per query tile) cost about what the dQ pass's recomputation of S and dP
+// costs, so the backward's time is nearly flat in the fraction between 1/2 and 7/8;
+// 65% measured fastest on the long workload.
+constexpr int kFusedDqPercent = 65;
+int fused_dq_blocks(int64_t n) {
+  const int nblk = (int)((n + vcja::kDkdvKeys - 1) / vcja::kDkdvKeys);
+  return (int)(((int64_t)nblk * kFusedDqPercent + 50) / 100);
+}
+
 // Forward workspace: V^T tiles | split-tail partials (unnormalised O, base, sum per row).
 size_t fwd_tail_bytes(const vc_jointattn_desc* d, int64_t n) {
   const int64_t wgs = std::min<int64_t>(kTailMaxWgs, joint_items(d, n));
@@ -238,6 +249,13 @@ size_t vc_jointattn_bwd_workspace_bytes(const vc_jointattn_desc* desc) {
   return bwd_ws_bytes(desc, n);
 }
 
+int64_t vc_jointattn_fused_dq_keys(const vc_jointattn_desc* desc) {
+  int64_t n = 0;
+  const vc_status st = check_desc(desc, &n);
+  if (st != VC_OK) return (int64_t)st;
+  return std::min<int64_t>(n, (int64_t)fused_dq_blocks(n) * vcja::kDkdvKeys);
+}
+
 size_t vc_spatialattn_bwd_workspace_bytes(const vc_jointattn_desc* desc) {
   int64_t n = 0;
   if (check_desc(desc, &n) != VC_OK) return 0;
@@ -247,6 +265,9 @@ size_t vc_spatialattn_bwd_workspace_bytes(const vc_jointattn_desc* desc) {
 }  // extern "C"
 
 namespace {
+
+vc_status prepare_impl(const vc_jointattn_desc* desc, const void* q, const void* k, const void* o, const float* lse,
+                       const void* dout, void* workspace, size_t workspace_bytes, void* stream, bool tiles);
 
 // Joint attention (frame_len 0) or the spatial branch (frame_len = tokens per frame).
 vc_status fwd_impl(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
@@ -310,6 +331,17 @@ vc_status vc_spatialattn_fwd(const vc_jointattn_desc* desc, const void* q, const
 vc_status vc_jointattn_bwd_prepare(const vc_jointattn_desc* desc, const void* q, const void* k, const void* o,
                                    const float* lse, const void* dout, void* workspace, size_t workspace_bytes,
                                    void* stream) {
+  return prepare_impl(desc, q, k, o, lse, dout, workspace, workspace_bytes, stream, desc && desc->deterministic);
+}
+
+}  // extern "C"
+
+namespace {
+
+// Backward stage 1; `tiles`: also the transposed token tiles of q and dout (read by the
+// separate dK/dV pass only; the fused backward reads those of k alone, in its dQ pass).
+vc_status prepare_impl(const vc_jointattn_desc* desc, const void* q, const void* k, const void* o, const float* lse,
+                       const void* dout, void* workspace, size_t workspace_bytes, void* stream, bool tiles) {
   int64_t n = 0;
   vc_status st = check_desc(desc, &n);
   if (st != VC_OK) return st;
@@ -321,21 +353,19 @@ vc_status vc_jointattn_bwd_prepare(const vc_jointattn_desc* desc, const void* q,
   const int B = desc->batch, H = desc->heads, D = desc->head_dim, N = (int)n;
   hipStream_t s = as_stream(stream);
   if (vcja::launch_bwd_prepare(bf(o), lse, bf(dout), w.dd, w.lse2, B, H, N, ntiles(n) * vcja::kTileTok, D, s) !=
-          hipSuccess ||
-      vcja::launch_token_tiles(bf(q), w.qt, B, H, N, D, s) != hipSuccess ||
-      vcja::launch_token_tiles(bf(dout), w.dot, B, H, N, D, s) != hipSuccess ||
-      vcja::launch_token_tiles(bf(k), w.kt, B, H, N, D, s) != hipSuccess)
+      hipSuccess)
     return VC_ERR_HIP;
+  if (tiles && (vcja::launch_token_tiles(bf(q), w.qt, B, H, N, D, s) != hipSuccess ||
+                vcja::launch_token_tiles(bf(dout), w.dot, B, H, N, D, s) != hipSuccess))
+    return VC_ERR_HIP;
+  if (vcja::launch_token_tiles(bf(k), w.kt, B, H, N, D, s) != hipSuccess) return VC_ERR_HIP;
   return VC_OK;
 }
 
-}  // extern "C"
-
-namespace {
-
 vc_status dkdv_impl(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v, const void* dout,
                     const int32_t* text_len, const uint8_t* key_mask, void* dk, void* dv, void* workspace,
-                    size_t workspace_bytes, void* stream, bool spatial) {
+                    size_t workspace_bytes, void* stream, bool spatial, bool fused = false,
+                    bool staged = false) {
   int64_t n = 0;
   vc_status st = check_desc(desc, &n);
   if (st != VC_OK) return st;
@@ -347,8 +377,11 @@ vc_status dkdv_impl(const vc_jointattn_desc* desc, const void* q, const void* k,
       VC_OK)
     return st;
   if ((st = check_device()) != VC_OK) return st;
+  // The separate stages 2 and 3 read the token-major copies, which stage 1 makes only for
+  // the deterministic backward.
+  if (staged && !desc->deterministic) return VC_ERR_UNSUPPORTED;
   const BwdWorkspace w = split_bwd_ws(desc, n, workspace);
-  vcja::DkdvArgs a;
+  vcja::DkdvArgs a{};
   const TextSplit ts = spatial ? text_split(desc, n) : TextSplit{0, 1, 0};
   a.text_part = reinterpret_cast<float*>(static_cast<char*>(workspace) + bwd_ws_bytes(desc, n));
   a.text_blocks = ts.blocks;
@@ -371,6 +404,10 @@ vc_status dkdv_impl(const vc_jointattn_desc* desc, const void* q, const void* k,
   a.key_mask = key_mask;
   a.dk = static_cast<__bf16*>(dk);
   a.dv = static_cast<__bf16*>(dv);
+  // Fused dQ: the fp32 accumulator takes the place of the transposed Q and dO tiles, which
+  // the fused backward does not make (2 tile sets >= 4 bytes per element of dq).
+  a.dq_acc = fused ? reinterpret_cast<float*>(w.qt) : nullptr;
+  a.dq_blocks = fused ? fused_dq_blocks(n) : 0;
   a.B = desc->batch;
   a.H = desc->heads;
   a.N = (int)n;
@@ -384,7 +421,7 @@ vc_status dkdv_impl(const vc_jointattn_desc* desc, const void* q, const void* k,
 
 vc_status dq_impl(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v, const void* dout,
                   const int32_t* text_len, const uint8_t* key_mask, void* dq, void* workspace,
-                  size_t workspace_bytes, void* stream, bool spatial) {
+                  size_t workspace_bytes, void* stream, bool spatial, bool fused = false) {
   int64_t n = 0;
   vc_status st = check_desc(desc, &n);
   if (st != VC_OK) return st;
@@ -394,7 +431,13 @@ vc_status dq_impl(const vc_jointattn_desc* desc, const void* q, const void* k, c
   if ((st = check_ws(workspace, workspace_bytes, bwd_ws_bytes(desc, n))) != VC_OK) return st;
   if ((st = check_device()) != VC_OK) return st;
   const BwdWorkspace w = split_bwd_ws(desc, n, workspace);
-  vcja::DqArgs a;
+  vcja::DqArgs a{};
+  // Completing a fused backward: the key tiles of the blocks that did not add their dQ
+  // share, plus the accumulator the others filled.
+  if (fused) {
+    a.kt_min = fused_dq_blocks(n) * (vcja::kDkdvKeys / vcja::kTileTok);
+    a.dq_acc = reinterpret_cast<const float*>(w.qt);
+  }
   a.q = bf(q);
   a.k = bf(k);
   a.v = bf(v);
@@ -433,8 +476,16 @@ vc_status bwd_impl(const vc_jointattn_desc* desc, const void* q, const void* k, 
   if (st != VC_OK) return st;
   if (!q || !k || !v || !o || !lse || !dout || !dq || !dk || !dv) return VC_ERR_NULL;
   if (spatial && (st = check_ws(workspace, workspace_bytes, spatial_bwd_ws_bytes(desc, n))) != VC_OK) return st;
-  if ((st = vc_jointattn_bwd_prepare(desc, q, k, o, lse, dout, workspace, workspace_bytes, stream)) != VC_OK)
-    return st;
+  // Joint attention: dQ fused into the key-stationary kernel (atomics), unless the caller
+  // asks for bitwise reproducible results.
+  if (!spatial && !desc->deterministic) {
+    if ((st = prepare_impl(desc, q, k, o, lse, dout, workspace, workspace_bytes, stream, false)) != VC_OK ||
+        (st = vc_jointattn_bwd_fused(desc, q, k, v, dout, text_len, key_mask, dk, dv, workspace, workspace_bytes,
+                                     stream)) != VC_OK)
+      return st;
+    return dq_impl(desc, q, k, v, dout, text_len, key_mask, dq, workspace, workspace_bytes, stream, false, true);
+  }
+  if ((st = prepare_impl(desc, q, k, o, lse, dout, workspace, workspace_bytes, stream, true)) != VC_OK) return st;
   if ((st = dkdv_impl(desc, q, k, v, dout, text_len, key_mask, dk, dv, workspace, workspace_bytes, stream,
                       spatial)) != VC_OK)
     return st;
@@ -448,13 +499,21 @@ extern "C" {
 vc_status vc_jointattn_bwd_dkdv(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
                                 const void* dout, const int32_t* text_len, const uint8_t* key_mask, void* dk,
                                 void* dv, void* workspace, size_t workspace_bytes, void* stream) {
-  return dkdv_impl(desc, q, k, v, dout, text_len, key_mask, dk, dv, workspace, workspace_bytes, stream, false);
+  return dkdv_impl(desc, q, k, v, dout, text_len, key_mask, dk, dv, workspace, workspace_bytes, stream, false,
+                   false, true);
 }
 
 vc_status vc_jointattn_bwd_dq(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
                               const void* dout, const int32_t* text_len, const uint8_t* key_mask, void* dq,
                               void* workspace, size_t workspace_bytes, void* stream) {
-  return dq_impl(desc, q, k, v, dout, text_len, key_mask, dq, workspace, workspace_bytes, stream, false);
+  return dq_impl(desc, q, k, v, dout, text_len, key_mask, dq, workspace, workspace_bytes, stream, false,
+                 desc && !desc->deterministic);
+}
+
+vc_status vc_jointattn_bwd_fused(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
+                                 const void* dout, const int32_t* text_len, const uint8_t* key_mask, void* dk,
+                                 void* dv, void* workspace, size_t workspace_bytes, void* stream) {
+  return dkdv_impl(desc, q, k, v, dout, text_len, key_mask, dk, dv, workspace, workspace_bytes, stream, false, true);
 }
 
 vc_status vc_jointattn_bwd(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v, const void* o,

@@ -1,27 +1,43 @@
-// Backward joint text-video attention for gfx950, without atomics.
+// Backward joint text-video attention for gfx950.
 //
 // Prepare: per query row, -D_i = -<dO_i, O_i> and LSE_i*log2(e) in fp32, padded
 //   to whole tiles of 64 rows (padding rows get LSE = +inf so that their
-//   probabilities vanish, and D = 0); transposed token tiles of Q, dO and K
-//   come from the reformatting pass. D is stored negated so that dP - D is
+//   probabilities vanish, and D = 0). D is stored negated so that dP - D is
 //   what the dP accumulator holds when it starts from -D.
 // dK/dV (key-stationary): one workgroup of eight waves owns 256 keys of one
 //   (sample, head), each wave 32, with K and V of its keys in registers and
 //   dK^T, dV^T accumulated in registers. It walks over all query tiles of 64,
-//   whose row-major Q and dO tiles, transposed Q^T and dO^T tiles, LSE and D
-//   are copied asynchronously global -> LDS into a two-stage ring one tile
-//   ahead; one barrier per tile. Per tile it recomputes S = Q K^T and
-//   P = exp2(S c log2(e) - LSE log2(e)), forms dP - D = -D + dO V^T and
-//   dS = P o (dP - D) with the matrix cores, and accumulates dV^T += dO^T P and
-//   dK^T += Q^T dS straight from the accumulator layout (lane column = key).
-// dQ (query-stationary): one workgroup of eight waves owns 256 queries, each
-//   wave 32, with Q^T and dO^T of its queries in registers and the lane's
+//   whose row-major Q and dO tiles, LSE and D are copied asynchronously
+//   global -> LDS into a two-stage ring one tile ahead; one barrier per tile. Per
+//   tile it recomputes S = Q K^T and P = exp2(S c log2(e) - LSE log2(e)), forms
+//   dP - D = -D + dO V^T and dS = P o (dP - D) with the matrix cores, and
+//   accumulates dV^T += dO^T P and dK^T += Q^T dS straight from the accumulator
+//   layout (lane column = key). The transposed operands Q^T, dO^T come either
+//   from transposed token tiles made by a reformatting pass (separate dQ pass)
+//   or, with dQ fused in, from the row-major tiles through transposing LDS reads.
+// dQ, fused (the default for joint attention): in the workgroups of the first
+//   key blocks (a fraction set by the host), after the dK/dV products of a tile,
+//   the waves exchange dS^T through LDS (the first 32 queries in a region of its
+//   own, the others over the tile's Q|dO region, dead by then) and each wave
+//   computes one 32x32 block of the tile's dQ / scale = dS K over the
+//   workgroup's 256 keys, with K^T held in LDS for the workgroup's lifetime. The block is added to an fp32 accumulator with
+//   atomics one tile later (so that the wait for the next tile's copies does not
+//   also wait for them), and the workgroups of each XCD start their walk at a
+//   different query tile so that concurrent atomics spread over the accumulator.
+//   For those keys S and dP are computed once per (query, key) pair; the atomic
+//   traffic (fp32 dQ rows per key block) is what limits the fraction: the dQ pass
+//   below then covers only the other key blocks' tiles and adds the accumulator.
+//   The order of the atomic additions, and so the rounding of dQ, varies from run
+//   to run.
+// dQ, separate (deterministic): one workgroup of eight waves owns 256 queries,
+//   each wave 32, with Q^T and dO^T of its queries in registers and the lane's
 //   LSE and -D as scalars. It walks over the key tiles like the forward,
 //   computing S^T = K Q^T and dP^T = V dO^T, dS^T, and dQ^T += K^T dS^T with
 //   dS^T taken straight from the accumulator layout (lane column = query).
-// Splitting the gradient this way recomputes S and dP once more instead of
-// scattering dQ partial sums with atomics; the result is bitwise reproducible.
+//   This recomputes S and dP once more instead of scattering dQ partial sums
+//   with atomics; the result is bitwise reproducible.
 #include <algorithm>
+#include <type_traits>
 
 #include "common.hpp"
 
@@ -76,15 +92,40 @@ __global__ __launch_bounds__(256) void bwd_prepare_kernel(const __bf16* __restri
   }
 }
 
-template <int D, bool SPATIAL>
+// LDS layout of the dK/dV kernel. A stage holds one query tile: Q | dO (row-major) |
+// Q^T | dO^T (transposed tiles; not with dQ fused) | LSE*log2e[64] | -D[64]. With dQ
+// fused, K^T of the workgroup's keys ([D][256 + 8] bf16) follows the two stages, then
+// dS^T of the tile's first 32 queries ([256 keys][32] bf16); dS^T of the other 32 is
+// written over the current stage's Q | dO region once every wave is done with it.
+// dS^T rows are 72 bytes (32 queries + 4 pad): the writes (one key per lane) hit 64
+// distinct banks, and every address is a per-lane base plus an immediate offset.
+template <int D, bool FUSED>
+struct DkdvLds {
+  static constexpr int RT = RowTile<D>::kBytes;
+  static constexpr int TT = FUSED ? 0 : (int)tile_elems(D) * 2;
+  static constexpr int STAGE = 2 * RT + 2 * TT + 512;
+  static constexpr int KTS = (kBKV + 8) * 2;  // K^T row stride (bytes)
+  static constexpr int DSS = (32 + 4) * 2;    // dS^T row stride (bytes)
+  static constexpr int DSB = kBKV * DSS;      // dS^T of 32 queries
+  static_assert(DSB <= 2 * RT, "dS^T must fit in a stage's Q | dO region");
+  static constexpr int KT_OFF = 2 * STAGE;
+  static constexpr int DS_OFF = KT_OFF + D * KTS;  // dS^T of the first 32 queries
+  static constexpr int BYTES = FUSED ? DS_OFF + DSB : 2 * STAGE;
+  // Byte offset of the 8-byte unit u (queries 4u .. 4u+3) of dS^T row j.
+  static __device__ __forceinline__ int ds_at(int j, int u) { return j * DSS + 8 * u; }
+};
+
+template <int D, bool SPATIAL, bool FUSED>
 __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a) {
-  constexpr int RT = RowTile<D>::kBytes;      // row-major Q or dO tile bytes
+  static_assert(!(SPATIAL && FUSED), "dQ is fused for joint attention only");
+  using Lds = DkdvLds<D, FUSED>;
+  constexpr int RT = Lds::RT;                 // row-major Q or dO tile bytes
   constexpr int RS = RowTile<D>::kStride;     // their row stride
-  constexpr int TT = (int)tile_elems(D) * 2;  // transposed tile bytes
-  constexpr int STAGE = 2 * RT + 2 * TT + 512;  // Q | dO | Q^T | dO^T | LSE*log2e[64] | D[64]
+  constexpr int TT = Lds::TT;                 // transposed tile bytes
+  constexpr int STAGE = Lds::STAGE;
   constexpr int RCOPIES = RowTile<D>::kCopies;
   constexpr int TCOPIES = TT / 1024;
-  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+  __shared__ __attribute__((aligned(1024))) char smem[Lds::BYTES];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -125,6 +166,7 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
   }
   // This workgroup's keys (spatial branch: text keys, or keys of one frame).
   const RowBlock rb = row_block(kb, N, a.T, SPATIAL ? a.frame_len : 0, kBKV, true);
+  const bool do_dq = FUSED && kb < a.dq_blocks;  // this key block carries its share of dQ
   const int key = rb.r0 + w * 32 + l32;  // this lane's key (accumulator column)
   const bool key_in = key < rb.r1;
   // Partial dK of this lane's key in its chunk (dV partials follow all dK partials); formed
@@ -178,17 +220,19 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
   auto issue = [&](int qt, int st) {
     VC_LDS char* sq = (VC_LDS char*)smem + st * STAGE;
     for (int idx = w; idx < RCOPIES; idx += kDkdvWaves) {
-      copy_row_tile<D>(a.q + base, tok, qt * kBQ, N, sq, idx, lane);
-      copy_row_tile<D>(a.dout + base, tok, qt * kBQ, N, sq + RT, idx, lane);
+      copy_row_tile<D, true, FUSED>(a.q + base, tok, qt * kBQ, N, sq, idx, lane);  // fused: perm_row order
+      copy_row_tile<D, true, FUSED>(a.dout + base, tok, qt * kBQ, N, sq + RT, idx, lane);
     }
-    const size_t toff = (bh * a.ntile + qt) * tile_elems(D);
-    for (int idx = w; idx < TCOPIES; idx += kDkdvWaves) {
-      copy16_to_lds(a.qt + toff + idx * 512 + lane * 8, sq + 2 * RT + idx * 1024);
-      copy16_to_lds(a.dot + toff + idx * 512 + lane * 8, sq + 2 * RT + TT + idx * 1024);
+    if constexpr (!FUSED) {
+      const size_t toff = (bh * a.ntile + qt) * tile_elems(D);
+      for (int idx = w; idx < TCOPIES; idx += kDkdvWaves) {
+        copy16_to_lds_opaque(a.qt + toff + idx * 512 + lane * 8, sq + 2 * RT + idx * 1024);
+        copy16_to_lds_opaque(a.dot + toff + idx * 512 + lane * 8, sq + 2 * RT + TT + idx * 1024);
+      }
     }
     if (w == kDkdvWaves - 1 && lane < 32) {
       const float* src = (lane < 16 ? a.lse2 : a.dd) + bh * npad + qt * kBQ + 4 * (lane & 15);
-      copy16_to_lds(src, sq + 2 * RT + 2 * TT);
+      copy16_to_lds_opaque(src, sq + 2 * RT + 2 * TT);
     }
   };
 
@@ -201,6 +245,16 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
       kf[ks] = *(const bf16x8*)(a.k + kr + 16 * ks);
       vf[ks] = *(const bf16x8*)(a.v + kr + 16 * ks);
     }
+  }
+
+  // Fused dQ: K^T of the workgroup's keys (row d holds K[key][d] of its 256 keys).
+  if (FUSED && do_dq) {
+    VC_LDS __bf16* ktl = (VC_LDS __bf16*)(smem + Lds::KT_OFF);
+    const int kl = w * 32 + l32;
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks)
+#pragma unroll
+      for (int t = 0; t < 8; ++t) ktl[(16 * ks + 8 * hi + t) * (Lds::KTS / 2) + kl] = kf[ks][t];
   }
 
   f32x16 dk_acc[D / 32], dv_acc[D / 32];
@@ -234,94 +288,214 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
   const bool wave_one_frame = SPATIAL && kw0 >= a.T && kw1 < N && rule.frame_start(kw1) == wks;
   const int2 kr = key_range(rule, key);  // spatial: queries attending to this lane's key
 
-  int qt = next_q(0);
-  if (qt < a.ntile) issue(qt, 0);
-  for (int pos = 0; qt < a.ntile; ++pos) {
-    const int qn = next_q(qt + 1);
-    wait_all_memory();
-    __syncthreads();  // stage pos&1 holds tile qt; every wave is done with the other stage
-    if (qn < a.ntile) issue(qn, (pos + 1) & 1);
-    const int q0 = qt * kBQ;
-    const bool pair_mask = SPATIAL && !((wave_text_keys && q0 >= a.T) ||
-                                        (wave_one_frame && q0 >= wks && q0 + kBQ <= wks + rule.L));
-    const VC_LDS char* q_lds = (const VC_LDS char*)smem + (pos & 1) * STAGE;
-    const VC_LDS char* do_lds = q_lds + RT;
-    const VC_LDS char* qt_lds = q_lds + 2 * RT;
-    const VC_LDS char* dot_lds = qt_lds + TT;
-    const VC_LDS float* lse_lds = (const VC_LDS float*)(qt_lds + 2 * TT);
-    const VC_LDS float* dd_lds = lse_lds + kBQ;
-
-#pragma unroll 1
-    for (int qb = 0; qb < kBQ / 32; ++qb) {
-      f32x16 s = zero_f32x16(), dp;
+  // Fused dQ: the workgroups of each XCD (dispatch is round-robin over the XCDs) start
+  // their walk over the query tiles at a different eighth of them, so that the atomics
+  // of concurrent workgroups land on different rows of the accumulator. Walk position u
+  // visits tile phys(u).
+  const int xs = (FUSED && !tail) ? (int)((blockIdx.x % kXcds) * ((a.ntile + kXcds - 1) / kXcds)) % a.ntile : 0;
+  auto phys = [&](int u) { return u + xs >= a.ntile ? u + xs - a.ntile : u + xs; };
+  // Fused dQ: this wave's 32x32 block of the tile's dQ (query block dq_qb, dim block dq_db)
+  // over key steps [dq_s0, dq_s0 + DQ_STEPS) of 16 keys; when the dim blocks are fewer
+  // than the waves, several waves share a block, each over part of the keys.
+  constexpr int DQ_BLOCKS = 2 * (D / 32);
+  constexpr int DQ_STEPS = kBKV / 16 / (kDkdvWaves / DQ_BLOCKS);
+  static_assert(kDkdvWaves % DQ_BLOCKS == 0, "dQ blocks per wave");
+  const int dq_qb = (w % DQ_BLOCKS) & 1, dq_db = (w % DQ_BLOCKS) >> 1, dq_s0 = (w / DQ_BLOCKS) * DQ_STEPS;
+  f32x16 dq_blk;
+  int dq_row0 = -1;  // first query row of the block awaiting its atomics, -1: none
+  // The lane index as a value the compiler must treat as new at each use: per-lane
+  // addresses of the fused steps derived from it are formed where they are used instead
+  // of being kept in registers across the whole loop (registers are the limit here).
+  auto fresh_lane = [&]() {
+    int x = lane;
+    asm volatile("" : "+v"(x));
+    return x;
+  };
+  // Adds the pending dQ block to the accumulator (rows past N are padding): a uniform base
+  // plus a 32-bit per-lane offset.
+  float* const dq_dst = FUSED ? a.dq_acc + (size_t)b * N * tok + (size_t)h * D + dq_db * 32 : nullptr;
+  auto flush_dq = [&]() {
+    if (dq_row0 < 0) return;
+    const int ln = fresh_lane();
+    const int col = ln & 31, half = ln >> 5;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {  // dP accumulates on top of -D of its query rows
-        const f32x4 nd = *(const VC_LDS f32x4*)(dd_lds + qb * 32 + 8 * j + 4 * hi);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) dp[4 * j + i] = nd[i];
-      }
-#pragma unroll
-      for (int ks = 0; ks < D / 16; ++ks) {
-        const bf16x8 qa = *(const VC_LDS bf16x8*)(q_lds + (qb * 32 + l32) * RS + (2 * ks + hi) * 16);
-        s = mfma32(qa, kf[ks], s);
-      }
-#pragma unroll
-      for (int ks = 0; ks < D / 16; ++ks) {
-        const bf16x8 da = *(const VC_LDS bf16x8*)(do_lds + (qb * 32 + l32) * RS + (2 * ks + hi) * 16);
-        dp = mfma32(da, vf[ks], dp);
-      }
-      // Register r holds query row qb*32 + 8*(r/4) + 4*hi + r%4: four runs of 4 rows.
-      // Spatial branch: on tiles needing the per-pair test, queries outside [kr.x, kr.y)
-      // (this lane's key range) get probability zero.
-      const int row0 = pair_mask ? q0 + qb * 32 : kr.x;
-      float p[16], ds[16];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const f32x4 l2 = *(const VC_LDS f32x4*)(lse_lds + qb * 32 + 8 * j + 4 * hi);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int r = 4 * j + i;
-          p[r] = fast_exp2(fmaf(s[r], a.scale_log2, -l2[i]));
-          if (SPATIAL) {
-            const int qrow = row0 + acc_row(r, hi);
-            p[r] = (valid & (!pair_mask | ((qrow >= kr.x) & (qrow < kr.y)))) ? p[r] : 0.0f;
-          }
-          // Joint attention needs no test here: the probabilities of an invalid key reach
-          // only its own lane's dK, dV, which are written as zero at the end.
-          ds[r] = p[r] * dp[r];
-        }
-      }
-      // Operand element t of k-step st2 is query 16*st2 + 8*(t/4) + 4*hi + t%4, stored by
-      // the transposed tiles as 8 consecutive elements at position 16*st2 + 8*hi.
-      // Operands of the 2 * D/32 products in order (k-step st2 major, dim block db minor),
-      // each read one product ahead: the read is in flight while the previous pair runs.
-      constexpr int NB = D / 32;
-      const int obase = (l32 * kTileRow + qb * 32 + 8 * hi) * 2;
-      auto opnd = [&](int idx, const VC_LDS char* bp) {
-        return *(const VC_LDS bf16x8*)(bp + obase + ((idx % NB) * 32 * kTileRow + 16 * (idx / NB)) * 2);
-      };
-      bf16x8 av = opnd(0, dot_lds), ak = opnd(0, qt_lds);
-#pragma unroll
-      for (int st2 = 0; st2 < 2; ++st2) {
-        const bf16x8 pb = to_bf16x8(&p[8 * st2]);
-        const bf16x8 sb = to_bf16x8(&ds[8 * st2]);
-#pragma unroll
-        for (int db = 0; db < NB; ++db) {
-          const int nx = st2 * NB + db + 1;
-          bf16x8 vn = av, kn = ak;
-          if (nx < 2 * NB) {
-            vn = opnd(nx, dot_lds);
-            kn = opnd(nx, qt_lds);
-          }
-          dv_acc[db] = mfma32(av, pb, dv_acc[db]);
-          dk_acc[db] = mfma32(ak, sb, dk_acc[db]);
-          av = vn;
-          ak = kn;
-        }
-      }
+    for (int r = 0; r < 16; ++r) {
+      const int qrow = dq_row0 + acc_row(r, half);
+      if (qrow < N) atomicAdd(dq_dst + (unsigned)(qrow * (int)tok + col), dq_blk[r]);
     }
-    qt = qn;
-  }
+    dq_row0 = -1;
+  };
+  // Transposing reads of the A operands Q^T, dO^T from the row-major tiles (fused: rows in
+  // perm_row order): lane l of 16-lane group G supplies query 4*hi + (l%16)/4, i.e. row
+  // 4*((l%16)/4) + hi, and column 16*(G%2) + 4*(l%4), relative to the operand's first query
+  // row and dim block; the operand's other four queries (+8) lie 2 rows further.
+  const int tr_base = (4 * ((lane & 15) >> 2) + hi) * RS + (16 * ((lane >> 4) & 1) + 4 * (lane & 3)) * 2;
+  // Row of this lane's query in the plain operand reads (fused: perm_row order).
+  const int prow = FUSED ? perm_row(l32) : l32;
+  VC_LDS char* ds_own = (VC_LDS char*)smem + Lds::DS_OFF;
+
+  // The walk over the query tiles; DQ: this workgroup also adds its dQ share (a separate
+  // instance of the loop, so that neither carries the other's registers).
+  auto walk = [&](auto dq_tag) {
+    constexpr bool DQ = FUSED && decltype(dq_tag)::value;
+    int qt = next_q(0);
+    if (qt < a.ntile) issue(phys(qt), 0);
+    for (int st = 0; qt < a.ntile; st ^= 1) {  // stage st holds tile qt, stage st ^ 1 the next
+      const int qn = next_q(qt + 1);
+      wait_all_memory();
+      __syncthreads();  // stage st holds tile qt; every wave is done with the other stage
+      if constexpr (DQ) {
+        flush_dq();     // the previous tile's dQ block; waited for at the next tile
+        sched_fence();  // its registers are free before the copies and products begin
+      }
+      if (qn < a.ntile) issue(phys(qn), st ^ 1);
+      const int q0 = phys(qt) * kBQ;
+      const bool pair_mask = SPATIAL && !((wave_text_keys && q0 >= a.T) ||
+                                          (wave_one_frame && q0 >= wks && q0 + kBQ <= wks + rule.L));
+      VC_LDS char* stage = (VC_LDS char*)smem + st * STAGE;
+      const VC_LDS char* q_lds = stage;
+      const VC_LDS char* do_lds = q_lds + RT;
+      const VC_LDS char* qt_lds = q_lds + 2 * RT;
+      const VC_LDS char* dot_lds = qt_lds + TT;
+      const VC_LDS float* lse_lds = (const VC_LDS float*)(qt_lds + 2 * TT);
+      const VC_LDS float* dd_lds = lse_lds + kBQ;
+      bf16x8 ds_keep[2];  // fused: dS of the second query block as bf16 operands, for dQ
+
+      auto query_block = [&](int qb) {
+        f32x16 s = zero_f32x16(), dp;
+  #pragma unroll
+        for (int j = 0; j < 4; ++j) {  // dP accumulates on top of -D of its query rows
+          const f32x4 nd = *(const VC_LDS f32x4*)(dd_lds + qb * 32 + 8 * j + 4 * hi);
+  #pragma unroll
+          for (int i = 0; i < 4; ++i) dp[4 * j + i] = nd[i];
+        }
+  #pragma unroll
+        for (int ks = 0; ks < D / 16; ++ks) {
+          const bf16x8 qa = *(const VC_LDS bf16x8*)(q_lds + (qb * 32 + prow) * RS + (2 * ks + hi) * 16);
+          s = mfma32(qa, kf[ks], s);
+        }
+  #pragma unroll
+        for (int ks = 0; ks < D / 16; ++ks) {
+          const bf16x8 da = *(const VC_LDS bf16x8*)(do_lds + (qb * 32 + prow) * RS + (2 * ks + hi) * 16);
+          dp = mfma32(da, vf[ks], dp);
+        }
+        // Register r holds query row qb*32 + 8*(r/4) + 4*hi + r%4: four runs of 4 rows.
+        // Spatial branch: on tiles needing the per-pair test, queries outside [kr.x, kr.y)
+        // (this lane's key range) get probability zero.
+        const int row0 = pair_mask ? q0 + qb * 32 : kr.x;
+        float p[16], ds[16];
+  #pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const f32x4 l2 = *(const VC_LDS f32x4*)(lse_lds + qb * 32 + 8 * j + 4 * hi);
+  #pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int r = 4 * j + i;
+            p[r] = fast_exp2(fmaf(s[r], a.scale_log2, -l2[i]));
+            if (SPATIAL) {
+              const int qrow = row0 + acc_row(r, hi);
+              p[r] = (valid & (!pair_mask | ((qrow >= kr.x) & (qrow < kr.y)))) ? p[r] : 0.0f;
+            }
+            // Joint attention needs no test for dK, dV: the probabilities of an invalid key
+            // reach only its own lane's dK, dV, which are written as zero at the end. Its dS
+            // also reaches dQ, so with dQ fused it is zeroed (its P may even be inf).
+            ds[r] = p[r] * dp[r];
+            if (DQ) ds[r] = valid ? ds[r] : 0.0f;
+          }
+        }
+        // Operand element t of k-step st2 is query 16*st2 + 8*(t/4) + 4*hi + t%4: stored by
+        // the transposed tiles as 8 consecutive elements at position 16*st2 + 8*hi, or read
+        // from the row-major tiles by two transposing reads (rows +0..3 and +8..11).
+        // Operands of the 2 * D/32 products in order (k-step st2 major, dim block db minor),
+        // each read one product ahead: the read is in flight while the previous pair runs.
+        constexpr int NB = D / 32;
+        const int obase = (l32 * kTileRow + qb * 32 + 8 * hi) * 2;
+        auto opnd = [&](int idx, const VC_LDS char* bp) {
+          if constexpr (FUSED) {
+            const VC_LDS char* p0 = bp + tr_base + (qb * 32 + 16 * (idx / NB)) * RS + (idx % NB) * 64;
+            return cat4(lds_read_tr(p0), lds_read_tr(p0 + 2 * RS));
+          } else {
+            return *(const VC_LDS bf16x8*)(bp + obase + ((idx % NB) * 32 * kTileRow + 16 * (idx / NB)) * 2);
+          }
+        };
+        if constexpr (DQ) {
+          // dS^T of this query block: element t of operand st2 is query 16*st2 + 8*(t/4) +
+          // 4*hi + t%4, i.e. units 4*st2 + hi and 4*st2 + 2 + hi. Block 0 goes to its own
+          // region now; block 1 waits until the stage's Q and dO are no longer read.
+          if (qb == 0) {
+            const int ln = fresh_lane();
+            const int kl = w * 32 + (ln & 31), hl = ln >> 5;  // dS^T row, lane half
+  #pragma unroll
+            for (int st2 = 0; st2 < 2; ++st2) {
+              const bf16x8 x = to_bf16x8(&ds[8 * st2]);
+              *(VC_LDS bf16x4*)(ds_own + Lds::ds_at(kl, 4 * st2 + hl)) = bf16x4{x[0], x[1], x[2], x[3]};
+              *(VC_LDS bf16x4*)(ds_own + Lds::ds_at(kl, 4 * st2 + 2 + hl)) = bf16x4{x[4], x[5], x[6], x[7]};
+            }
+          }
+        }
+        const VC_LDS char* v_src = FUSED ? do_lds : dot_lds;
+        const VC_LDS char* k_src = FUSED ? q_lds : qt_lds;
+        bf16x8 av = opnd(0, v_src), ak = opnd(0, k_src);
+  #pragma unroll
+        for (int st2 = 0; st2 < 2; ++st2) {
+          const bf16x8 pb = to_bf16x8(&p[8 * st2]);
+          const bf16x8 sb = to_bf16x8(&ds[8 * st2]);
+          if constexpr (DQ) ds_keep[st2] = sb;
+  #pragma unroll
+          for (int db = 0; db < NB; ++db) {
+            const int nx = st2 * NB + db + 1;
+            bf16x8 vn = av, kn = ak;
+            if (nx < 2 * NB) {
+              vn = opnd(nx, v_src);
+              kn = opnd(nx, k_src);
+            }
+            dv_acc[db] = mfma32(av, pb, dv_acc[db]);
+            dk_acc[db] = mfma32(ak, sb, dk_acc[db]);
+            av = vn;
+            ak = kn;
+          }
+        }
+      };
+  #pragma unroll 1
+      for (int qb = 0; qb < kBQ / 32; ++qb) query_block(qb);
+
+      if constexpr (DQ) {
+        __syncthreads();  // every wave is done reading this stage's Q and dO
+        const int ln = fresh_lane();
+        {
+          const int kl = w * 32 + (ln & 31), hl = ln >> 5;
+  #pragma unroll
+          for (int st2 = 0; st2 < 2; ++st2) {
+            const bf16x8 x = ds_keep[st2];
+            *(VC_LDS bf16x4*)(stage + Lds::ds_at(kl, 4 * st2 + hl)) = bf16x4{x[0], x[1], x[2], x[3]};
+            *(VC_LDS bf16x4*)(stage + Lds::ds_at(kl, 4 * st2 + 2 + hl)) = bf16x4{x[4], x[5], x[6], x[7]};
+          }
+        }
+        __syncthreads();  // dS^T of both query blocks complete
+        // dQ block: A = dS (queries x keys) by transposing reads of dS^T (this wave's query
+        // block's region), B = K from K^T. Lane l of 16-lane group G supplies key row
+        // 16*st + 8*hi + (l%16)/4 (+4) and unit 4*(G%2) + l%4 of that row.
+        const VC_LDS char* ds_src = dq_qb ? (const VC_LDS char*)stage : (const VC_LDS char*)ds_own;
+        const int arow = dq_s0 * 16 + 8 * (ln >> 5) + ((ln & 15) >> 2), aunit = 4 * ((ln >> 4) & 1) + (ln & 3);
+        const VC_LDS char* b_base = (const VC_LDS char*)smem + Lds::KT_OFF + (dq_db * 32 + (ln & 31)) * Lds::KTS +
+                                    (dq_s0 * 16 + 8 * (ln >> 5)) * 2;
+        dq_blk = zero_f32x16();
+  #pragma unroll
+        for (int st = 0; st < DQ_STEPS; ++st) {
+          const int j = arow + 16 * st;
+          const bf16x8 da = cat4(lds_read_tr(ds_src + Lds::ds_at(j, aunit)), lds_read_tr(ds_src + Lds::ds_at(j + 4, aunit)));
+          const bf16x8 kb8 = *(const VC_LDS bf16x8*)(b_base + st * 32);
+          dq_blk = mfma32(da, kb8, dq_blk);
+        }
+        dq_row0 = q0 + dq_qb * 32;
+      }
+      qt = qn;
+    }
+    if constexpr (DQ) flush_dq();
+  };
+  if (do_dq)
+    walk(std::true_type{});
+  else
+    walk(std::false_type{});
 
   if (tail) {
     // An invalid key's partials are zero (its accumulators may hold anything).
@@ -509,7 +683,7 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
     for (int idx = w; idx < TCOPIES; idx += kDqWaves) copy16_to_lds(tsrc + idx * 512 + lane * 8, sk + 2 * RT + idx * 1024);
   };
 
-  int kt = next_tile(kt0);
+  int kt = next_tile(max(kt0, a.kt_min));  // completing a fused backward: keys >= kt_min only
   if (kt < a.ntile) issue(kt, 0);
   int st = 0;
   while (kt < a.ntile) {
@@ -585,12 +759,15 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
       }
   } else if (qi < rb.r1) {
     __bf16* qp = a.dq + base + (size_t)qi * tok;
+    const float* fp = a.dq_acc ? a.dq_acc + base + (size_t)qi * tok : nullptr;  // the fused keys' share
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        bf16x4 t = {(__bf16)(dq_acc[db][4 * j + 0] * a.scale), (__bf16)(dq_acc[db][4 * j + 1] * a.scale),
-                    (__bf16)(dq_acc[db][4 * j + 2] * a.scale), (__bf16)(dq_acc[db][4 * j + 3] * a.scale)};
+        f32x4 x = {dq_acc[db][4 * j + 0], dq_acc[db][4 * j + 1], dq_acc[db][4 * j + 2], dq_acc[db][4 * j + 3]};
+        if (fp) x += *(const f32x4*)(fp + db * 32 + 8 * j + 4 * hi);
+        bf16x4 t = {(__bf16)(x[0] * a.scale), (__bf16)(x[1] * a.scale), (__bf16)(x[2] * a.scale),
+                    (__bf16)(x[3] * a.scale)};
         *(bf16x4*)(qp + db * 32 + 8 * j + 4 * hi) = t;
       }
   }
@@ -598,7 +775,8 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
 
 // Joint tail of the dQ kernel: dQ of the split items as the sum of their chunks' partials.
 template <int D>
-__global__ void tail_reduce_dq_kernel(const float* part, __bf16* dq, int B, int H, int N, int items, int chunks) {
+__global__ void tail_reduce_dq_kernel(const float* part, __bf16* dq, int B, int H, int N, int items, int chunks,
+                                      const float* dq_acc, float scale) {
   const int nblk = (N + kDqBM - 1) / kDqBM;
   const size_t total = (size_t)items * kDqBM * (D / 4);
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -612,7 +790,16 @@ __global__ void tail_reduce_dq_kernel(const float* part, __bf16* dq, int B, int 
   const int h = (item / nblk) % H, b = item / (nblk * H);
   f32x4 s = {0.0f, 0.0f, 0.0f, 0.0f};
   for (int c = 0; c < chunks; ++c) s += *(const f32x4*)(part + (((size_t)slot * chunks + c) * kDqBM + k) * D + d);
-  *(bf16x4*)(dq + (((size_t)b * N + row) * H + h) * D + d) = bf16x4{(__bf16)s[0], (__bf16)s[1], (__bf16)s[2], (__bf16)s[3]};
+  const size_t off = (((size_t)b * N + row) * H + h) * D + d;
+  if (dq_acc) s += scale * *(const f32x4*)(dq_acc + off);  // the fused keys' share (unscaled)
+  *(bf16x4*)(dq + off) = bf16x4{(__bf16)s[0], (__bf16)s[1], (__bf16)s[2], (__bf16)s[3]};
+}
+
+// Fused dQ: zeroes the fp32 accumulator (a kernel, not a memset, so that a captured graph
+// replays it like any other node). n4 = elements / 4.
+__global__ void zero_f32_kernel(float* x, size_t n4) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n4) ((f32x4*)x)[i] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 }
 
 }  // namespace
@@ -635,14 +822,22 @@ hipError_t launch_bwd_dkdv(const DkdvArgs& a, int head_dim, hipStream_t s) {
   // Spatial: 3-D grid renumbered by XCD. Joint: 1-D grid of items, the split tail last.
   dim3 grid = spatial ? dim3(nblk + (split ? (a.text_chunks - 1) * a.text_blocks : 0), a.H, a.B)
                       : dim3(nblk * a.H * a.B + a.tail_blocks * (a.tail_chunks - 1));
+  const bool fused = !spatial && a.dq_acc;
+  const size_t dq4 = (size_t)a.B * a.N * a.H * head_dim / 4;
+  const dim3 egrid((unsigned)((dq4 + 255) / 256));
+  if (fused) hipLaunchKernelGGL(zero_f32_kernel, egrid, dim3(256), 0, s, a.dq_acc, dq4);
   if (head_dim == 128 && spatial)
-    hipLaunchKernelGGL((bwd_dkdv_kernel<128, true>), grid, dim3(64 * kDkdvWaves), 0, s, a);
+    hipLaunchKernelGGL((bwd_dkdv_kernel<128, true, false>), grid, dim3(64 * kDkdvWaves), 0, s, a);
+  else if (head_dim == 128 && fused)
+    hipLaunchKernelGGL((bwd_dkdv_kernel<128, false, true>), grid, dim3(64 * kDkdvWaves), 0, s, a);
   else if (head_dim == 128)
-    hipLaunchKernelGGL((bwd_dkdv_kernel<128, false>), grid, dim3(64 * kDkdvWaves), 0, s, a);
+    hipLaunchKernelGGL((bwd_dkdv_kernel<128, false, false>), grid, dim3(64 * kDkdvWaves), 0, s, a);
   else if (spatial)
-    hipLaunchKernelGGL((bwd_dkdv_kernel<64, true>), grid, dim3(64 * kDkdvWaves), 0, s, a);
+    hipLaunchKernelGGL((bwd_dkdv_kernel<64, true, false>), grid, dim3(64 * kDkdvWaves), 0, s, a);
+  else if (fused)
+    hipLaunchKernelGGL((bwd_dkdv_kernel<64, false, true>), grid, dim3(64 * kDkdvWaves), 0, s, a);
   else
-    hipLaunchKernelGGL((bwd_dkdv_kernel<64, false>), grid, dim3(64 * kDkdvWaves), 0, s, a);
+    hipLaunchKernelGGL((bwd_dkdv_kernel<64, false, false>), grid, dim3(64 * kDkdvWaves), 0, s, a);
   if (!spatial && a.tail_blocks > 0) {
     const size_t threads = (size_t)a.tail_blocks * kBKV * (head_dim / 4);
     dim3 rgrid((unsigned)((threads + 255) / 256));
@@ -681,10 +876,10 @@ hipError_t launch_bwd_dq(const DqArgs& a, int head_dim, hipStream_t s) {
     dim3 rgrid((unsigned)((threads + 255) / 256));
     if (head_dim == 128)
       hipLaunchKernelGGL(tail_reduce_dq_kernel<128>, rgrid, dim3(256), 0, s, a.tail_part, a.dq, a.B, a.H, a.N,
-                         a.tail_blocks, a.tail_chunks);
+                         a.tail_blocks, a.tail_chunks, a.dq_acc, a.scale);
     else
       hipLaunchKernelGGL(tail_reduce_dq_kernel<64>, rgrid, dim3(256), 0, s, a.tail_part, a.dq, a.B, a.H, a.N,
-                         a.tail_blocks, a.tail_chunks);
+                         a.tail_blocks, a.tail_chunks, a.dq_acc, a.scale);
   }
   return hipGetLastError();
 }

@@ -65,6 +65,19 @@ __device__ __forceinline__ void copy16_to_lds(const void* g, VC_LDS void* lds_wa
   __builtin_amdgcn_global_load_lds(g, lds_wave_base, 16, 0, 0);
 }
 
+// The same copy issued through inline assembly. The compiler then does not know that the
+// instruction writes LDS, so it inserts no wait for it before later LDS reads: it would
+// otherwise wait for every copy in flight before any read whose address it cannot prove
+// distinct from the copies' (the ring's other stage, in practice). The caller waits for
+// the copies (wait_all_memory) before reading what they write. Sets M0; a kernel using it
+// must issue all of its LDS copies this way, so that nothing else relies on M0.
+__device__ __forceinline__ void copy16_to_lds_opaque(const void* g, VC_LDS void* lds_wave_base) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+               :
+               : "s"((unsigned)(size_t)lds_wave_base), "v"(g)
+               : "memory");
+}
+
 // Waits for every outstanding memory operation of this wave (vector memory and LDS).
 __device__ __forceinline__ void wait_all_memory() { __builtin_amdgcn_s_waitcnt(0); }
 
@@ -89,17 +102,28 @@ struct RowTile {
   static_assert(kTileTok * kChunks % 64 == 0, "tile must be whole wave copies");
 };
 
+// Row order of a permuted row tile: token 16g + 4m + i of the tile sits in LDS row
+// 16g + 4i + m (a 4x4 transpose inside each run of 16; its own inverse). Four consecutive
+// tokens then lie 4 rows apart, so that a transposing read of them (4 rows x 64 bytes per
+// half-wave) hits 64 distinct banks, while 16 consecutive tokens still occupy 16 distinct
+// rows of the run for the plain 16-byte reads.
+__host__ __device__ constexpr int perm_row(int t) { return (t & ~15) | ((t & 3) << 2) | ((t >> 2) & 3); }
+
 // Issues wave copy `idx` of a row tile: rows row0 .. row0+63 of the [B, N, H, D] tensor
 // slice at src (row r at src + r*tok), rows clamped to N-1. The pad chunk of each row
-// repeats the row's last chunk.
-template <int D>
+// repeats the row's last chunk. PERM: the tile's rows in perm_row order.
+template <int D, bool OPAQUE = false, bool PERM = false>
 __device__ __forceinline__ void copy_row_tile(const __bf16* src, size_t tok, int row0, int N, VC_LDS char* dst,
                                               int idx, int lane) {
   constexpr int CH = RowTile<D>::kChunks;
   const int lin = idx * 64 + lane;
   const int r = lin / CH;
   const int c = min(lin - r * CH, CH - 2);
-  copy16_to_lds(src + (size_t)min(row0 + r, N - 1) * tok + c * 8, dst + idx * 1024);
+  const __bf16* g = src + (size_t)min(row0 + (PERM ? perm_row(r) : r), N - 1) * tok + c * 8;
+  if constexpr (OPAQUE)
+    copy16_to_lds_opaque(g, dst + idx * 1024);
+  else
+    copy16_to_lds(g, dst + idx * 1024);
 }
 
 // Scheduling hint for the basic block it ends: issue `lead` LDS reads, then `n` times
@@ -315,6 +339,13 @@ struct DkdvArgs {
   // writing fp32 partial dK, dV (scaled) to tail_part, [2][tail_blocks][tail_chunks][256][D].
   float* tail_part;
   int tail_blocks, tail_chunks, tail_span;
+  // Joint attention with dQ fused in (dq_acc non-NULL): the workgroups of key blocks
+  // [0, dq_blocks) also add their keys' share of dQ / scale, dS K, into the fp32
+  // accumulator dq_acc ([B, N, H, D], zeroed by the launch) with atomics; the dQ pass adds
+  // the share of the other keys. qt and dot are not read (transposed operands come from the
+  // row-major tiles).
+  float* dq_acc;
+  int dq_blocks;
 };
 
 constexpr int kDkdvKeys = 256;  // keys per dK/dV workgroup
@@ -339,6 +370,11 @@ struct DqArgs {
   // partial dQ (scaled) in tail_part, [tail_blocks][tail_chunks][256][D].
   float* tail_part;
   int tail_blocks, tail_chunks, tail_span;
+  // Completing a fused backward: only key tiles >= kt_min are visited, and dq_acc (fp32
+  // [B, N, H, D], the other keys' dQ / scale) is added before scaling. kt_min = 0 and
+  // dq_acc = NULL for the whole dQ.
+  int kt_min;
+  const float* dq_acc;
 };
 
 // Temporal branch: attention of each spatial position across the F frames. Video token

@@ -32,7 +32,7 @@ def test_exports_every_declared_function(lib):
 
 
 def test_version_and_strings(lib):
-    assert vc.vc_jointattn_abi_version() == 5
+    assert vc.vc_jointattn_abi_version() == 6
     for code in vc.STATUS:
         assert isinstance(vc.vc_status_string(code), str) and vc.vc_status_string(code)
     assert vc.vc_status_string(12345) == "unknown status"
