@@ -97,8 +97,10 @@ __global__ __launch_bounds__(256) void bwd_prepare_kernel(const __bf16* __restri
 // fused, K^T of the workgroup's keys ([D][256 + 8] bf16) follows the two stages, then
 // dS^T of the tile's first 32 queries ([256 keys][32] bf16); dS^T of the other 32 is
 // written over the current stage's Q | dO region once every wave is done with it.
-// dS^T rows are 72 bytes (32 queries + 4 pad): the writes (one key per lane) hit 64
-// distinct banks, and every address is a per-lane base plus an immediate offset.
+// dS^T rows are 72 bytes (32 queries + 4 pad), and key 32u + 4j + e sits in row
+// 32u + 8e + j: the writes (32 consecutive keys, one per lane) hit 64 distinct banks, the
+// transposing reads (4 consecutive keys x 32 queries per half-wave) too, as the 4 keys'
+// rows lie 8 apart; every address is a per-lane base plus an immediate offset.
 template <int D, bool FUSED>
 struct DkdvLds {
   static constexpr int RT = RowTile<D>::kBytes;
@@ -111,8 +113,9 @@ struct DkdvLds {
   static constexpr int KT_OFF = 2 * STAGE;
   static constexpr int DS_OFF = KT_OFF + D * KTS;  // dS^T of the first 32 queries
   static constexpr int BYTES = FUSED ? DS_OFF + DSB : 2 * STAGE;
-  // Byte offset of the 8-byte unit u (queries 4u .. 4u+3) of dS^T row j.
+  // Byte offset of the 8-byte unit u (queries 4u .. 4u+3) of dS^T row j; row of key k.
   static __device__ __forceinline__ int ds_at(int j, int u) { return j * DSS + 8 * u; }
+  static __device__ __forceinline__ int ds_row(int k) { return (k & ~31) | ((k & 3) << 3) | ((k >> 2) & 7); }
 };
 
 template <int D, bool SPATIAL, bool FUSED>
@@ -423,7 +426,7 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
           // region now; block 1 waits until the stage's Q and dO are no longer read.
           if (qb == 0) {
             const int ln = fresh_lane();
-            const int kl = w * 32 + (ln & 31), hl = ln >> 5;  // dS^T row, lane half
+            const int kl = Lds::ds_row(w * 32 + (ln & 31)), hl = ln >> 5;  // dS^T row, lane half
   #pragma unroll
             for (int st2 = 0; st2 < 2; ++st2) {
               const bf16x8 x = to_bf16x8(&ds[8 * st2]);
@@ -462,7 +465,7 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
         __syncthreads();  // every wave is done reading this stage's Q and dO
         const int ln = fresh_lane();
         {
-          const int kl = w * 32 + (ln & 31), hl = ln >> 5;
+          const int kl = Lds::ds_row(w * 32 + (ln & 31)), hl = ln >> 5;
   #pragma unroll
           for (int st2 = 0; st2 < 2; ++st2) {
             const bf16x8 x = ds_keep[st2];
@@ -472,17 +475,18 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
         }
         __syncthreads();  // dS^T of both query blocks complete
         // dQ block: A = dS (queries x keys) by transposing reads of dS^T (this wave's query
-        // block's region), B = K from K^T. Lane l of 16-lane group G supplies key row
-        // 16*st + 8*hi + (l%16)/4 (+4) and unit 4*(G%2) + l%4 of that row.
+        // block's region), B = K from K^T. Lane l of 16-lane group G supplies key
+        // 16*st + 8*hi + (l%16)/4 (+4), i.e. row 32*(st/2) + 4*(st%2) + 8*((l%16)/4) + 2*hi
+        // (+1), and unit 4*(G%2) + l%4 of that row (k-steps counted from the wave's first).
         const VC_LDS char* ds_src = dq_qb ? (const VC_LDS char*)stage : (const VC_LDS char*)ds_own;
-        const int arow = dq_s0 * 16 + 8 * (ln >> 5) + ((ln & 15) >> 2), aunit = 4 * ((ln >> 4) & 1) + (ln & 3);
+        const int arow = dq_s0 * 16 + 8 * ((ln & 15) >> 2) + 2 * (ln >> 5), aunit = 4 * ((ln >> 4) & 1) + (ln & 3);
         const VC_LDS char* b_base = (const VC_LDS char*)smem + Lds::KT_OFF + (dq_db * 32 + (ln & 31)) * Lds::KTS +
                                     (dq_s0 * 16 + 8 * (ln >> 5)) * 2;
         dq_blk = zero_f32x16();
   #pragma unroll
         for (int st = 0; st < DQ_STEPS; ++st) {
-          const int j = arow + 16 * st;
-          const bf16x8 da = cat4(lds_read_tr(ds_src + Lds::ds_at(j, aunit)), lds_read_tr(ds_src + Lds::ds_at(j + 4, aunit)));
+          const int j = arow + 32 * (st >> 1) + 4 * (st & 1);
+          const bf16x8 da = cat4(lds_read_tr(ds_src + Lds::ds_at(j, aunit)), lds_read_tr(ds_src + Lds::ds_at(j + 1, aunit)));
           const bf16x8 kb8 = *(const VC_LDS bf16x8*)(b_base + st * 32);
           dq_blk = mfma32(da, kb8, dq_blk);
         }
