@@ -88,6 +88,23 @@ def test_null_descriptor_and_pointers(lib):
     assert lib.vc_jointattn_bwd(ctypes.byref(d), p, p, p, p, p, None, None, None, p, p, p, p, 1 << 30, None) == -1
     assert lib.vc_jointattn_bwd_dkdv(ctypes.byref(d), p, p, None, p, None, None, p, p, p, 1 << 30, None) == -1
     assert lib.vc_jointattn_bwd_dq(ctypes.byref(d), p, p, p, p, None, None, None, p, 1 << 30, None) == -1
+    assert lib.vc_jointattn_bwd_fused(ctypes.byref(d), p, p, p, p, None, None, p, None, p, 1 << 30, None) == -1
+    assert lib.vc_jointattn_bwd_fused(None, p, p, p, p, None, None, p, p, p, 1 << 30, None) == -1
+
+
+def test_fused_dq_keys():
+    """Keys whose dQ share the fused pass carries: the leading 65% of the 256-key blocks,
+    rounded to whole blocks, never more than N; an invalid descriptor gives its status."""
+    long720p = vc.make_desc(1, 24, 128, 256, 16, 45, 80)  # 57,856 tokens, 226 blocks
+    assert vc.vc_jointattn_fused_dq_keys(long720p) == 147 * 256
+    tiny = vc.make_desc(1, 1, 64, 0, 1, 1, 5)  # 5 tokens, one block
+    assert vc.vc_jointattn_fused_dq_keys(tiny) == 5
+    for n_blocks in (1, 2, 3, 7, 100):
+        d = vc.make_desc(1, 1, 64, 0, 1, 1, 256 * n_blocks)
+        k = vc.vc_jointattn_fused_dq_keys(d)
+        assert k % 256 == 0 and 0 <= k <= 256 * n_blocks
+        assert k == 256 * ((n_blocks * 65 + 50) // 100)
+    assert vc.vc_jointattn_fused_dq_keys(vc.make_desc(1, 1, 96, 0, 1, 1, 5)) == -3  # head_dim
 
 
 def test_misaligned_pointers(lib):
@@ -98,6 +115,8 @@ def test_misaligned_pointers(lib):
     assert lib.vc_jointattn_fwd(ctypes.byref(d), p, p, p, None, None, p, p, p + 16, 1 << 30, None) == -4  # ws 256
     assert lib.vc_jointattn_bwd_prepare(ctypes.byref(d), p, p, p, p, p, p + 16, 1 << 30, None) == -4
     assert lib.vc_jointattn_bwd_dq(ctypes.byref(d), p, p, p, p, None, None, p + 8, p, 1 << 30, None) == -4
+    assert lib.vc_jointattn_bwd_fused(ctypes.byref(d), p, p, p, p, None, None, p + 8, p, p, 1 << 30, None) == -4
+    assert lib.vc_jointattn_bwd_fused(ctypes.byref(d), p, p, p, p, None, None, p, p, p + 64, 1 << 30, None) == -4
 
 
 def test_workspace_checks(lib):

@@ -317,3 +317,37 @@ def test_backward_reproducibility():
     for i, n in ((2, "dQ"), (3, "dK"), (4, "dV")):  # against the deterministic backward
         for f in (f0, f1):
             assert _same_up_to_order(bf16_values(f[i]), bf16_values(runs[True][0][i]), n + " fused vs deterministic")
+
+
+def test_staged_backward_calls():
+    """The stage entry points reproduce vc_jointattn_bwd in both modes, and the separate
+    dK/dV stage refuses a descriptor of the fused backward (whose stage 1 does not make the
+    token-major copies it reads)."""
+    import torch
+    vc = _vc()
+    w = W.custom(1, 2, 128, 24, 3, 9, 10, ragged_text=True)
+    x = W.make_inputs(w, seed=77)
+    g = _inputs_on_gpu(x)
+    q, k, v, do, tl = g["q"], g["k"], g["v"], g["do"], g["text_len"]
+    for det in (True, False):
+        desc = vc.desc_for(w, deterministic=det)
+        o, lse = vc.fwd(q, k, v, desc, tl)
+        ref = vc.bwd(q, k, v, o, lse, do, desc, tl)
+        dq, dk, dv = (torch.empty_like(q) for _ in range(3))
+        ws = vc.workspace(desc, "cuda")
+        s = torch.cuda.current_stream().cuda_stream
+        vc.vc_jointattn_bwd_prepare(desc, q, k, o, lse, do, ws, ws.numel(), s)
+        if det:
+            vc.vc_jointattn_bwd_dkdv(desc, q, k, v, do, tl, None, dk, dv, ws, ws.numel(), s)
+        else:
+            with pytest.raises(vc.JointAttnError) as e:
+                vc.vc_jointattn_bwd_dkdv(desc, q, k, v, do, tl, None, dk, dv, ws, ws.numel(), s)
+            assert e.value.status == -8
+            vc.vc_jointattn_bwd_fused(desc, q, k, v, do, tl, None, dk, dv, ws, ws.numel(), s)
+        vc.vc_jointattn_bwd_dq(desc, q, k, v, do, tl, None, dq, ws, ws.numel(), s)
+        torch.cuda.synchronize()
+        assert torch.equal(dk, ref[1]) and torch.equal(dv, ref[2])
+        if det:
+            assert torch.equal(dq, ref[0])
+        else:
+            assert _same_up_to_order(bf16_values(dq), bf16_values(ref[0]), "dQ staged vs one call")
