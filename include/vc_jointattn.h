@@ -135,7 +135,9 @@ size_t vc_jointattn_bwd_workspace_bytes(const vc_jointattn_desc* desc);
  * workgroups, and so the summation order of its rows, differs).
  * desc->deterministic = 0: stage 1 (token-major copy of k only),
  * vc_jointattn_bwd_fused, then stage 3 over the remaining keys; dk, dv are
- * reproducible run to run, dq only up to the rounding of its fp32 sums. */
+ * reproducible run to run, dq only up to the rounding of its fp32 sums. When
+ * vc_jointattn_fused_dq_keys(desc) is 0 (head_dim 64, where the fused pass is
+ * slower) it runs the deterministic stages instead. */
 vc_status vc_jointattn_bwd(const vc_jointattn_desc* desc,
                            const void* q, const void* k, const void* v,
                            const void* o, const float* lse, const void* dout,
@@ -184,8 +186,9 @@ vc_status vc_jointattn_bwd_dq(const vc_jointattn_desc* desc,
  * workspace; stage 3 (vc_jointattn_bwd_dq with desc->deterministic = 0)
  * completes dq. */
 /* Keys [0, K) whose share of dq the fused pass adds (vc_jointattn_bwd_fused);
- * stage 3 covers keys [K, N). Returns K, or a negative vc_status if the
- * descriptor is invalid. Host only. */
+ * stage 3 covers keys [K, N). Returns K (0 for head_dim 64: there
+ * vc_jointattn_bwd runs the deterministic stages whatever desc->deterministic
+ * says), or a negative vc_status if the descriptor is invalid. Host only. */
 int64_t vc_jointattn_fused_dq_keys(const vc_jointattn_desc* desc);
 
 vc_status vc_jointattn_bwd_fused(const vc_jointattn_desc* desc,

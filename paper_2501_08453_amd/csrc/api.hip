@@ -115,9 +115,13 @@ size_t tail_part_bytes(const vc_jointattn_desc* d, int64_t n) {
 // the key-stationary pass; the dQ pass covers the others. Per key block, the atomics (an
 // fp32 dQ tile per query tile) cost about what the dQ pass's recomputation of S and dP
 // costs, so the backward's time is nearly flat in the fraction between 1/2 and 7/8;
-// 65% measured fastest on the long workload.
+// 65% measured fastest on the long workload. With head_dim 64 two waves share each dQ
+// block (each over half the keys), doubling the atomics, and the fused backward is slower
+// than the separate passes (medium workload: 2.6 against 2.3 ms): none, and the one-call
+// backward runs the separate passes.
 constexpr int kFusedDqPercent = 65;
-int fused_dq_blocks(int64_t n) {
+int fused_dq_blocks(const vc_jointattn_desc* d, int64_t n) {
+  if (d->head_dim != 128) return 0;
   const int nblk = (int)((n + vcja::kDkdvKeys - 1) / vcja::kDkdvKeys);
   return (int)(((int64_t)nblk * kFusedDqPercent + 50) / 100);
 }
@@ -253,7 +257,7 @@ int64_t vc_jointattn_fused_dq_keys(const vc_jointattn_desc* desc) {
   int64_t n = 0;
   const vc_status st = check_desc(desc, &n);
   if (st != VC_OK) return (int64_t)st;
-  return std::min<int64_t>(n, (int64_t)fused_dq_blocks(n) * vcja::kDkdvKeys);
+  return std::min<int64_t>(n, (int64_t)fused_dq_blocks(desc, n) * vcja::kDkdvKeys);
 }
 
 size_t vc_spatialattn_bwd_workspace_bytes(const vc_jointattn_desc* desc) {
@@ -407,7 +411,7 @@ vc_status dkdv_impl(const vc_jointattn_desc* desc, const void* q, const void* k,
   // Fused dQ: the fp32 accumulator takes the place of the transposed Q and dO tiles, which
   // the fused backward does not make (2 tile sets >= 4 bytes per element of dq).
   a.dq_acc = fused ? reinterpret_cast<float*>(w.qt) : nullptr;
-  a.dq_blocks = fused ? fused_dq_blocks(n) : 0;
+  a.dq_blocks = fused ? fused_dq_blocks(desc, n) : 0;
   a.B = desc->batch;
   a.H = desc->heads;
   a.N = (int)n;
@@ -435,7 +439,7 @@ vc_status dq_impl(const vc_jointattn_desc* desc, const void* q, const void* k, c
   // Completing a fused backward: the key tiles of the blocks that did not add their dQ
   // share, plus the accumulator the others filled.
   if (fused) {
-    a.kt_min = fused_dq_blocks(n) * (vcja::kDkdvKeys / vcja::kTileTok);
+    a.kt_min = fused_dq_blocks(desc, n) * (vcja::kDkdvKeys / vcja::kTileTok);
     a.dq_acc = reinterpret_cast<const float*>(w.qt);
   }
   a.q = bf(q);
@@ -476,9 +480,9 @@ vc_status bwd_impl(const vc_jointattn_desc* desc, const void* q, const void* k, 
   if (st != VC_OK) return st;
   if (!q || !k || !v || !o || !lse || !dout || !dq || !dk || !dv) return VC_ERR_NULL;
   if (spatial && (st = check_ws(workspace, workspace_bytes, spatial_bwd_ws_bytes(desc, n))) != VC_OK) return st;
-  // Joint attention: dQ fused into the key-stationary kernel (atomics), unless the caller
-  // asks for bitwise reproducible results.
-  if (!spatial && !desc->deterministic) {
+  // Joint attention: dQ partly fused into the key-stationary kernel (atomics), unless the
+  // caller asks for bitwise reproducible results or the fused pass would carry no keys.
+  if (!spatial && !desc->deterministic && fused_dq_blocks(desc, n) > 0) {
     if ((st = prepare_impl(desc, q, k, o, lse, dout, workspace, workspace_bytes, stream, false)) != VC_OK ||
         (st = vc_jointattn_bwd_fused(desc, q, k, v, dout, text_len, key_mask, dk, dv, workspace, workspace_bytes,
                                      stream)) != VC_OK)

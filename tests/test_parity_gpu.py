@@ -319,13 +319,16 @@ def test_backward_reproducibility():
             assert _same_up_to_order(bf16_values(f[i]), bf16_values(runs[True][0][i]), n + " fused vs deterministic")
 
 
-def test_staged_backward_calls():
+@pytest.mark.parametrize("head_dim", [128, 64])
+def test_staged_backward_calls(head_dim):
     """The stage entry points reproduce vc_jointattn_bwd in both modes, and the separate
     dK/dV stage refuses a descriptor of the fused backward (whose stage 1 does not make the
-    token-major copies it reads)."""
+    token-major copies it reads). With head_dim 64 the fused pass carries no keys' dQ and
+    vc_jointattn_bwd runs the separate passes; the staged fused calls still give the same
+    gradients (dK, dV summed over the query tiles in another order)."""
     import torch
     vc = _vc()
-    w = W.custom(1, 2, 128, 24, 3, 9, 10, ragged_text=True)
+    w = W.custom(1, 2, head_dim, 24, 3, 9, 10, ragged_text=True)
     x = W.make_inputs(w, seed=77)
     g = _inputs_on_gpu(x)
     q, k, v, do, tl = g["q"], g["k"], g["v"], g["do"], g["text_len"]
@@ -346,8 +349,13 @@ def test_staged_backward_calls():
             vc.vc_jointattn_bwd_fused(desc, q, k, v, do, tl, None, dk, dv, ws, ws.numel(), s)
         vc.vc_jointattn_bwd_dq(desc, q, k, v, do, tl, None, dq, ws, ws.numel(), s)
         torch.cuda.synchronize()
-        assert torch.equal(dk, ref[1]) and torch.equal(dv, ref[2])
-        if det:
+        if det or head_dim == 128:
+            assert torch.equal(dk, ref[1]) and torch.equal(dv, ref[2])
+        else:
+            assert vc.vc_jointattn_fused_dq_keys(desc) == 0
+            assert _same_up_to_order(bf16_values(dk), bf16_values(ref[1]), "dK staged fused vs separate")
+            assert _same_up_to_order(bf16_values(dv), bf16_values(ref[2]), "dV staged fused vs separate")
+        if det or head_dim == 64:
             assert torch.equal(dq, ref[0])
         else:
             assert _same_up_to_order(bf16_values(dq), bf16_values(ref[0]), "dQ staged vs one call")
