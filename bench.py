@@ -176,12 +176,24 @@ TEMPORAL_SOURCES = ["paper_2501_08453_amd/csrc/temporal.hip", "paper_2501_08453_
                     "paper_2501_08453_amd/csrc/common.hpp"]
 
 
+def code_only(text: str) -> str:
+    """Source text without // comments, trailing blanks and blank lines, so that a traffic
+    record stays tied to the code it was measured on, not to its commentary. (The kernel
+    sources keep no // inside string literals.)"""
+    out = []
+    for line in text.splitlines():
+        line = line.split("//", 1)[0].rstrip()
+        if line:
+            out.append(line)
+    return "\n".join(out)
+
+
 def kernel_source_digest(sources=KERNEL_SOURCES) -> str:
     import hashlib
     h = hashlib.sha256()
     for rel in sources:
-        with open(os.path.join(ROOT, rel), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, rel), encoding="utf-8") as f:
+            h.update(code_only(f.read()).encode())
     return h.hexdigest()
 
 

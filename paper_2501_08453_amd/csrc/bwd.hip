@@ -15,17 +15,18 @@
 //   layout (lane column = key). The transposed operands Q^T, dO^T come either
 //   from transposed token tiles made by a reformatting pass (separate dQ pass)
 //   or, with dQ fused in, from the row-major tiles through transposing LDS reads.
-// dQ, fused (the default for joint attention): in the workgroups of the first
-//   key blocks (a fraction set by the host), after the dK/dV products of a tile,
-//   the waves exchange dS^T through LDS (the first 32 queries in a region of its
-//   own, the others over the tile's Q|dO region, dead by then) and each wave
-//   computes one 32x32 block of the tile's dQ / scale = dS K over the
-//   workgroup's 256 keys, with K^T held in LDS for the workgroup's lifetime. The block is added to an fp32 accumulator with
-//   atomics one tile later (so that the wait for the next tile's copies does not
-//   also wait for them), and the workgroups of each XCD start their walk at a
-//   different query tile so that concurrent atomics spread over the accumulator.
-//   For those keys S and dP are computed once per (query, key) pair; the atomic
-//   traffic (fp32 dQ rows per key block) is what limits the fraction: the dQ pass
+// dQ, fused (the default for joint attention at head_dim 128): in the workgroups
+//   of the first key blocks (a fraction set by the host), after the dK/dV products
+//   of a tile, the waves exchange dS^T through LDS (the first 32 queries in a
+//   region of its own, the others over the tile's Q|dO region, dead by then) and
+//   each wave computes one 32x32 block of the tile's dQ / scale = dS K over the
+//   workgroup's 256 keys, with K^T held in LDS for the workgroup's lifetime. The
+//   block is added to an fp32 accumulator with atomics one tile later (so that
+//   the wait for the next tile's copies does not also wait for them), and the
+//   workgroups of each XCD start their walk at a different query tile so that
+//   concurrent atomics spread over the accumulator. For those keys S and dP are
+//   computed once per (query, key) pair; the atomic traffic (fp32 dQ rows per key
+//   block, performed at the memory side) is what limits the fraction: the dQ pass
 //   below then covers only the other key blocks' tiles and adds the accumulator.
 //   The order of the atomic additions, and so the rounding of dQ, varies from run
 //   to run.
