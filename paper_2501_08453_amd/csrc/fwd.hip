@@ -7,7 +7,10 @@
 // global -> LDS. Scores read the K tile one step before the P V products read
 // the V^T tile of the same keys, so each has its own two-slot ring (tile t in
 // slot t mod 2): the copies of step j+1 are in flight during step j, and one
-// barrier per tile suffices. All eight waves share each tile.
+// barrier per tile suffices. All eight waves share each tile. Each wave issues its
+// share of those copies between its score products rather than all at the top of
+// the step, where eight waves' worth of copy instructions would stall the start of
+// the matrix-core work.
 //
 // The wave computes the transposed score block S^T = K Q^T with 32x32x16 bf16
 // matrix-core steps, so each lane's accumulator column is one query: the
@@ -47,21 +50,36 @@ struct FwdTile {
   static constexpr int LDS = 2 * KT + 2 * VTB;        // K ring | V^T ring
 };
 
+struct NoHook {
+  __device__ void operator()(int) const {}
+};
+
 // S^T (keys x queries) of one 64-key tile: two 32x32 blocks, A = K rows from LDS,
-// B = this wave's Q^T fragments.
-template <int D>
-__device__ __forceinline__ void scores(const VC_LDS char* ks_lds, const bf16x8* qf, int l32, int hi, f32x16* s) {
+// B = this wave's Q^T fragments, K fragments read two k-steps ahead of their products.
+// hook(j) runs after k-step 2j+1 (j < D/32).
+template <int D, class Hook = NoHook>
+__device__ __forceinline__ void scores(const VC_LDS char* ks_lds, const bf16x8* qf, int l32, int hi, f32x16* s,
+                                       Hook hook = Hook()) {
   constexpr int KS = FwdTile<D>::KS;
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) s[kb] = zero_f32x16();
+  constexpr int KSN = D / 16;
+  bf16x8 f[KSN][2];
+  auto rd = [&](int ks) {
 #pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks) {
+    for (int kb = 0; kb < 2; ++kb) f[ks][kb] = *(const VC_LDS bf16x8*)(ks_lds + (kb * 32 + l32) * KS + (2 * ks + hi) * 16);
+  };
+  rd(0);
+  rd(1);
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      const bf16x8 af = *(const VC_LDS bf16x8*)(ks_lds + (kb * 32 + l32) * KS + (2 * ks + hi) * 16);
-      s[kb] = mfma32(af, qf[ks], s[kb]);
-    }
+  for (int ks = 0; ks < KSN; ++ks) {
+    sched_fence();
+    if (ks + 2 < KSN) rd(ks + 2);
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) s[kb] = mfma32(f[ks][kb], qf[ks], s[kb]);
+    if (ks & 1) hook(ks >> 1);
   }
+  sched_fence();
 }
 
 // O^T += V^T P^T for one 64-key tile. Operand element t of k-step st2 (lane half hi) is
@@ -236,15 +254,31 @@ __global__ __launch_bounds__(64 * kWaves, kWavesPerSimd * 4 / kWaves) void fwd_k
   }
   auto next_tile = [&](int kt) { return runs.next(kt); };
   // Copies tile kt's K rows (rows past N repeat row N-1 and are masked) or V^T tile into
-  // ring slot `slot`.
+  // ring slot `slot`. The copies are issued through inline assembly, so the compiler
+  // neither waits for them nor lets them force full waits on LDS reads; the kernel waits
+  // for them itself (wait_all_memory) before the barrier after which they are read.
   auto issue_k = [&](int kt, int slot) {
     VC_LDS char* dst = (VC_LDS char*)smem + slot * KT;
-    for (int idx = w; idx < KCOPIES; idx += kWaves) copy_row_tile<D>(a.k + base, tok, kt * kBN, N, dst, idx, lane);
+    for (int idx = w; idx < KCOPIES; idx += kWaves) copy_row_tile<D, true>(a.k + base, tok, kt * kBN, N, dst, idx, lane);
   };
   auto issue_v = [&](int kt, int slot) {
     VC_LDS char* dst = (VC_LDS char*)smem + 2 * KT + slot * VTB;
     const __bf16* vsrc = vt_bh + (size_t)kt * tile_elems(D);
-    for (int idx = w; idx < VCOPIES; idx += kWaves) copy16_to_lds(vsrc + idx * 512 + lane * 8, dst + idx * 1024);
+    for (int idx = w; idx < VCOPIES; idx += kWaves) copy16_to_lds_opaque(vsrc + idx * 512 + lane * 8, dst + idx * 1024);
+  };
+  // The j-th K or V^T copy of this wave (a no-op past the tile), issued from the score
+  // loop's hook.
+  static_assert((KCOPIES + kWaves - 1) / kWaves <= D / 32 && (VCOPIES + kWaves - 1) / kWaves <= D / 32,
+                "every copy of a wave needs a hook slot");
+  auto k_copy = [&](int j, int kt, int slot) {
+    const int idx = w + j * kWaves;
+    if (idx < KCOPIES) copy_row_tile<D, true>(a.k + base, tok, kt * kBN, N, (VC_LDS char*)smem + slot * KT, idx, lane);
+  };
+  auto v_copy = [&](int j, int kt, int slot) {
+    const int idx = w + j * kWaves;
+    if (idx < VCOPIES)
+      copy16_to_lds_opaque(vt_bh + (size_t)kt * tile_elems(D) + idx * 512 + lane * 8,
+                           (VC_LDS char*)smem + 2 * KT + slot * VTB + idx * 1024);
   };
   auto k_slot = [&](int slot) { return (const VC_LDS char*)smem + slot * KT; };
   auto v_slot = [&](int slot) { return (const VC_LDS char*)smem + 2 * KT + slot * VTB; };
@@ -285,14 +319,17 @@ __global__ __launch_bounds__(64 * kWaves, kWavesPerSimd * 4 / kWaves) void fwd_k
       wait_all_memory();
       __syncthreads();  // K of `nxt` and V^T of `cur` landed; K of `cur` and V^T of the
                         // previous tile are no longer read by any wave
-      if (nn < a.ntile) issue_k(nn, par);
-      issue_v(nxt, par ^ 1);
       if (__any(raise)) {
 #pragma unroll
         for (int i = 0; i < D / 32; ++i) oacc[i] *= alpha;
       }
       f32x16 s[2];
-      scores<D>(k_slot(par ^ 1), qf, l32, hi, s);
+      // The copies of this step go to the slots freed by the barrier: K of `nn` to the
+      // slot of K of `cur`, V^T of `nxt` to the slot of the previous V^T tile.
+      scores<D>(k_slot(par ^ 1), qf, l32, hi, s, [&](int j) {
+        if (nn < a.ntile) k_copy(j, nn, par);
+        v_copy(j, nxt, par ^ 1);
+      });
       if (mask.tile_needs_mask(nxt * kBN)) mask.apply(s, nxt * kBN, hi);
       // P V of `cur` in four chunks of D/32 products; between them the vector ALUs do
       // the softmax of `nxt`: first its new base, then one operand's probabilities per
@@ -309,6 +346,14 @@ __global__ __launch_bounds__(64 * kWaves, kWavesPerSimd * 4 / kWaves) void fwd_k
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) oacc[db] = mfma32(fa[db], pb[c], oacc[db]);
         pn[c] = probs8(s[c >> 1], c & 1, a.scale_log2, m, psum);
+        if (c < 3) {  // the next chunk's reads first, then products and softmax interleaved
+          __builtin_amdgcn_sched_group_barrier(0x100, D / 32, 0);
+#pragma unroll
+          for (int db = 0; db < D / 32; ++db) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
+          }
+        }
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) fa[db] = fb[db];
       }
