@@ -681,11 +681,26 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
   auto issue = [&](int kt, int st) {
     VC_LDS char* sk = (VC_LDS char*)smem + st * STAGE;
     for (int idx = w; idx < RCOPIES; idx += kDqWaves) {
-      copy_row_tile<D>(a.k + base, tok, kt * kBN, N, sk, idx, lane);
-      copy_row_tile<D>(a.v + base, tok, kt * kBN, N, sk + RT, idx, lane);
+      copy_row_tile<D, true>(a.k + base, tok, kt * kBN, N, sk, idx, lane);
+      copy_row_tile<D, true>(a.v + base, tok, kt * kBN, N, sk + RT, idx, lane);
     }
     const __bf16* tsrc = a.kt + (bh * a.ntile + kt) * tile_elems(D);
-    for (int idx = w; idx < TCOPIES; idx += kDqWaves) copy16_to_lds(tsrc + idx * 512 + lane * 8, sk + 2 * RT + idx * 1024);
+    for (int idx = w; idx < TCOPIES; idx += kDqWaves) copy16_to_lds_opaque(tsrc + idx * 512 + lane * 8, sk + 2 * RT + idx * 1024);
+  };
+  // The j-th copies of this wave (no-ops past the tile), issued between the score
+  // products of the step's first key block: issued all at the top of the step, eight
+  // waves' copies would hold up the start of every wave's matrix-core work.
+  static_assert((RCOPIES + kDqWaves - 1) / kDqWaves <= D / 32 && (TCOPIES + kDqWaves - 1) / kDqWaves <= D / 32,
+                "every copy of a wave needs a slot among the score products");
+  auto issue_j = [&](int j, int kt, int st) {
+    VC_LDS char* sk = (VC_LDS char*)smem + st * STAGE;
+    const int idx = w + j * kDqWaves;
+    if (idx < RCOPIES) {
+      copy_row_tile<D, true>(a.k + base, tok, kt * kBN, N, sk, idx, lane);
+      copy_row_tile<D, true>(a.v + base, tok, kt * kBN, N, sk + RT, idx, lane);
+    }
+    if (idx < TCOPIES)
+      copy16_to_lds_opaque(a.kt + (bh * a.ntile + kt) * tile_elems(D) + idx * 512 + lane * 8, sk + 2 * RT + idx * 1024);
   };
 
   int kt = next_tile(max(kt0, a.kt_min));  // completing a fused backward: keys >= kt_min only
@@ -695,7 +710,6 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
     const int kn = next_tile(kt + 1);
     wait_all_memory();
     __syncthreads();
-    if (kn < a.ntile) issue(kn, st ^ 1);
     const VC_LDS char* k_lds = (const VC_LDS char*)smem + st * STAGE;
     const VC_LDS char* v_lds = k_lds + RT;
     const VC_LDS char* kt_lds = k_lds + 2 * RT;
@@ -717,6 +731,7 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
       for (int ks = 0; ks < D / 16; ++ks) {
         const bf16x8 ka = *(const VC_LDS bf16x8*)(k_lds + (kb * 32 + l32) * RS + (2 * ks + hi) * 16);
         s = mfma32(ka, qf[ks], s);
+        if (kb == 0 && (ks & 1) && kn < a.ntile) issue_j(ks >> 1, kn, st ^ 1);
       }
 #pragma unroll
       for (int ks = 0; ks < D / 16; ++ks) {
