@@ -1,0 +1,100 @@
+"""Properties of the compiled gfx950 kernels that the compiler does not check for us (CPU only:
+hipcc cross-compiles the device code to assembly).
+
+- The inline-assembly LDS copies set M0 themselves; a kernel that uses them must not rely on
+  M0 anywhere else. Every M0 write must therefore be one copy's own, right before its
+  global -> LDS instruction, and every such instruction must come from those copies.
+- Packed fp32 arithmetic is disabled at build time; no packed fp32 add, multiply or fma may
+  appear in any kernel.
+- The hot joint-attention kernels fit their register budget without scratch spills.
+"""
+import os
+import re
+import shutil
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+from paper_2501_08453_amd import build as B  # noqa: E402
+
+SOURCES = ["fwd.hip", "bwd.hip", "temporal.hip", "layout.hip", "offload.hip"]
+
+
+@pytest.fixture(scope="module")
+def device_asm(tmp_path_factory):
+    try:
+        cc = B.hipcc()
+    except Exception as e:  # pragma: no cover - toolchain missing
+        pytest.skip("hipcc not available: %s" % e)
+    if not shutil.which(cc) and not os.path.exists(cc):
+        pytest.skip("hipcc not available")
+    out = tmp_path_factory.mktemp("asm")
+    flags = [f for f in B.HIPCC_FLAGS if f not in ("-shared", "-fPIC")]
+    asm = {}
+    for fn in SOURCES:
+        dst = str(out / (fn + ".s"))
+        r = subprocess.run([cc, *flags, "-I", os.path.join(ROOT, "include"), "--cuda-device-only", "-S",
+                            os.path.join(B.CSRC, fn), "-o", dst], capture_output=True, text=True, timeout=600)
+        assert r.returncode == 0, r.stderr[-2000:]
+        with open(dst) as f:
+            asm[fn] = f.read()
+    return asm
+
+
+def kernels(text):
+    """(mangled name, body) of every kernel in an assembly file."""
+    for m in re.finditer(r"^(_Z\w+):", text, re.M):
+        end = text.find(".Lfunc_end", m.end())
+        yield m.group(1), text[m.end():end]
+
+
+def instructions(body):
+    for line in body.split("\n"):
+        line = line.split(";", 1)[0].strip()
+        if line and not line.startswith(".") and not line.endswith(":"):
+            yield line
+
+
+def test_m0_is_set_only_by_the_lds_copies(device_asm):
+    seen_copies = 0
+    for fn, text in device_asm.items():
+        for name, body in kernels(text):
+            ins = list(instructions(body))
+            for i, line in enumerate(ins):
+                if re.search(r"\bm0\b", line):
+                    assert re.match(r"s_mov_b32 m0, s\d+$", line), (fn, name, line)
+                    nxt = [x for x in ins[i + 1:i + 3] if not x.startswith("s_nop")]
+                    assert nxt and nxt[0].startswith("global_load_lds_dwordx4"), (fn, name, ins[i:i + 3])
+                if line.startswith("global_load_lds") or re.match(r"buffer_load\w*.*\blds\b", line):
+                    prev = [x for x in ins[max(0, i - 2):i] if not x.startswith("s_nop")]
+                    assert prev and prev[-1].startswith("s_mov_b32 m0,"), (fn, name, ins[max(0, i - 2):i + 1])
+                    seen_copies += 1
+    assert seen_copies > 0  # the forward, dK/dV and dQ kernels all copy tiles this way
+
+
+def test_no_packed_fp32_arithmetic(device_asm):
+    for fn, text in device_asm.items():
+        hits = re.findall(r"\bv_pk_(?:add|mul|fma)_f32\b", text)
+        assert not hits, (fn, hits[:3])
+
+
+HOT = [
+    ("fwd.hip", "fwd_kernelILi128EE"),
+    ("fwd.hip", "fwd_kernelILi64EE"),
+    ("bwd.hip", "bwd_dkdv_kernelILi128ELb0ELb1EE"),  # fused joint dK/dV (+dQ)
+    ("bwd.hip", "bwd_dkdv_kernelILi128ELb0ELb0EE"),  # separate joint dK/dV
+    ("bwd.hip", "bwd_dq_kernelILi128EE"),
+    ("bwd.hip", "bwd_dq_kernelILi64EE"),
+]
+
+
+@pytest.mark.parametrize("fn,kernel", HOT, ids=[k for _, k in HOT])
+def test_hot_kernels_do_not_spill(device_asm, fn, kernel):
+    text = device_asm[fn]
+    m = re.search(r"\.name:\s+_Z\w*%s\w*\n(?:.*\n){0,40}?\s+\.vgpr_spill_count:\s+(\d+)" % kernel, text)
+    assert m, kernel
+    assert int(m.group(1)) == 0, (kernel, "spills", m.group(1))
