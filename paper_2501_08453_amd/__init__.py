@@ -15,6 +15,11 @@ PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG_DIR, "libvc_jointattn.so")
 HEADER = os.path.join(os.path.dirname(PKG_DIR), "include", "vc_jointattn.h")
 
+# The ABI the signatures below describe (VC_JOINTATTN_ABI_VERSION of include/vc_jointattn.h);
+# a library reporting another version is refused, so that no call can reach an entry point
+# whose arguments differ from what this binding passes.
+ABI_VERSION = 6
+
 VC_OK = 0
 STATUS = {
     0: "VC_OK", -1: "VC_ERR_NULL", -2: "VC_ERR_SHAPE", -3: "VC_ERR_HEAD_DIM", -4: "VC_ERR_ALIGN",
@@ -86,6 +91,14 @@ def _lib() -> ctypes.CDLL:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError("libvc_jointattn.so is not built (%s); run __graft_entry__.build()" % LIB_PATH)
         lib = ctypes.CDLL(LIB_PATH)
+        # The version first, through the one signature every version shares; nothing else is
+        # bound unless it matches.
+        ver = lib.vc_jointattn_abi_version
+        ver.restype, ver.argtypes = ctypes.c_int, []
+        got = ver()
+        if got != ABI_VERSION:
+            raise RuntimeError("%s implements C ABI version %d, this binding version %d; rebuild the library "
+                               "(__graft_entry__.build())" % (LIB_PATH, got, ABI_VERSION))
         for name, (res, args) in _SIGS.items():
             fn = getattr(lib, name)
             fn.restype = res
@@ -242,17 +255,23 @@ def vc_temporalattn_bwd(desc, q, k, v, o, lse, dout, key_mask, dq, dk, dv, works
 # Tensor-level helpers: allocate outputs with torch, then call the library.
 # --------------------------------------------------------------------------
 
-def _check_tensor(name, t, shape, dtype):
-    import torch
-    if t.device.type != "cuda":
-        raise ValueError("%s must be on a GPU" % name)
+def _check_shape(name, t, shape, dtype):
     if t.dtype != dtype:
         raise ValueError("%s must be %s, got %s" % (name, dtype, t.dtype))
     if tuple(t.shape) != tuple(shape):
         raise ValueError("%s has shape %s, expected %s" % (name, tuple(t.shape), tuple(shape)))
+
+
+def _check_placed(name, t):
+    if t.device.type != "cuda":
+        raise ValueError("%s must be on a GPU" % name)
     if not t.is_contiguous():
         raise ValueError("%s must be contiguous" % name)
-    del torch
+
+
+def _check_tensor(name, t, shape, dtype):
+    _check_shape(name, t, shape, dtype)
+    _check_placed(name, t)
 
 
 def _workspace(nbytes, device):
@@ -276,20 +295,42 @@ def spatial_workspace(desc, device):
     return _workspace(vc_spatialattn_bwd_workspace_bytes(desc), device)
 
 
+def _check_joint_inputs(desc, tensors, text_len=None, key_mask=None, lse=None):
+    """Shapes, dtypes and layout of the tensors of one call against each other and the
+    descriptor (the library reads and writes [B, N, H, D] as the descriptor says, so a
+    descriptor larger than the tensors must never reach it). Shapes and dtypes are checked
+    before placement. Returns (B, N, H, D)."""
+    import torch
+    q = tensors[0][1]
+    if q.dim() != 4:
+        raise ValueError("q must have shape [B, N, H, D], got %s" % (tuple(q.shape),))
+    B, N, H, D = q.shape
+    every = [(n, t, (B, N, H, D), torch.bfloat16) for n, t in tensors]
+    if text_len is not None:
+        every.append(("text_len", text_len, (B,), torch.int32))
+    if key_mask is not None:
+        every.append(("key_mask", key_mask, (B, N), torch.uint8))
+    if lse is not None:
+        every.append(("lse", lse, (B, H, N), torch.float32))
+    for n, t, shape, dtype in every:
+        _check_shape(n, t, shape, dtype)
+    if (desc.batch, desc.heads, desc.head_dim) != (B, H, D):
+        raise ValueError("descriptor gives B=%d, H=%d, D=%d, tensors have B=%d, H=%d, D=%d"
+                         % (desc.batch, desc.heads, desc.head_dim, B, H, D))
+    if vc_jointattn_tokens(desc) != N:
+        raise ValueError("descriptor gives N=%d, tensors have N=%d" % (vc_jointattn_tokens(desc), N))
+    for n, t, _, _ in every:
+        _check_placed(n, t)
+    return B, N, H, D
+
+
 def fwd(q, k, v, desc, text_len=None, key_mask=None, out=None, lse=None, ws=None):
     """(o, lse) for bf16 q, k, v of shape [B, N, H, D]."""
     import torch
-    B, N, H, D = q.shape
-    for n, t in (("q", q), ("k", k), ("v", v)):
-        _check_tensor(n, t, (B, N, H, D), torch.bfloat16)
-    if vc_jointattn_tokens(desc) != N:
-        raise ValueError("descriptor gives N=%d, tensors have N=%d" % (vc_jointattn_tokens(desc), N))
-    if text_len is not None:
-        _check_tensor("text_len", text_len, (B,), torch.int32)
-    if key_mask is not None:
-        _check_tensor("key_mask", key_mask, (B, N), torch.uint8)
+    B, N, H, D = _check_joint_inputs(desc, (("q", q), ("k", k), ("v", v)), text_len, key_mask)
     o = torch.empty_like(q) if out is None else out
     lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device) if lse is None else lse
+    _check_joint_inputs(desc, (("q", q), ("o", o)), lse=lse)
     ws = fwd_workspace(desc, q.device) if ws is None else ws
     vc_jointattn_fwd(desc, q, k, v, text_len, key_mask, o, lse, ws, ws.numel())
     return o, lse
@@ -298,39 +339,27 @@ def fwd(q, k, v, desc, text_len=None, key_mask=None, out=None, lse=None, ws=None
 def bwd(q, k, v, o, lse, dout, desc, text_len=None, key_mask=None, ws=None, dq=None, dk=None, dv=None):
     """(dq, dk, dv) for bf16 tensors of shape [B, N, H, D]."""
     import torch
-    B, N, H, D = q.shape
-    for n, t in (("q", q), ("k", k), ("v", v), ("o", o), ("dout", dout)):
-        _check_tensor(n, t, (B, N, H, D), torch.bfloat16)
-    _check_tensor("lse", lse, (B, H, N), torch.float32)
+    _check_joint_inputs(desc, (("q", q), ("k", k), ("v", v), ("o", o), ("dout", dout)), text_len, key_mask, lse)
     ws = workspace(desc, q.device) if ws is None else ws
     dq = torch.empty_like(q) if dq is None else dq
     dk = torch.empty_like(q) if dk is None else dk
     dv = torch.empty_like(q) if dv is None else dv
+    _check_joint_inputs(desc, (("q", q), ("dq", dq), ("dk", dk), ("dv", dv)))
     vc_jointattn_bwd(desc, q, k, v, o, lse, dout, text_len, key_mask, dq, dk, dv, ws, ws.numel())
     return dq, dk, dv
 
 
 def _check_branch_inputs(desc, tensors, key_mask=None):
-    import torch
-    q = tensors[0][1]
-    B, N, H, D = q.shape
-    for n, t in tensors:
-        _check_tensor(n, t, (B, N, H, D), torch.bfloat16)
-    if vc_jointattn_tokens(desc) != N:
-        raise ValueError("descriptor gives N=%d, tensors have N=%d" % (vc_jointattn_tokens(desc), N))
-    if key_mask is not None:
-        _check_tensor("key_mask", key_mask, (B, N), torch.uint8)
-    return B, N, H, D
+    return _check_joint_inputs(desc, tensors, None, key_mask)
 
 
 def spatial_fwd(q, k, v, desc, text_len=None, key_mask=None, out=None, lse=None, ws=None):
     """Spatial branch (o, lse) for bf16 q, k, v of shape [B, N, H, D] (joint layout)."""
     import torch
-    B, N, H, D = _check_branch_inputs(desc, (("q", q), ("k", k), ("v", v)), key_mask)
-    if text_len is not None:
-        _check_tensor("text_len", text_len, (B,), torch.int32)
+    B, N, H, D = _check_joint_inputs(desc, (("q", q), ("k", k), ("v", v)), text_len, key_mask)
     o = torch.empty_like(q) if out is None else out
     lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device) if lse is None else lse
+    _check_joint_inputs(desc, (("q", q), ("o", o)), lse=lse)
     ws = fwd_workspace(desc, q.device) if ws is None else ws
     vc_spatialattn_fwd(desc, q, k, v, text_len, key_mask, o, lse, ws, ws.numel())
     return o, lse
@@ -339,8 +368,7 @@ def spatial_fwd(q, k, v, desc, text_len=None, key_mask=None, out=None, lse=None,
 def spatial_bwd(q, k, v, o, lse, dout, desc, text_len=None, key_mask=None, ws=None):
     """Spatial branch (dq, dk, dv)."""
     import torch
-    B, N, H, D = _check_branch_inputs(desc, (("q", q), ("k", k), ("v", v), ("o", o), ("dout", dout)), key_mask)
-    _check_tensor("lse", lse, (B, H, N), torch.float32)
+    _check_joint_inputs(desc, (("q", q), ("k", k), ("v", v), ("o", o), ("dout", dout)), text_len, key_mask, lse)
     ws = spatial_workspace(desc, q.device) if ws is None else ws
     dq, dk, dv = (torch.empty_like(q) for _ in range(3))
     vc_spatialattn_bwd(desc, q, k, v, o, lse, dout, text_len, key_mask, dq, dk, dv, ws, ws.numel())
@@ -353,6 +381,7 @@ def temporal_fwd(q, k, v, desc, key_mask=None, out=None, lse=None):
     B, N, H, D = _check_branch_inputs(desc, (("q", q), ("k", k), ("v", v)), key_mask)
     o = torch.empty_like(q) if out is None else out
     lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device) if lse is None else lse
+    _check_joint_inputs(desc, (("q", q), ("o", o)), lse=lse)
     vc_temporalattn_fwd(desc, q, k, v, key_mask, o, lse)
     return o, lse
 
@@ -367,6 +396,7 @@ def temporal_fwd_sum(q, k, v, desc, o_joint=None, o_spatial=None, key_mask=None,
     o = torch.empty_like(q)
     lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
     out = torch.empty_like(q) if out is None else out
+    _check_joint_inputs(desc, (("q", q), ("out", out)))
     vc_temporalattn_fwd_sum(desc, q, k, v, key_mask, o_joint, o_spatial, o, lse, out)
     return o, lse, out
 
@@ -374,11 +404,12 @@ def temporal_fwd_sum(q, k, v, desc, o_joint=None, o_spatial=None, key_mask=None,
 def branch_sum(desc, o_joint=None, o_spatial=None, o_temporal=None, out=None):
     """Block output o_joint + o_spatial + o_temporal (bf16, summed in fp32, one rounding)."""
     import torch
-    first = next(t for t in (o_joint, o_spatial, o_temporal) if t is not None)
-    for name, t in (("o_joint", o_joint), ("o_spatial", o_spatial), ("o_temporal", o_temporal)):
-        if t is not None:
-            _check_tensor(name, t, tuple(first.shape), torch.bfloat16)
-    out = torch.empty_like(first) if out is None else out
+    given = [(n, t) for n, t in (("o_joint", o_joint), ("o_spatial", o_spatial), ("o_temporal", o_temporal))
+             if t is not None]
+    if not given:
+        raise ValueError("branch_sum needs at least one branch output")
+    out = torch.empty_like(given[0][1]) if out is None else out
+    _check_joint_inputs(desc, given + [("out", out)])
     vc_branchsum(desc, o_joint, o_spatial, o_temporal, out)
     return out
 
@@ -426,8 +457,7 @@ class Offload:
 def temporal_bwd(q, k, v, o, lse, dout, desc, key_mask=None, ws=None):
     """Temporal branch (dq, dk, dv)."""
     import torch
-    B, N, H, D = _check_branch_inputs(desc, (("q", q), ("k", k), ("v", v), ("o", o), ("dout", dout)), key_mask)
-    _check_tensor("lse", lse, (B, H, N), torch.float32)
+    _check_joint_inputs(desc, (("q", q), ("k", k), ("v", v), ("o", o), ("dout", dout)), None, key_mask, lse)
     ws = _workspace(vc_temporalattn_bwd_workspace_bytes(desc), q.device) if ws is None else ws
     dq, dk, dv = (torch.empty_like(q) for _ in range(3))
     vc_temporalattn_bwd(desc, q, k, v, o, lse, dout, key_mask, dq, dk, dv, ws, ws.numel())

@@ -32,7 +32,7 @@ def test_exports_every_declared_function(lib):
 
 
 def test_version_and_strings(lib):
-    assert vc.vc_jointattn_abi_version() == 6
+    assert vc.vc_jointattn_abi_version() == vc.ABI_VERSION
     for code in vc.STATUS:
         assert isinstance(vc.vc_status_string(code), str) and vc.vc_status_string(code)
     assert vc.vc_status_string(12345) == "unknown status"
@@ -205,3 +205,70 @@ def test_offload_argument_errors(lib):
         h = ctypes.c_void_p(123)
         assert lib.vc_offload_create(ctypes.byref(h)) == -6
         assert h.value is None
+
+
+def _header_define(name):
+    import re
+    with open(vc.HEADER) as f:
+        m = re.search(r"#define\s+%s\s+(.+)" % name, f.read())
+    return m.group(1).strip()
+
+
+def test_binding_constants_match_header():
+    assert int(_header_define("VC_JOINTATTN_ABI_VERSION")) == vc.ABI_VERSION
+
+
+def test_binding_refuses_other_abi_version(tmp_path, monkeypatch):
+    """A library reporting another ABI version is refused before any other symbol is bound
+    (a binding passing a newer argument list to an older entry point would hand it a device
+    pointer where it expects the stream)."""
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc") or shutil.which("cc")
+    if gcc is None:
+        pytest.skip("no host C compiler")
+    src = tmp_path / "old.c"
+    src.write_text("int vc_jointattn_abi_version(void) { return %d; }\n" % (vc.ABI_VERSION - 1))
+    so = tmp_path / "libold.so"
+    subprocess.run([gcc, "-shared", "-fPIC", str(src), "-o", str(so)], check=True)
+    monkeypatch.setattr(vc, "_LIB", None)
+    monkeypatch.setattr(vc, "LIB_PATH", str(so))
+    with pytest.raises(RuntimeError, match="C ABI version %d, this binding version %d"
+                       % (vc.ABI_VERSION - 1, vc.ABI_VERSION)):
+        vc.vc_jointattn_tokens(good_desc())
+    assert vc._LIB is None
+
+
+def test_binding_validates_before_calling():
+    """fwd()/bwd() check the tensors against each other and the descriptor before the
+    library sees them: a descriptor larger than the tensors, a wrong dtype for text_len or
+    key_mask, or a wrong LSE shape raise ValueError; shapes are checked before placement."""
+    torch = pytest.importorskip("torch")
+    B, N, H, D = 1, 16 + 2 * 64, 2, 64
+    t = lambda: torch.zeros((B, N, H, D), dtype=torch.bfloat16)  # noqa: E731
+    q, k, v, o, do = t(), t(), t(), t(), t()
+    lse = torch.zeros((B, H, N), dtype=torch.float32)
+    d = good_desc()
+    big = good_desc(frames=3)
+    with pytest.raises(ValueError, match="descriptor gives N"):
+        vc.bwd(q, k, v, o, lse, do, big)
+    with pytest.raises(ValueError, match="descriptor gives N"):
+        vc.fwd(q, k, v, big)
+    with pytest.raises(ValueError, match="descriptor gives B=1, H=3"):
+        vc.bwd(q, k, v, o, lse, do, good_desc(heads=3))
+    with pytest.raises(ValueError, match="text_len must be torch.int32"):
+        vc.bwd(q, k, v, o, lse, do, d, text_len=torch.zeros(B, dtype=torch.int64))
+    with pytest.raises(ValueError, match="key_mask has shape"):
+        vc.bwd(q, k, v, o, lse, do, d, key_mask=torch.zeros((B, N + 1), dtype=torch.uint8))
+    with pytest.raises(ValueError, match="lse has shape"):
+        vc.bwd(q, k, v, o, lse[:, :, :-1], do, d)
+    with pytest.raises(ValueError, match="dout must be torch.bfloat16"):
+        vc.bwd(q, k, v, o, lse, do.float(), d)
+    with pytest.raises(ValueError, match="must be on a GPU"):
+        vc.bwd(q, k, v, o, lse, do, d)
+    with pytest.raises(ValueError, match="descriptor gives N"):
+        vc.spatial_bwd(q, k, v, o, lse, do, big)
+    with pytest.raises(ValueError, match="text_len must be torch.int32"):
+        vc.spatial_fwd(q, k, v, d, text_len=torch.zeros(B, dtype=torch.int64))
+    with pytest.raises(ValueError, match="descriptor gives N"):
+        vc.temporal_bwd(q, k, v, o, lse, do, big)

@@ -126,6 +126,32 @@ def test_against_torch_sdpa(case):
     np.testing.assert_allclose(lse, torch.logsumexp(s, dim=-1).numpy(), rtol=1e-12)
 
 
+@pytest.mark.parametrize("head_dim", [4, 64, 128])
+def test_default_scale_against_torch_sdpa_default(head_dim):
+    """The oracle's default scale (scale=None) against torch SDPA's own default (no scale
+    argument: 1/sqrt of the query's last dimension), so that a wrong default in the oracle
+    cannot go unnoticed; the GPU parity tests run the library with its default scale
+    (descriptor softmax_scale = 0) against this oracle default."""
+    torch = pytest.importorskip("torch")
+    B, N, H, D, T = 1, 10, 2, head_dim, 3
+    q, k, v, do = (rnd((B, N, H, D), 90 + i) for i in range(4))
+    valid = ora.key_validity(B, N, T, np.array([2]))
+    o, lse = ora.attention_forward(q, k, v, valid, None, threads=1)
+    dq, dk, dv = ora.attention_backward(q, k, v, do, valid, None, threads=1)
+    tq, tk, tv = (torch.tensor(a.transpose(0, 2, 1, 3), dtype=torch.float64, requires_grad=True)
+                  for a in (q, k, v))
+    mask = torch.tensor(valid)[:, None, None, :]
+    to = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv, attn_mask=mask)
+    to.backward(torch.tensor(do.transpose(0, 2, 1, 3)))
+    np.testing.assert_allclose(o, to.detach().numpy().transpose(0, 2, 1, 3), rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(dq, tq.grad.numpy().transpose(0, 2, 1, 3), rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dk, tk.grad.numpy().transpose(0, 2, 1, 3), rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dv, tv.grad.numpy().transpose(0, 2, 1, 3), rtol=1e-10, atol=1e-12)
+    # a different scale gives a different result, so the comparison above has power
+    o2, _ = ora.attention_forward(q, k, v, valid, 1.1 / math.sqrt(D), threads=1)
+    assert np.abs(o2 - o).max() > 1e-6
+
+
 # --------------------------------------------------------------------------
 # Invariants of exact attention.
 # --------------------------------------------------------------------------

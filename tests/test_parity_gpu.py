@@ -84,10 +84,16 @@ def test_split_tail_of_last_round(det):
     """Joint kernels split the items of their last, partial round of workgroups over several
     workgroups (fp32 partials merged or summed afterwards). 9 heads x 30 blocks of 256 rows
     = 270 items: on 256 compute units the last 14 items (blocks 16-29 of head 8) are split
-    into 18 chunks each. Head 8 (and head 0, unsplit) on every element, with ragged text and a
-    key mask so that split items hold masked keys too."""
-    w = W.custom(1, 9, 64, 100, 4, 43, 43, name="tail", ragged_text=True)
+    into 17 chunks of 7 query (key) tiles each. head_dim 128, so that the two ids run different backwards: the
+    fused one (key blocks 0-19 add their dQ share with atomics, 4 of them inside the split
+    tail; the dQ pass covers blocks 20-29) and the deterministic one (separate dK/dV pass,
+    dQ pass over every key). Head 8 (and head 0, unsplit) on every element, with ragged
+    text and a key mask so that split items hold masked keys too."""
+    import paper_2501_08453_amd as vc
+    w = W.custom(1, 9, 128, 100, 4, 43, 43, name="tail", ragged_text=True)
     assert (w.tokens + 255) // 256 == 30
+    fused_keys = vc.vc_jointattn_fused_dq_keys(vc.desc_for(w))
+    assert fused_keys == 20 * 256, fused_keys
     x = W.make_inputs(w, seed=71)
     km = W.random_key_mask(w, seed=72, keep=0.9)
     log("split tail: 270 items of 256 rows", w.shape, "deterministic" if det else "fused")
@@ -168,22 +174,29 @@ def test_ragged_workload_sampled_heads():
     _full_compare(w, x, heads=[0, 15], samples=[0, 1, 2, 3])
 
 
-def _sampled_large(wid, heads, n_rows, with_cols):
+def _sampled_large(wid, heads, n_rows, with_cols, det=False):
+    """Workload `wid` through the C ABI (fused backward, or det: the deterministic one),
+    against the oracle on sampled query rows (O, LSE, dQ) and, with_cols, the same
+    positions as key columns (dK, dV) of the given heads. The sample holds n_rows random
+    rows, 16 random rows among the last 48 blocks of 256 rows (they hold the items of the
+    last, split round of dispatch at these sizes, all of the last head) and the text
+    boundary and ends."""
     import torch
     vc = _vc()
     w = W.WORKLOADS[wid]
-    log("workload", wid, "generating inputs", w.shape)
+    log("workload", wid, "generating inputs", w.shape, "deterministic" if det else "fused")
     x = W.make_inputs(w)
     g = _inputs_on_gpu(x)
     del x
-    desc = vc.desc_for(w)
+    desc = vc.desc_for(w, deterministic=det)
     out = run_gpu(desc, g["q"], g["k"], g["v"], g["do"], g["text_len"], None, host=False)
     log("workload", wid, "GPU done")
     B, N, H, D = w.shape
     c = ora.default_scale(D)
     valid = ora.key_validity(B, N, w.text_slot, None)
     rng = np.random.Generator(np.random.PCG64(2024 + wid))
-    rows = np.unique(np.r_[0, 1, w.text_slot - 1, w.text_slot, N - 1, rng.integers(0, N, n_rows)])
+    rows = np.unique(np.r_[0, 1, w.text_slot - 1, w.text_slot, N - 1, rng.integers(0, N, n_rows),
+                           rng.integers(max(0, N - 48 * 256), N, 16)])
     rows_t = torch.from_numpy(rows).to("cuda")
     res = {n: [] for n in ("o", "lse", "dq", "dk", "dv")}
     ref = {n: [] for n in res}
@@ -222,9 +235,17 @@ def test_long_workload_sampled():
     _sampled_large(3, heads=[0, 23], n_rows=48, with_cols=True)
 
 
+def test_long_workload_sampled_deterministic():
+    """Workload 3 with the deterministic backward (separate dK/dV pass with token-major Q and
+    dO copies, dQ pass over every key, both with their split last round and tail sums):
+    rows and columns of heads 0 and 23."""
+    _sampled_large(3, heads=[0, 23], n_rows=48, with_cols=True, det=True)
+
+
 def test_max_workload_sampled():
-    """Workload 5 (123,136 tokens): query rows of heads 0 and 23, identities on all heads."""
-    _sampled_large(5, heads=[0, 23], n_rows=48, with_cols=False)
+    """Workload 5 (123,136 tokens): rows and columns of heads 0 and 23, identities on all
+    heads."""
+    _sampled_large(5, heads=[0, 23], n_rows=48, with_cols=True)
 
 
 @pytest.mark.parametrize("det", MODES, ids=MODE_IDS)
