@@ -8,12 +8,13 @@ import numpy as np
 
 # Bar for bf16 inputs, per output tensor (O, LSE, dQ, dK, dV):
 #   max |gpu - ref| <= 2e-2  and  sum |gpu - ref| / sum |ref| <= 5e-3.
-# bf16 outputs (O, dQ, dK, dV): where half a bf16 spacing at max |ref| exceeds
-# 2e-2 (max |ref| >= 8, only in degenerate edge cases such as dV = sum of all dO
-# rows when a single key is valid), 2e-2 is below what a correctly rounded bf16
-# result can meet; there the max-abs bound is one bf16 spacing at max |ref| (the
-# output rounding plus as much again for the fp32 sums). fp32 outputs (LSE) keep
-# an absolute bound, the tighter of 2e-2 and lse_bound(N).
+# bf16 outputs (O, dQ, dK, dV): where one bf16 spacing at max |ref| exceeds 2e-2
+# (max |ref| >= 4: outputs of the five joint workloads stay below 1; the temporal
+# branch, whose queries have only F keys, reaches about 5), an absolute 2e-2 is less
+# than a bf16 result resolves there: the output's own rounding is up to half a
+# spacing, and the bf16 operands of the products (P, dS, relative 2^-8) add about as
+# much again. There the max-abs bound is one bf16 spacing at max |ref|. fp32 outputs
+# (LSE) keep an absolute bound, the tighter of 2e-2 and lse_bound(N).
 MAX_ABS = 2e-2
 MEAN_REL = 5e-3
 
@@ -87,7 +88,7 @@ def assert_close(name: str, gpu, ref, max_abs=MAX_ABS, mean_rel=MEAN_REL, kind=N
         bound = min(max_abs, lse_bound(2 ** 17 if n_keys is None else int(n_keys)))
     else:
         sp = bf16_spacing(m["ref_max"])
-        bound = sp if sp / 2 > max_abs else max_abs
+        bound = sp if sp > max_abs else max_abs
     assert m["max_abs"] <= bound, "%s max_abs %.3e > %.2e" % (name, m["max_abs"], bound)
     assert m["mean_rel"] <= mean_rel, "%s mean_rel %.3e > %.1e" % (name, m["mean_rel"], mean_rel)
     return m

@@ -63,17 +63,19 @@ def test_lse_bound_is_nearly_reached():
 
 
 def test_bf16_bar_grows_only_past_representability():
-    """Below magnitude 8 the bf16 max-abs bar is the stated 2e-2; above it, one bf16
-    spacing (half a spacing there already exceeds 2e-2)."""
-    ref = np.array([0.5, -7.9])
-    assert_close("o", ref + 0.019, ref)
+    """Below magnitude 4 the bf16 max-abs bar is the stated 2e-2; from 4 on, one bf16
+    spacing (0.03125 in [4, 8), 0.0625 in [8, 16)), as 2e-2 is then less than a spacing."""
+    ref = np.array([0.5, -3.9] + [1.0] * 98)
+    assert bf16_spacing(3.9) < MAX_ABS
+    assert_close("o", ref + np.r_[0.0, 0.019, np.zeros(98)], ref)
     with pytest.raises(AssertionError):
-        assert_close("o", ref + np.array([0.0, 0.021]), ref)
-    ref = np.array([9.0] + [1.0] * 99)
-    assert bf16_spacing(9.0) / 2 > MAX_ABS
-    assert_close("dv", ref + np.r_[bf16_spacing(9.0) * 0.99, np.zeros(99)], ref)
-    with pytest.raises(AssertionError):
-        assert_close("dv", ref + np.r_[bf16_spacing(9.0) * 1.01, np.zeros(99)], ref)
+        assert_close("o", ref + np.r_[0.0, 0.021, np.zeros(98)], ref)
+    for top in (5.0, 9.0):
+        ref = np.array([top] + [1.0] * 99)
+        assert bf16_spacing(top) > MAX_ABS
+        assert_close("dv", ref + np.r_[bf16_spacing(top) * 0.99, np.zeros(99)], ref)
+        with pytest.raises(AssertionError):
+            assert_close("dv", ref + np.r_[bf16_spacing(top) * 1.01, np.zeros(99)], ref)
 
 
 def test_lse_bar_is_absolute():
