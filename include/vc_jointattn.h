@@ -37,7 +37,8 @@
  *  - lse: fp32 [B, H, N], device memory, 16-byte aligned.
  *  - text_len: device int32 [B] or NULL (NULL means every text token is real).
  *  - key_mask: device uint8 [B, N] or NULL (NULL means no extra mask).
- *  - All memory is owned by the caller, workspaces included. The library never
+ *  - All memory is owned by the caller, workspaces included (except the fixed
+ *    scratch array of vc_jointattn_fwd_noalloc). The library never
  *    allocates, frees or synchronises, keeps no per-call state, and only launches kernels on
  *    `stream` (a hipStream_t; NULL = the null stream). Outputs are
  *    overwritten, never accumulated into, and must not alias inputs.
@@ -45,7 +46,8 @@
  *    Faults inside kernels surface at the caller's next synchronisation with
  *    the stream, as for any HIP kernel.
  *  - Thread-safe: the only shared state is a per-device property cache filled
- *    once.
+ *    once (and the per-device scratch array of vc_jointattn_fwd_noalloc, whose
+ *    concurrent calls on one device race).
  */
 #ifndef VC_JOINTATTN_H
 #define VC_JOINTATTN_H
@@ -57,7 +59,9 @@
 extern "C" {
 #endif
 
-#define VC_JOINTATTN_ABI_VERSION 6
+/* Raised with every change of a signature, a struct or the meaning of an argument; the
+ * Python binding refuses a library that reports another version. */
+#define VC_JOINTATTN_ABI_VERSION 7
 
 typedef enum vc_status {
   VC_OK = 0,
@@ -69,7 +73,9 @@ typedef enum vc_status {
   VC_ERR_DEVICE = -6,      /* no current HIP device, or it is not gfx950       */
   VC_ERR_HIP = -7,         /* a HIP launch reported an error                   */
   VC_ERR_UNSUPPORTED = -8, /* a requested mode is not available                */
-  VC_ERR_ALIAS = -9        /* an output is the same buffer as another output   */
+  VC_ERR_ALIAS = -9,       /* an output is the same buffer as another output   */
+  VC_ERR_SCRATCH = -10     /* the problem needs more scratch than the library's
+                              fixed device array holds (no-allocation entry point) */
 } vc_status;
 
 /* Problem descriptor (passed by pointer, read only during the call). */
@@ -116,6 +122,29 @@ vc_status vc_jointattn_fwd(const vc_jointattn_desc* desc,
                            const int32_t* text_len, const uint8_t* key_mask,
                            void* o, float* lse,
                            void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Forward without caller workspace, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): as vc_jointattn_fwd, with the workspace taken from a file-scope device
+ * array of VC_JOINTATTN_NOALLOC_SCRATCH_BYTES inside the library, one per device,
+ * held from the library's first use on that device until the process ends. The
+ * call itself allocates and frees nothing; on its first call on a device it looks
+ * up that device's copy of the array (with that device current) and keeps the
+ * address. Problems whose vc_jointattn_fwd_workspace_bytes exceed the array return
+ * VC_ERR_SCRATCH before anything is launched (256 MiB holds, at head_dim 128, up to
+ * about 8.1e5 (sample, head, token) rows, e.g. 3 heads of 271k tokens; at head_dim 64
+ * about 1.7e6). Every call on one device uses the same array: calls that overlap on a
+ * device (other streams, other threads) race and must be serialised by the caller.
+ * Nothing in the array needs clearing between calls: every byte read is written
+ * first by the same call. Results are bitwise those of vc_jointattn_fwd.
+ * ------------------------------------------------------------------------- */
+#define VC_JOINTATTN_NOALLOC_SCRATCH_BYTES ((size_t)256 << 20)
+
+vc_status vc_jointattn_fwd_noalloc(const vc_jointattn_desc* desc,
+                                   const void* q, const void* k, const void* v,
+                                   const int32_t* text_len, const uint8_t* key_mask,
+                                   void* o, float* lse, void* stream);
 
 /* Bytes of device workspace the backward needs: per query row fp32 -D and
  * LSE*log2(e) ([B,H,Npad], Npad = N rounded up to 64), token-major copies of

@@ -18,13 +18,15 @@ HEADER = os.path.join(os.path.dirname(PKG_DIR), "include", "vc_jointattn.h")
 # The ABI the signatures below describe (VC_JOINTATTN_ABI_VERSION of include/vc_jointattn.h);
 # a library reporting another version is refused, so that no call can reach an entry point
 # whose arguments differ from what this binding passes.
-ABI_VERSION = 6
+ABI_VERSION = 7
+# Bytes of the no-allocation forward's fixed scratch array (VC_JOINTATTN_NOALLOC_SCRATCH_BYTES).
+NOALLOC_SCRATCH_BYTES = 256 << 20
 
 VC_OK = 0
 STATUS = {
     0: "VC_OK", -1: "VC_ERR_NULL", -2: "VC_ERR_SHAPE", -3: "VC_ERR_HEAD_DIM", -4: "VC_ERR_ALIGN",
     -5: "VC_ERR_WORKSPACE", -6: "VC_ERR_DEVICE", -7: "VC_ERR_HIP", -8: "VC_ERR_UNSUPPORTED",
-    -9: "VC_ERR_ALIAS",
+    -9: "VC_ERR_ALIAS", -10: "VC_ERR_SCRATCH",
 }
 
 
@@ -58,6 +60,7 @@ _SIGS = {
     "vc_jointattn_tokens": (ctypes.c_int64, [_DP]),
     "vc_jointattn_fwd_workspace_bytes": (ctypes.c_size_t, [_DP]),
     "vc_jointattn_fwd": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "vc_jointattn_fwd_noalloc": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P]),
     "vc_jointattn_bwd_workspace_bytes": (ctypes.c_size_t, [_DP]),
     "vc_jointattn_bwd": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "vc_jointattn_bwd_prepare": (ctypes.c_int, [_DP, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
@@ -174,6 +177,11 @@ def vc_jointattn_bwd_workspace_bytes(desc) -> int:
 def vc_jointattn_fwd(desc, q, k, v, text_len, key_mask, o, lse, workspace, workspace_bytes, stream=None):
     _call("vc_jointattn_fwd", ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(text_len), _ptr(key_mask),
           _ptr(o), _ptr(lse), _ptr(workspace), int(workspace_bytes), _stream(stream))
+
+
+def vc_jointattn_fwd_noalloc(desc, q, k, v, text_len, key_mask, o, lse, stream=None):
+    _call("vc_jointattn_fwd_noalloc", ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(text_len),
+          _ptr(key_mask), _ptr(o), _ptr(lse), _stream(stream))
 
 
 def vc_jointattn_bwd(desc, q, k, v, o, lse, dout, text_len, key_mask, dq, dk, dv, workspace, workspace_bytes,

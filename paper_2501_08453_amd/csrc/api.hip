@@ -35,6 +35,31 @@ vc_status check_device() {
   return di.is_gfx950 ? VC_OK : VC_ERR_DEVICE;
 }
 
+// Workspace of vc_jointattn_fwd_noalloc: a file-scope device array (each device holds its
+// own copy from the library's first use on it until the process ends). In host code
+// `scratch` names a host-side stand-in, not device memory: kernels and copies take the
+// device address looked up below, never the array's name.
+static __device__ __align__(256) char scratch[VC_JOINTATTN_NOALLOC_SCRATCH_BYTES];
+
+struct ScratchAddr {
+  std::once_flag once;
+  void* ptr = nullptr;
+};
+ScratchAddr g_scratch[kMaxDevices];
+
+// Device address of this device's copy of `scratch`, looked up once per device with that
+// device current (the caller has checked it with check_device); NULL if the lookup failed.
+void* scratch_ptr() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  ScratchAddr& sa = g_scratch[dev];
+  std::call_once(sa.once, [&] {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) == hipSuccess) sa.ptr = p;
+  });
+  return sa.ptr;
+}
+
 // Compute units of the current device (after check_device succeeded).
 int device_cus() {
   int dev = 0;
@@ -231,6 +256,8 @@ const char* vc_status_string(int status) {
     case VC_ERR_HIP: return "a HIP kernel launch failed";
     case VC_ERR_UNSUPPORTED: return "requested mode is not available";
     case VC_ERR_ALIAS: return "an output is the same buffer as another output";
+    case VC_ERR_SCRATCH:
+      return "the problem needs more workspace than the no-allocation entry point's fixed scratch array holds";
     default: return "unknown status";
   }
 }
@@ -324,6 +351,20 @@ vc_status vc_jointattn_fwd(const vc_jointattn_desc* desc, const void* q, const v
                            const int32_t* text_len, const uint8_t* key_mask, void* o, float* lse, void* workspace,
                            size_t workspace_bytes, void* stream) {
   return fwd_impl(desc, q, k, v, text_len, key_mask, o, lse, workspace, workspace_bytes, stream, false);
+}
+
+vc_status vc_jointattn_fwd_noalloc(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
+                                   const int32_t* text_len, const uint8_t* key_mask, void* o, float* lse,
+                                   void* stream) {
+  int64_t n = 0;
+  vc_status st = check_desc(desc, &n);
+  if (st != VC_OK) return st;
+  if (fwd_ws_bytes(desc, n) > VC_JOINTATTN_NOALLOC_SCRATCH_BYTES) return VC_ERR_SCRATCH;
+  if ((st = check_device()) != VC_OK) return st;
+  void* ws = scratch_ptr();
+  if (!ws) return VC_ERR_HIP;
+  return fwd_impl(desc, q, k, v, text_len, key_mask, o, lse, ws, VC_JOINTATTN_NOALLOC_SCRATCH_BYTES, stream,
+                  false);
 }
 
 vc_status vc_spatialattn_fwd(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,

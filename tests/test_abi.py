@@ -216,6 +216,8 @@ def _header_define(name):
 
 def test_binding_constants_match_header():
     assert int(_header_define("VC_JOINTATTN_ABI_VERSION")) == vc.ABI_VERSION
+    assert _header_define("VC_JOINTATTN_NOALLOC_SCRATCH_BYTES") == "((size_t)256 << 20)"
+    assert vc.NOALLOC_SCRATCH_BYTES == 256 << 20
 
 
 def test_binding_refuses_other_abi_version(tmp_path, monkeypatch):
@@ -237,6 +239,26 @@ def test_binding_refuses_other_abi_version(tmp_path, monkeypatch):
                        % (vc.ABI_VERSION - 1, vc.ABI_VERSION)):
         vc.vc_jointattn_tokens(good_desc())
     assert vc._LIB is None
+
+
+def test_noalloc_forward_argument_errors(lib):
+    """The no-allocation forward validates the descriptor, then refuses problems whose
+    workspace exceeds its fixed scratch array (before touching a device), then checks the
+    device and the pointers."""
+    p = 1 << 20
+    assert lib.vc_jointattn_fwd_noalloc(None, p, p, p, None, None, p, p, None) == -1
+    assert lib.vc_jointattn_fwd_noalloc(ctypes.byref(good_desc(head_dim=96)), p, p, p, None, None, p, p,
+                                        None) == -3
+    long720p = vc.make_desc(1, 24, 128, 256, 16, 45, 80)  # 400 MB of V^T tiles
+    assert vc.vc_jointattn_fwd_workspace_bytes(long720p) > vc.NOALLOC_SCRATCH_BYTES
+    assert lib.vc_jointattn_fwd_noalloc(ctypes.byref(long720p), p, p, p, None, None, p, p, None) == -10
+    assert "no-allocation" in vc.vc_status_string(-10)
+    # one GPU's share of it under 8-way head sharding (3 heads) fits
+    share = vc.make_desc(1, 3, 128, 256, 16, 45, 80)
+    assert vc.vc_jointattn_fwd_workspace_bytes(share) <= vc.NOALLOC_SCRATCH_BYTES
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        assert lib.vc_jointattn_fwd_noalloc(ctypes.byref(share), p, p, p, None, None, p, p, None) == -6
 
 
 def test_binding_validates_before_calling():
