@@ -71,13 +71,13 @@ def spatial_flops(w, text_len):
 
 def temporal_bytes(w):
     """Forward, backward algorithmic HBM bytes of the temporal branch (bf16 tensors of the
-    video rows, fp32 LSE and D): forward reads q, k, v and writes o, lse; backward reads
-    q, k, v, o, dO, lse and writes dq, dk, dv (D kept on chip would save its round trip;
-    it is counted once as written and once as read)."""
+    video rows, fp32 LSE): the least the step must move. Forward reads q, k, v and writes
+    o, lse; backward reads q, k, v, o, dO, lse and writes dq, dk, dv (D = rowsum(dO o O)
+    needs no bytes of its own: o and dO are read anyway)."""
     rows = w.batch * w.frames * w.grid_h * w.grid_w * w.heads
     t = rows * w.head_dim * 2.0
     r = rows * 4.0
-    return 3 * t + t + r, 5 * t + r + 3 * t + 2 * r
+    return 3 * t + t + r, 5 * t + r + 3 * t
 
 
 def cpu_baseline_branch(kind, w, g, text_len, target_s):
@@ -171,9 +171,15 @@ def cpu_baseline(w, g, text_len, target_s):
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_bwd_dkdv_long720p.json")
 KERNEL_SOURCES = ["paper_2501_08453_amd/csrc/bwd.hip", "paper_2501_08453_amd/csrc/common.hpp"]
-TEMPORAL_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_temporal_bwd_long720p.json")
-TEMPORAL_SOURCES = ["paper_2501_08453_amd/csrc/temporal.hip", "paper_2501_08453_amd/csrc/bwd.hip",
-                    "paper_2501_08453_amd/csrc/common.hpp"]
+# Traffic records of the temporal backward, per workload: the short-clip kernel (with its
+# preparation pass) at the long workload, the long-clip kernel at the 144-frame clip.
+TEMPORAL_TRAFFIC = {
+    3: (os.path.join(ROOT, "profiles", "traffic_temporal_bwd_long720p.json"),
+        ["paper_2501_08453_amd/csrc/temporal.hip", "paper_2501_08453_amd/csrc/bwd.hip",
+         "paper_2501_08453_amd/csrc/common.hpp"]),
+    6: (os.path.join(ROOT, "profiles", "traffic_temporal_bwd_clip144f.json"),
+        ["paper_2501_08453_amd/csrc/temporal_long.hip", "paper_2501_08453_amd/csrc/common.hpp"]),
+}
 
 
 def code_only(text: str) -> str:
@@ -216,7 +222,8 @@ def main(argv=None):
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", type=int, default=W.HEADLINE, choices=sorted(W.WORKLOADS))
+    ap.add_argument("--workload", type=int, default=W.HEADLINE, choices=sorted(W.WORKLOADS) + sorted(W.EXTRA),
+                    help="1-5: the five configurations; 6: a 144-frame clip (branch measurements)")
     ap.add_argument("--branch", default="joint", choices=["joint", "spatial", "temporal", "block"],
                     help="attention branch to measure (joint = the headline; block = all three and their sum)")
     ap.add_argument("--layers", type=int, default=4, help="stacked layers for --branch block")
@@ -237,14 +244,18 @@ def main(argv=None):
     import torch
     import paper_2501_08453_amd as vc
 
-    w = W.WORKLOADS[args.workload]
-    x = W.make_inputs(w)
+    w = W.get(args.workload)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    g = {n: torch.from_numpy(x[n]).to(dev).to(torch.bfloat16).contiguous() for n in ("q", "k", "v", "do")}
-    text_len = x["text_len"]
+    if args.workload in W.EXTRA:
+        g = W.make_inputs_device(w, device=dev)
+        text_len = g.pop("text_len")
+    else:
+        x = W.make_inputs(w)
+        g = {n: torch.from_numpy(x[n]).to(dev).to(torch.bfloat16).contiguous() for n in ("q", "k", "v", "do")}
+        text_len = x["text_len"]
+        del x
     tl = None if text_len is None else torch.from_numpy(text_len).to(dev)
-    del x
     desc = vc.desc_for(w, deterministic=args.deterministic)
     # The joint backward bench.py times is the one vc_jointattn_bwd runs by default: fused,
     # unless the fused pass would carry no keys (head_dim 64), then the separate passes.
@@ -255,15 +266,17 @@ def main(argv=None):
     o = torch.empty_like(g["q"])
     lse = torch.empty((B, H, N), dtype=torch.float32, device=dev)
     dq, dk, dv = (torch.empty_like(g["q"]) for _ in range(3))
-    fws = vc.fwd_workspace(desc, dev)
-    ws = vc.spatial_workspace(desc, dev) if args.branch == "spatial" else vc.workspace(desc, dev)
-    fwsb, wsb = fws.numel(), ws.numel()
-    q, k, v, do = g["q"], g["k"], g["v"], g["do"]
     stream = torch.cuda.current_stream()
     sh = stream.cuda_stream
+    q, k, v, do = g["q"], g["k"], g["v"], g["do"]
+    if args.branch == "temporal":  # no joint workspaces
+        return branch_main(args, w, g, text_len, tl, desc, o, lse, dq, dk, dv, None, None, stream)
+    fws = vc.fwd_workspace(desc, dev)
     if args.branch == "block":
-        del o, lse, dq, dk, dv, ws
+        del o, lse, dq, dk, dv
         return block_main(args, w, g, text_len, tl, desc, fws, stream)
+    ws = vc.spatial_workspace(desc, dev) if args.branch == "spatial" else vc.workspace(desc, dev)
+    fwsb, wsb = fws.numel(), ws.numel()
     if args.branch != "joint":
         return branch_main(args, w, g, text_len, tl, desc, o, lse, dq, dk, dv, fws, ws, stream)
 
@@ -444,7 +457,8 @@ def branch_main(args, w, g, text_len, tl, desc, o, lse, dq, dk, dv, fws, ws, str
                      "frac": round(bwd_rate / peak, 4), "traffic": None,
                      "algorithmic_per_launch": a_bwd},
     }
-    tr = traffic_record(TEMPORAL_TRAFFIC_FILE, TEMPORAL_SOURCES) if args.branch == "temporal" else None
+    tr = (traffic_record(*TEMPORAL_TRAFFIC[args.workload])
+          if args.branch == "temporal" and args.workload in TEMPORAL_TRAFFIC else None)
     if tr is not None:
         line["roofline"]["traffic"] = tr
     if not args.no_cpu_baseline:

@@ -273,8 +273,10 @@ vc_status vc_spatialattn_bwd(const vc_jointattn_desc* desc,
  * f' = 0..F-1, with key_mask (NULL = none) applied to those keys; a query with
  * no valid key gets O = 0, LSE = -inf. Text rows take no part: their o, dq, dk,
  * dv are written as 0 and their lse as -inf. text_len is not used. Requires
- * F <= 32 (VC_ERR_SHAPE otherwise). Tensor conventions as above; results are
- * deterministic and no atomics are used.
+ * F <= 144 (VC_ERR_SHAPE otherwise; the paper's longest clip has 144 frames,
+ * Sec. VI-D): up to 32 frames one matrix-core block packs several positions,
+ * beyond that a workgroup takes one position at a time, frames in blocks of 32.
+ * Tensor conventions as above; results are deterministic and no atomics are used.
  * ------------------------------------------------------------------------- */
 
 /* Temporal forward: writes o [B,N,H,D] bf16 and lse [B,H,N] fp32 (natural log).
@@ -297,7 +299,9 @@ vc_status vc_temporalattn_fwd_sum(const vc_jointattn_desc* desc,
                                   void* o, float* lse, void* out, void* stream);
 
 /* Bytes of device workspace the temporal backward needs: per row fp32 -D and
- * LSE*log2(e) ([B,H,Npad]). 0 for an invalid descriptor. Host only. */
+ * LSE*log2(e) ([B,H,Npad]). 0 for an invalid descriptor. Host only. With F > 32
+ * the backward forms both inside its kernel and neither reads nor checks the
+ * workspace (it may be NULL). */
 size_t vc_temporalattn_bwd_workspace_bytes(const vc_jointattn_desc* desc);
 
 /* Temporal backward: dq, dk, dv from q, k, v, the temporal forward's o and lse

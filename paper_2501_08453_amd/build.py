@@ -10,7 +10,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libvc_jointattn.so")
-SOURCES = ["api.hip", "layout.hip", "fwd.hip", "bwd.hip", "temporal.hip", "offload.hip"]
+SOURCES = ["api.hip", "layout.hip", "fwd.hip", "bwd.hip", "temporal.hip", "temporal_long.hip", "offload.hip"]
 HEADERS = ["common.hpp"]
 
 HIPCC_FLAGS = [

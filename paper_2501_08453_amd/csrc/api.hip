@@ -219,8 +219,6 @@ vc_status check_ws(void* ws, size_t have, size_t need) {
 
 inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
-constexpr int kMaxTemporalFrames = 32;
-
 // Temporal branch arguments common to the forward and the backward.
 vcja::TemporalArgs temporal_args(const vc_jointattn_desc* d, int64_t n) {
   vcja::TemporalArgs a{};
@@ -230,7 +228,7 @@ vcja::TemporalArgs temporal_args(const vc_jointattn_desc* d, int64_t n) {
   a.T = d->text_slot;
   a.F = d->frames;
   a.L = d->grid_h * d->grid_w;
-  a.G = 32 / d->frames;
+  a.G = d->frames <= vcja::kMaxTemporalFramesShort ? 32 / d->frames : 1;
   a.npad = ntiles(n) * vcja::kTileTok;
   a.scale = d->softmax_scale > 0.0f ? d->softmax_scale : 1.0f / sqrtf((float)d->head_dim);
   a.scale_log2 = a.scale * vcja::kLog2e;
@@ -587,7 +585,7 @@ vc_status temporal_fwd_impl(const vc_jointattn_desc* desc, const void* q, const 
   int64_t n = 0;
   vc_status st = check_desc(desc, &n);
   if (st != VC_OK) return st;
-  if (desc->frames > kMaxTemporalFrames) return VC_ERR_SHAPE;
+  if (desc->frames > vcja::kMaxTemporalFramesLong) return VC_ERR_SHAPE;
   if (!q || !k || !v || !o || !lse) return VC_ERR_NULL;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse) || !aligned16(o_joint) ||
       !aligned16(o_spatial) || !aligned16(out))
@@ -611,8 +609,10 @@ vc_status temporal_fwd_impl(const vc_jointattn_desc* desc, const void* q, const 
   if (out && vcja::launch_branch_sum(a.sum_a, a.sum_b, nullptr, a.sum_out, a.B, a.N, a.T, a.H * desc->head_dim, s) !=
                  hipSuccess)
     return VC_ERR_HIP;
-  if (vcja::launch_temporal_fwd(a, desc->head_dim, s) != hipSuccess) return VC_ERR_HIP;
-  return VC_OK;
+  const hipError_t e = desc->frames > vcja::kMaxTemporalFramesShort
+                          ? vcja::launch_temporal_long_fwd(a, desc->head_dim, device_cus(), s)
+                          : vcja::launch_temporal_fwd(a, desc->head_dim, s);
+  return e == hipSuccess ? VC_OK : VC_ERR_HIP;
 }
 
 }  // namespace
@@ -658,31 +658,38 @@ vc_status vc_temporalattn_bwd(const vc_jointattn_desc* desc, const void* q, cons
   int64_t n = 0;
   vc_status st = check_desc(desc, &n);
   if (st != VC_OK) return st;
-  if (desc->frames > kMaxTemporalFrames) return VC_ERR_SHAPE;
+  if (desc->frames > vcja::kMaxTemporalFramesLong) return VC_ERR_SHAPE;
   if (!q || !k || !v || !o || !lse || !dout || !dq || !dk || !dv) return VC_ERR_NULL;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse) || !aligned16(dout) ||
       !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
     return VC_ERR_ALIGN;
+  const bool long_clip = desc->frames > vcja::kMaxTemporalFramesShort;
   const size_t rb = rows_bytes(desc, n);
-  if ((st = check_ws(workspace, workspace_bytes, 2 * rb)) != VC_OK) return st;
+  if (!long_clip && (st = check_ws(workspace, workspace_bytes, 2 * rb)) != VC_OK) return st;
   if ((st = check_device()) != VC_OK) return st;
   vcja::TemporalArgs a = temporal_args(desc, n);
-  float* dd = static_cast<float*>(workspace);
-  float* lse2 = reinterpret_cast<float*>(static_cast<char*>(workspace) + rb);
   a.q = bf(q);
   a.k = bf(k);
   a.v = bf(v);
   a.dout = bf(dout);
   a.key_mask = key_mask;
-  a.lse2 = lse2;
-  a.dd = dd;
   a.o = static_cast<__bf16*>(dq);
   a.dk = static_cast<__bf16*>(dk);
   a.dv = static_cast<__bf16*>(dv);
   hipStream_t s = as_stream(stream);
+  if (vcja::launch_text_rows(a.o, a.dk, a.dv, nullptr, a.B, a.H, a.N, a.T, desc->head_dim, s) != hipSuccess)
+    return VC_ERR_HIP;
+  if (long_clip) {  // -D and LSE*log2(e) are formed inside the kernel: no workspace
+    a.lse = const_cast<float*>(lse);
+    a.o_in = bf(o);
+    return vcja::launch_temporal_long_bwd(a, desc->head_dim, device_cus(), s) == hipSuccess ? VC_OK : VC_ERR_HIP;
+  }
+  float* dd = static_cast<float*>(workspace);
+  float* lse2 = reinterpret_cast<float*>(static_cast<char*>(workspace) + rb);
+  a.lse2 = lse2;
+  a.dd = dd;
   if (vcja::launch_bwd_prepare(bf(o), lse, bf(dout), dd, lse2, a.B, a.H, a.N, a.npad, desc->head_dim, s) !=
           hipSuccess ||
-      vcja::launch_text_rows(a.o, a.dk, a.dv, nullptr, a.B, a.H, a.N, a.T, desc->head_dim, s) != hipSuccess ||
       vcja::launch_temporal_bwd(a, desc->head_dim, s) != hipSuccess)
     return VC_ERR_HIP;
   return VC_OK;

@@ -378,7 +378,11 @@ struct DqArgs {
 };
 
 // Temporal branch: attention of each spatial position across the F frames. Video token
-// (f, l) sits at T + f*L + l of the joint sequence; one wave handles G = 32/F positions.
+// (f, l) sits at T + f*L + l of the joint sequence. F <= 32: one wave handles G = 32/F
+// positions; 32 < F <= kMaxTemporalFramesLong: one workgroup per position (frame blocks
+// of 32), persistent over positions.
+constexpr int kMaxTemporalFramesShort = 32;
+constexpr int kMaxTemporalFramesLong = 144;
 struct TemporalArgs {
   const __bf16* q;
   const __bf16* k;
@@ -388,7 +392,8 @@ struct TemporalArgs {
   const float* lse2;    // backward: LSE * log2(e) per token, +inf where there is none, [B, H, Npad]
   const float* dd;      // backward: -D = -rowsum(dO o O), [B, H, Npad]
   __bf16* o;            // forward output / backward dQ
-  float* lse;           // forward output
+  float* lse;           // forward output; backward of long clips: the forward's LSE (input)
+  const __bf16* o_in;   // backward of long clips: the forward's O (for D = rowsum(dO o O))
   __bf16* dk;           // backward
   __bf16* dv;           // backward
   // Forward with the branch sum fused into the epilogue (sum_out non-NULL): also writes
@@ -414,6 +419,10 @@ hipError_t launch_bwd_dkdv(const DkdvArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_bwd_dq(const DqArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_temporal_fwd(const TemporalArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_temporal_bwd(const TemporalArgs& a, int head_dim, hipStream_t s);
+// Long clips (F > 32): persistent grid of at most `cus` workgroups; the backward forms
+// -D and LSE*log2(e) itself (no lse2 / dd inputs).
+hipError_t launch_temporal_long_fwd(const TemporalArgs& a, int head_dim, int cus, hipStream_t s);
+hipError_t launch_temporal_long_bwd(const TemporalArgs& a, int head_dim, int cus, hipStream_t s);
 // out = a + b + c over rows [0, rows) of every sample of [B, N, H, D] tensors (row_elems =
 // H*D); each element summed in fp32 in that order and rounded once to bf16. A NULL input
 // counts as zero; out may be one of the inputs.

@@ -1,0 +1,449 @@
+// Temporal attention branch for long clips (33 <= F <= 144 frames) on gfx950.
+//
+// Each spatial position l of a (sample, head) attends across its F frames, the rows
+// T + f*L + l of the joint [B, N, H, D] layout (Sec. III-B regroups [B, F, L, ...] as
+// [B*L, F, ...]). Sequences this long no longer fit one 32-slot matrix-core block, so a
+// workgroup takes one position at a time and splits its frames into blocks of 32:
+// wave j owns query (or key) block j, and walks over the other side's blocks.
+//
+// The work is bound by memory traffic (about 0.25 KiB per row and head each way against
+// a few hundred flops per byte of matrix work), so the kernels are built to keep HBM
+// busy: a persistent workgroup per compute unit walks a strided sequence of positions
+// (head fastest, so that concurrent workgroups read whole token rows together) and
+// stages the rows the next step reads in LDS while the current step computes.
+//   Forward: two buffers of K | V rows; while position p is computed from one, the
+//     rows of p+1 are copied into the other.
+//   Backward: buffer A holds K | V, buffer B Q | dO. The lane-per-query half (dQ) reads
+//     A while the Q, dO rows of the same position are copied into B; the lane-per-key
+//     half (dK, dV) reads B while the K, V rows of the next position are copied into A.
+//     D_i = <dO_i, O_i> and LSE_i are formed in the dQ half (no preparation pass, no
+//     workspace) and handed to the dK/dV half through LDS.
+// Rows sit in LDS in the permuted order of the fused joint backward (frame 16g + 4m + i
+// in row 16g + 4i + m) with a 16-byte pad chunk per row, so that the transposing reads of
+// four consecutive frames hit distinct banks; reads past the last frame are clamped to it
+// (their probabilities are zero), so a position needs F rows of LDS, not 32*ceil(F/32).
+#include <algorithm>
+
+#include "common.hpp"
+
+namespace vcja {
+namespace {
+
+constexpr int kLongWaves = 8;
+constexpr int kLongMaxBlocks = (kMaxTemporalFramesLong + 31) / 32;  // frame blocks of 32
+constexpr int kLongPadRows = (kMaxTemporalFramesLong + 15) / 16 * 16;
+
+template <int D>
+struct LongLds {
+  static constexpr int CH = D / 8 + 1;   // 16-byte chunks per row, pad included
+  static constexpr int RS = CH * 16;     // row stride (bytes)
+  // 1 KiB wave copies of one tensor's rows (kLongPadRows rows), and its LDS region
+  static constexpr int COPIES = (kLongPadRows * CH + 63) / 64;
+  static constexpr int REGION = COPIES * 1024;
+  static constexpr int STATS = 2 * 32 * kLongMaxBlocks * 4;  // LSE*log2e | -D per query slot
+  static constexpr int BYTES = 4 * REGION + STATS;
+};
+
+// The lane index as a value the compiler must treat as new where it is taken: per-lane
+// addresses derived from it are then formed in each phase instead of being hoisted out of
+// the position loop and kept (or spilled) across it.
+__device__ __forceinline__ int opaque_lane() {
+  int x = threadIdx.x & 63;
+  asm volatile("" : "+v"(x));
+  return x;
+}
+
+// The rows (frames) of one position of one tensor: frame f at src + f * fstride.
+struct PosRows {
+  const __bf16* src;
+  size_t fstride;
+};
+
+// Issues this wave's share of the copies of rows [0, round_up(F, 16)) into `dst` in
+// permuted order (LDS row r holds frame perm_row(r), clamped to the last frame).
+template <int D>
+__device__ __forceinline__ void copy_rows(PosRows pr, int F, VC_LDS char* dst, int w) {
+  constexpr int CH = LongLds<D>::CH;
+  const int lane = opaque_lane();
+  const int rows = (F + 15) & ~15;
+  const int copies = (rows * CH + 63) / 64;
+  for (int idx = w; idx < copies; idx += kLongWaves) {
+    const int lin = idx * 64 + lane;
+    const int r = lin / CH;
+    const int c = min(lin - r * CH, CH - 2);
+    const int f = min(perm_row(r), F - 1);
+    copy16_to_lds_opaque(pr.src + (size_t)f * pr.fstride + c * 8, dst + idx * 1024);
+  }
+}
+
+// Byte offset in a region of the 16-byte chunk `chunk` of frame t (clamped to F-1).
+template <int D>
+__device__ __forceinline__ int row_off(int t, int F) {
+  return perm_row(min(t, F - 1)) * LongLds<D>::RS;
+}
+
+// A operand of a product whose contraction runs over frames (X^T, m = dim, k = frame):
+// dims db*32 + l32, frames 16*st + 8*(t/4) + 4*hi + t%4 (t = 0..7) of block `blk`, the
+// order an accumulator column holds them; two transposing reads of 4 frames each. Each
+// lane supplies the address of frame r0 + e (e = (lane%16)/4, clamped) and 4 dims.
+template <int D>
+__device__ __forceinline__ bf16x8 frames_operand(const VC_LDS char* region, int blk, int st, int db, int F,
+                                                 int lane) {
+  const int hi = lane >> 5;
+  const int e = (lane & 15) >> 2;
+  const int col = (db * 32 + 16 * ((lane >> 4) & 1) + 4 * (lane & 3)) * 2;
+  const int r0 = blk * 32 + 16 * st + 4 * hi + e;
+  const bf16x4 a = lds_read_tr(region + row_off<D>(r0, F) + col);
+  const bf16x4 b = lds_read_tr(region + row_off<D>(r0 + 8, F) + col);
+  return cat4(a, b);
+}
+
+// A operand of a product whose contraction runs over dims (X rows, m = frame, k = dim):
+// frame blk*32 + l32, dims 16*ks + 8*hi .. +7.
+template <int D>
+__device__ __forceinline__ bf16x8 rows_operand(const VC_LDS char* region, int blk, int ks, int F, int lane) {
+  const int l32 = lane & 31, hi = lane >> 5;
+  return *(const VC_LDS bf16x8*)(region + row_off<D>(blk * 32 + l32, F) + (2 * ks + hi) * 16);
+}
+
+// Position item i: head fastest, then spatial position, then sample.
+struct PosItem {
+  int b, l, h;
+};
+__device__ __forceinline__ PosItem pos_item(int i, int H, int L) { return PosItem{i / (H * L), (i / H) % L, i % H}; }
+
+// Key validity of the 32 frames of block `blk` of the position starting at `kbase`
+// (frame f at kbase + f*L of the sample's key_mask row), as a bit mask (wave-uniform).
+__device__ __forceinline__ unsigned key_bits(const uint8_t* km, int kbase, int L, int F, int blk, int lane) {
+  const int f = blk * 32 + (lane & 31);
+  bool ok = f < F;
+  if (km) ok = ok & (km[kbase + (size_t)min(f, F - 1) * L] != 0);
+  return (unsigned)__ballot(ok);
+}
+
+template <int D, bool SUM>
+__global__ __launch_bounds__(64 * kLongWaves, 1) void temporal_long_fwd_kernel(TemporalArgs a) {
+  using Lds = LongLds<D>;
+  __shared__ __attribute__((aligned(1024))) char smem[Lds::BYTES];
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int F = a.F, L = a.L, H = a.H;
+  const int nblk = (F + 31) / 32;
+  const size_t tok = (size_t)H * D;
+  const int items = a.B * L * H;
+  auto rows_of = [&](const __bf16* t, PosItem it) {
+    return PosRows{t + ((size_t)it.b * a.N + a.T + it.l) * tok + (size_t)it.h * D, (size_t)L * tok};
+  };
+  auto issue = [&](int i, int buf) {
+    const PosItem it = pos_item(i, H, L);
+    VC_LDS char* dst = (VC_LDS char*)smem + buf * 2 * Lds::REGION;
+    copy_rows<D>(rows_of(a.k, it), F, dst, w);
+    copy_rows<D>(rows_of(a.v, it), F, dst + Lds::REGION, w);
+  };
+
+  int buf = 0;
+  if ((int)blockIdx.x < items) issue(blockIdx.x, 0);
+  for (int i = blockIdx.x; i < items; i += gridDim.x, buf ^= 1) {
+    wait_all_memory();
+    __syncthreads();  // K, V of item i are in buffer `buf`; nobody reads the other buffer
+    if (i + (int)gridDim.x < items) issue(i + gridDim.x, buf ^ 1);
+    if (w >= nblk) continue;  // no query block for this wave
+    const PosItem it = pos_item(i, H, L);
+    const int lane = opaque_lane();
+    const int l32 = lane & 31, hi = lane >> 5;
+    const VC_LDS char* kr = (const VC_LDS char*)smem + buf * 2 * Lds::REGION;
+    const VC_LDS char* vr = kr + Lds::REGION;
+    const uint8_t* km = a.key_mask ? a.key_mask + (size_t)it.b * a.N + a.T + it.l : nullptr;
+    // This lane's query: frame q of the wave's block (past F: the last frame, not written).
+    const int q = w * 32 + l32;
+    const bool q_in = q < F;
+    const size_t qrow = ((size_t)it.b * a.N + a.T + (size_t)min(q, F - 1) * L + it.l) * tok + (size_t)it.h * D;
+    bf16x8 qf[D / 16];
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) qf[ks] = *(const bf16x8*)(a.q + qrow + 16 * ks + 8 * hi);
+    f32x16 oacc[D / 32];
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) oacc[db] = zero_f32x16();
+    float m = -INFINITY, l = 0.0f;  // base (log2 units) and this half's sum
+    for (int kb = 0; kb < nblk; ++kb) {
+      const unsigned bits = key_bits(km, 0, L, F, kb, lane);
+      if (bits == 0) continue;  // no valid key in this block (uniform)
+      f32x16 s = zero_f32x16();
+#pragma unroll
+      for (int ks = 0; ks < D / 16; ++ks) s = mfma32(rows_operand<D>(kr, kb, ks, F, lane), qf[ks], s);
+      float mx = -INFINITY;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        s[r] = ((bits >> acc_row(r, hi)) & 1u) ? s[r] * a.scale_log2 : -INFINITY;
+        mx = fmaxf(mx, s[r]);
+      }
+      const float m_new = fmaxf(m, halves_max(mx));
+      const float alpha = fast_exp2(m - m_new);  // m = -inf at the first block: 0
+      m = m_new;
+      l *= alpha;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) oacc[db] *= alpha;
+      float p[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        p[r] = fast_exp2(s[r] - m);
+        l += p[r];
+      }
+      const bf16x8 pb0 = to_bf16x8(&p[0]), pb1 = to_bf16x8(&p[8]);
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) {
+        oacc[db] = mfma32(frames_operand<D>(vr, kb, 0, db, F, lane), pb0, oacc[db]);
+        oacc[db] = mfma32(frames_operand<D>(vr, kb, 1, db, F, lane), pb1, oacc[db]);
+      }
+    }
+    const float lt = halves_sum(l);
+    const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
+    if (q_in) {
+      const size_t orow = ((size_t)it.b * a.N + a.T + (size_t)q * L + it.l) * tok + (size_t)it.h * D;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int d = db * 32 + 8 * j + 4 * hi;
+          const bf16x4 o4 = {(__bf16)(oacc[db][4 * j + 0] * inv), (__bf16)(oacc[db][4 * j + 1] * inv),
+                             (__bf16)(oacc[db][4 * j + 2] * inv), (__bf16)(oacc[db][4 * j + 3] * inv)};
+          *(bf16x4*)(a.o + orow + d) = o4;
+          if constexpr (SUM) {  // out = (o_joint + o_spatial) + o in fp32, rounded once
+            f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+            if (a.sum_a) {
+              const bf16x4 x = *(const bf16x4*)(a.sum_a + orow + d);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) acc[e] += (float)x[e];
+            }
+            if (a.sum_b) {
+              const bf16x4 x = *(const bf16x4*)(a.sum_b + orow + d);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) acc[e] += (float)x[e];
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[e] += (float)o4[e];
+            *(bf16x4*)(a.sum_out + orow + d) = bf16x4{(__bf16)acc[0], (__bf16)acc[1], (__bf16)acc[2], (__bf16)acc[3]};
+          }
+        }
+      if (hi == 0)
+        a.lse[((size_t)it.b * H + it.h) * a.N + a.T + (size_t)q * L + it.l] =
+            lt > 0.0f ? (m + __log2f(lt)) * kLn2 : -INFINITY;
+    }
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(64 * kLongWaves, 1) void temporal_long_bwd_kernel(TemporalArgs a) {
+  using Lds = LongLds<D>;
+  __shared__ __attribute__((aligned(1024))) char smem[Lds::BYTES];
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int F = a.F, L = a.L, H = a.H;
+  const int nblk = (F + 31) / 32;
+  const size_t tok = (size_t)H * D;
+  const int items = a.B * L * H;
+  VC_LDS char* const bufA = (VC_LDS char*)smem;                  // K | V
+  VC_LDS char* const bufB = (VC_LDS char*)smem + 2 * Lds::REGION;  // Q | dO
+  VC_LDS float* const lse_s = (VC_LDS float*)(smem + 4 * Lds::REGION);  // LSE*log2e per query slot
+  VC_LDS float* const nd_s = lse_s + 32 * kLongMaxBlocks;              // -D per query slot
+  auto rows_of = [&](const __bf16* t, PosItem it) {
+    return PosRows{t + ((size_t)it.b * a.N + a.T + it.l) * tok + (size_t)it.h * D, (size_t)L * tok};
+  };
+  auto row_at = [&](PosItem it, int f) {
+    return ((size_t)it.b * a.N + a.T + (size_t)f * L + it.l) * tok + (size_t)it.h * D;
+  };
+
+  if ((int)blockIdx.x < items) {
+    const PosItem it = pos_item(blockIdx.x, H, L);
+    copy_rows<D>(rows_of(a.k, it), F, bufA, w);
+    copy_rows<D>(rows_of(a.v, it), F, bufA + Lds::REGION, w);
+  }
+  for (int i = blockIdx.x; i < items; i += gridDim.x) {
+    const PosItem it = pos_item(i, H, L);
+    const uint8_t* km = a.key_mask ? a.key_mask + (size_t)it.b * a.N + a.T + it.l : nullptr;
+    // per-lane values formed anew for each position (nothing per-lane held across the loop)
+    const int lane = opaque_lane();
+    const int l32 = lane & 31, hi = lane >> 5;
+    wait_all_memory();
+    __syncthreads();  // K, V of item i in A; every wave is done with B and the slot stats
+    copy_rows<D>(rows_of(a.q, it), F, bufB, w);
+    copy_rows<D>(rows_of(a.dout, it), F, bufB + Lds::REGION, w);
+
+    // ---- lane = query: dQ^T = c K^T dS^T over the key blocks (A: K, V rows) ----
+    bf16x8 kf[D / 16], vf[D / 16];  // the dK/dV half's K, V (key block w), read from A now
+    if (w < nblk) {
+      const int q = w * 32 + l32;
+      const bool q_in = q < F;
+      const size_t qrow = row_at(it, min(q, F - 1));
+      bf16x8 qf[D / 16], dof[D / 16];
+      float dsum = 0.0f;
+#pragma unroll
+      for (int ks = 0; ks < D / 16; ++ks) {
+        qf[ks] = *(const bf16x8*)(a.q + qrow + 16 * ks + 8 * hi);
+        dof[ks] = *(const bf16x8*)(a.dout + qrow + 16 * ks + 8 * hi);
+        const bf16x8 of = *(const bf16x8*)(a.o_in + qrow + 16 * ks + 8 * hi);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) dsum = fmaf((float)dof[ks][e], (float)of[e], dsum);
+      }
+      const float dd = halves_sum(dsum);  // D_q = <dO_q, O_q>
+      const float lse = a.lse[((size_t)it.b * H + it.h) * a.N + a.T + (size_t)min(q, F - 1) * L + it.l];
+      // LSE*log2e, +inf where the query has no valid key or is a padding slot past F (its
+      // probabilities are then 0 in both halves; the last block's wave writes those slots)
+      const float l2 = (q_in && lse != -INFINITY) ? lse * kLog2e : INFINITY;
+      if (hi == 0) {
+        lse_s[q] = l2;
+        nd_s[q] = q_in ? -dd : 0.0f;
+      }
+      f32x16 dq[D / 32];
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) dq[db] = zero_f32x16();
+      for (int kb = 0; kb < nblk; ++kb) {
+        const unsigned bits = key_bits(km, 0, L, F, kb, lane);
+        if (bits == 0) continue;
+        const int ln = opaque_lane();
+        f32x16 s = zero_f32x16(), dp = zero_f32x16();
+#pragma unroll
+        for (int ks = 0; ks < D / 16; ++ks) {
+          s = mfma32(rows_operand<D>(bufA, kb, ks, F, ln), qf[ks], s);
+          dp = mfma32(rows_operand<D>(bufA + Lds::REGION, kb, ks, F, ln), dof[ks], dp);
+        }
+        float ds[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float p = ((bits >> acc_row(r, hi)) & 1u) ? fast_exp2(fmaf(s[r], a.scale_log2, -l2)) : 0.0f;
+          ds[r] = p * (dp[r] - dd);
+        }
+        const bf16x8 sb0 = to_bf16x8(&ds[0]), sb1 = to_bf16x8(&ds[8]);
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) {
+          dq[db] = mfma32(frames_operand<D>(bufA, kb, 0, db, F, ln), sb0, dq[db]);
+          dq[db] = mfma32(frames_operand<D>(bufA, kb, 1, db, F, ln), sb1, dq[db]);
+        }
+      }
+      if (q_in) {
+        const size_t orow = row_at(it, q);
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            *(bf16x4*)(a.o + orow + db * 32 + 8 * j + 4 * hi) =
+                bf16x4{(__bf16)(dq[db][4 * j + 0] * a.scale), (__bf16)(dq[db][4 * j + 1] * a.scale),
+                       (__bf16)(dq[db][4 * j + 2] * a.scale), (__bf16)(dq[db][4 * j + 3] * a.scale)};
+      }
+      const int ln = opaque_lane();
+#pragma unroll
+      for (int ks = 0; ks < D / 16; ++ks) {
+        kf[ks] = rows_operand<D>(bufA, w, ks, F, ln);
+        vf[ks] = rows_operand<D>(bufA + Lds::REGION, w, ks, F, ln);
+      }
+    }
+    wait_all_memory();
+    __syncthreads();  // Q, dO of item i in B; slot stats written; nobody reads A any more
+    if (i + (int)gridDim.x < items) {
+      const PosItem nx = pos_item(i + gridDim.x, H, L);
+      copy_rows<D>(rows_of(a.k, nx), F, bufA, w);
+      copy_rows<D>(rows_of(a.v, nx), F, bufA + Lds::REGION, w);
+    }
+
+    // ---- lane = key: dV^T = dO^T P, dK^T = c Q^T dS over the query blocks (B: Q, dO) ----
+    if (w < nblk) {
+      const int j = w * 32 + l32;  // this lane's key frame
+      bool valid = j < F;
+      if (km) valid = valid & (km[(size_t)min(j, F - 1) * L] != 0);
+      f32x16 dk[D / 32], dv[D / 32];
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) {
+        dk[db] = zero_f32x16();
+        dv[db] = zero_f32x16();
+      }
+      for (int qb = 0; qb < nblk; ++qb) {
+        const int ln = opaque_lane();
+        f32x16 s = zero_f32x16(), dp;
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {  // dP accumulates on top of -D of its query rows
+          const f32x4 nd = *(const VC_LDS f32x4*)(nd_s + qb * 32 + 8 * jj + 4 * hi);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) dp[4 * jj + e] = nd[e];
+        }
+#pragma unroll
+        for (int ks = 0; ks < D / 16; ++ks) {
+          s = mfma32(rows_operand<D>(bufB, qb, ks, F, ln), kf[ks], s);
+          dp = mfma32(rows_operand<D>(bufB + Lds::REGION, qb, ks, F, ln), vf[ks], dp);
+        }
+        // An invalid key's P and dS reach only its own lane's dK, dV, written as zero.
+        bf16x8 pb[2], sb[2];
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2) {
+          float p[8], ds[8];
+#pragma unroll
+          for (int jj = 0; jj < 2; ++jj) {
+            const f32x4 l2 = *(const VC_LDS f32x4*)(lse_s + qb * 32 + 8 * (2 * h2 + jj) + 4 * hi);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const int r = 8 * h2 + 4 * jj + e;
+              p[4 * jj + e] = fast_exp2(fmaf(s[r], a.scale_log2, -l2[e]));
+              ds[4 * jj + e] = p[4 * jj + e] * dp[r];
+            }
+          }
+          pb[h2] = to_bf16x8(p);
+          sb[h2] = to_bf16x8(ds);
+        }
+        sched_fence();
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) {
+          dv[db] = mfma32(frames_operand<D>(bufB + Lds::REGION, qb, 0, db, F, ln), pb[0], dv[db]);
+          dv[db] = mfma32(frames_operand<D>(bufB + Lds::REGION, qb, 1, db, F, ln), pb[1], dv[db]);
+        }
+        sched_fence();
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) {
+          dk[db] = mfma32(frames_operand<D>(bufB, qb, 0, db, F, ln), sb[0], dk[db]);
+          dk[db] = mfma32(frames_operand<D>(bufB, qb, 1, db, F, ln), sb[1], dk[db]);
+        }
+      }
+      if (j < F) {
+        const size_t krow = row_at(it, j);
+        auto kv = [&](float x) { return (__bf16)(valid ? x * a.scale : 0.0f); };
+        auto vv = [&](float x) { return (__bf16)(valid ? x : 0.0f); };
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj) {
+            const int d = db * 32 + 8 * jj + 4 * hi;
+            *(bf16x4*)(a.dk + krow + d) = bf16x4{kv(dk[db][4 * jj + 0]), kv(dk[db][4 * jj + 1]),
+                                                 kv(dk[db][4 * jj + 2]), kv(dk[db][4 * jj + 3])};
+            *(bf16x4*)(a.dv + krow + d) = bf16x4{vv(dv[db][4 * jj + 0]), vv(dv[db][4 * jj + 1]),
+                                                 vv(dv[db][4 * jj + 2]), vv(dv[db][4 * jj + 3])};
+          }
+      }
+    }
+  }
+  wait_all_memory();  // no copy of this workgroup outlives it
+}
+
+}  // namespace
+
+hipError_t launch_temporal_long_fwd(const TemporalArgs& a, int head_dim, int cus, hipStream_t s) {
+  const int items = a.B * a.L * a.H;
+  dim3 grid((unsigned)std::max(1, std::min(items, cus)));
+  const bool sum = a.sum_out != nullptr;
+  if (head_dim == 128 && sum)
+    hipLaunchKernelGGL((temporal_long_fwd_kernel<128, true>), grid, dim3(64 * kLongWaves), 0, s, a);
+  else if (head_dim == 128)
+    hipLaunchKernelGGL((temporal_long_fwd_kernel<128, false>), grid, dim3(64 * kLongWaves), 0, s, a);
+  else if (sum)
+    hipLaunchKernelGGL((temporal_long_fwd_kernel<64, true>), grid, dim3(64 * kLongWaves), 0, s, a);
+  else
+    hipLaunchKernelGGL((temporal_long_fwd_kernel<64, false>), grid, dim3(64 * kLongWaves), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_temporal_long_bwd(const TemporalArgs& a, int head_dim, int cus, hipStream_t s) {
+  const int items = a.B * a.L * a.H;
+  dim3 grid((unsigned)std::max(1, std::min(items, cus)));
+  if (head_dim == 128)
+    hipLaunchKernelGGL(temporal_long_bwd_kernel<128>, grid, dim3(64 * kLongWaves), 0, s, a);
+  else
+    hipLaunchKernelGGL(temporal_long_bwd_kernel<64>, grid, dim3(64 * kLongWaves), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace vcja

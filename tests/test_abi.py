@@ -162,8 +162,8 @@ def test_binding_fails_loudly_without_library(monkeypatch):
 def test_temporal_argument_errors(lib):
     p = 1 << 20
     d = good_desc()
-    # more than 32 frames is outside what the temporal kernel packs
-    big = good_desc(frames=33, grid_h=2, grid_w=2)
+    # more than 144 frames is outside what the long-clip kernel stages in LDS
+    big = good_desc(frames=145, grid_h=2, grid_w=2)
     assert lib.vc_temporalattn_fwd(ctypes.byref(big), p, p, p, None, p, p, None) == -2
     assert lib.vc_temporalattn_bwd(ctypes.byref(big), p, p, p, p, p, p, None, p, p, p, p, 1 << 30, None) == -2
     assert lib.vc_temporalattn_fwd(ctypes.byref(good_desc(head_dim=48)), p, p, p, None, p, p, None) == -3
@@ -176,6 +176,11 @@ def test_temporal_argument_errors(lib):
     assert lib.vc_temporalattn_bwd(ctypes.byref(d), p, p, p, p, p, p, None, p, p, p, p, need - 1, None) == -5
     assert lib.vc_temporalattn_bwd(ctypes.byref(d), p, p, p, p, p, None, None, p, p, p, p, need, None) == -1
     assert vc.vc_temporalattn_bwd_workspace_bytes(good_desc(batch=0)) == 0
+    # long clips (33..144 frames) need no workspace: not checked, may be NULL (no device here
+    # or a GPU present: the call would run, so only the refusal paths are exercised)
+    longc = good_desc(frames=144, grid_h=1, grid_w=3)
+    assert lib.vc_temporalattn_fwd(ctypes.byref(longc), p, p, p, None, p, p + 4, None) == -4
+    assert lib.vc_temporalattn_bwd(ctypes.byref(longc), p, p, p, p, p, p, None, p, p, None, None, 0, None) == -1
 
 
 def test_branch_sum_argument_errors(lib):

@@ -73,6 +73,7 @@ SMALL = [
     ("T100-F3-L70-ragged", 2, 2, 128, 100, 3, 7, 10, True, False),
     ("T8-F8-L33-masked", 1, 3, 64, 8, 8, 3, 11, True, True),
     ("T0-F5-L64", 1, 2, 128, 0, 5, 8, 8, False, False),
+    ("T24-F40-L12-masked", 1, 2, 128, 24, 40, 3, 4, True, True),  # temporal: long-clip kernel
 ]
 
 

@@ -65,6 +65,18 @@ WORKLOADS = {
 
 HEADLINE = 3
 
+# Shapes measured by the benchmark's branch modes only (not parity workloads of the five
+# configurations): a 144-frame clip, the longest input length in frames the paper quotes
+# (Sec. VI-D), at the 720p token grid. Their inputs are drawn on the device
+# (make_inputs_device): a host draw of 6.4e9 values would take minutes.
+EXTRA = {
+    6: Workload(6, "clip-144f-720p", 1, 24, 128, 256, 144, 45, 80),
+}
+
+
+def get(wid: int) -> Workload:
+    return WORKLOADS[wid] if wid in WORKLOADS else EXTRA[wid]
+
 
 def make_inputs(w: Workload | int, seed: int | None = None, with_do: bool = True) -> dict:
     """Float32 q, k, v, do (numpy, [B,N,H,D]) and int32 text_len (or None)."""
@@ -83,6 +95,28 @@ def make_inputs(w: Workload | int, seed: int | None = None, with_do: bool = True
     if w.ragged_text:
         text_len = rng.integers(min(8, w.text_slot), w.text_slot + 1, size=w.batch).astype(np.int32)
     return {"q": q, "k": k, "v": v, "do": do, "text_len": text_len}
+
+
+def make_inputs_device(w: Workload, seed: int | None = None, device="cuda") -> dict:
+    """bf16 q, k, v, do ([B,N,H,D], standard normal) drawn with torch's generator on the
+    device (seed = 1000 + workload id), in that order; text_len as make_inputs draws it."""
+    import torch
+    seed = 1000 + w.wid if seed is None else seed
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed)
+    out = {}
+    for name in ("q", "k", "v", "do"):
+        x = torch.randn(w.shape, generator=gen, device=device, dtype=torch.float32)
+        if name == "q" and w.q_prescale != 1.0:
+            x *= w.q_prescale
+        out[name] = x.to(torch.bfloat16).contiguous()
+        del x
+    text_len = None
+    if w.ragged_text:
+        rng = np.random.Generator(np.random.PCG64(seed))
+        text_len = rng.integers(min(8, w.text_slot), w.text_slot + 1, size=w.batch).astype(np.int32)
+    out["text_len"] = text_len
+    return out
 
 
 def custom(batch, heads, head_dim, text_slot, frames, grid_h, grid_w, wid=0, name="custom",
