@@ -19,8 +19,9 @@ GB/s (bytes the step must move at least).
 --branch block measures the whole attention of the parallel block (the three
 branches and their fused sum) over --layers stacked layers, forward through all
 of them and backward in reverse, with the branch outputs each layer saves for
-its backward kept in HBM, recomputed before its backward, or offloaded to
-pinned host memory and loaded back (the memory strategies of Sec. V-B / VI-D).
+its backward kept in HBM, or, for a selective ratio of the layers, recomputed
+before its backward, offloaded to pinned host memory and loaded back, or both
+combined (the memory strategies of Sec. V-B / VI-D).
 """
 from __future__ import annotations
 
@@ -226,7 +227,9 @@ def main(argv=None):
                     help="1-5: the five configurations; 6: a 144-frame clip (branch measurements)")
     ap.add_argument("--branch", default="joint", choices=["joint", "spatial", "temporal", "block"],
                     help="attention branch to measure (joint = the headline; block = all three and their sum)")
-    ap.add_argument("--layers", type=int, default=4, help="stacked layers for --branch block")
+    ap.add_argument("--layers", type=int, default=10, help="stacked layers for --branch block")
+    ap.add_argument("--ratios", default="0.2,0.5,0.8,1",
+                    help="selective ratios measured by --branch block (share of layers recomputed/offloaded)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the oracle timing")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--deterministic", action="store_true",
@@ -271,10 +274,10 @@ def main(argv=None):
     q, k, v, do = g["q"], g["k"], g["v"], g["do"]
     if args.branch == "temporal":  # no joint workspaces
         return branch_main(args, w, g, text_len, tl, desc, o, lse, dq, dk, dv, None, None, stream)
-    fws = vc.fwd_workspace(desc, dev)
     if args.branch == "block":
         del o, lse, dq, dk, dv
-        return block_main(args, w, g, text_len, tl, desc, fws, stream)
+        return block_main(args, w, g, text_len, tl, desc, stream)
+    fws = vc.fwd_workspace(desc, dev)
     ws = vc.spatial_workspace(desc, dev) if args.branch == "spatial" else vc.workspace(desc, dev)
     fwsb, wsb = fws.numel(), ws.numel()
     if args.branch != "joint":
@@ -486,108 +489,71 @@ def pcie_rates(dev, mib=1024):
     return n / (ev[0].elapsed_time(ev[1]) * 1e-3) / 1e9, n / (ev[1].elapsed_time(ev[2]) * 1e-3) / 1e9
 
 
-def block_main(args, w, g, text_len, tl, desc, fws, stream):
+def block_main(args, w, g, text_len, tl, desc, stream):
     """`--layers` stacked attention blocks (joint, spatial and temporal branches with the
     sum fused into the temporal forward), forward through every layer, then backward in
-    reverse, as in a training step. q, k, v, dO are shared by the layers. Each layer saves
-    the O and LSE of its three branches for its backward:
-      keep       every layer's set stays in HBM;
-      recompute  one scratch set; a layer's three forwards run again before its backward;
-      offload    a ring of two device sets; the set of layer i is stored to pinned host
-                 memory on the offload engine's stream while layer i+1 computes, and loaded
-                 back while layer i+2's backward runs (the last two layers stay resident).
+    reverse, as in a training step; q, k, v, dO are shared by the layers. Each layer saves
+    the O and LSE of its three branches for its backward, and a plan (memory.plan) decides
+    per layer whether that set is kept in HBM, recomputed before the layer's backward or
+    offloaded to pinned host memory and loaded back (Sec. V-B). Measured: every layer kept,
+    then recomputation, offloading and their combination (offloaded share 0.2, the rest
+    recomputed) at each selective ratio of --ratios (the paper's tuned ratios by default).
     """
     import torch
     import paper_2501_08453_amd as vc
+    from paper_2501_08453_amd import memory as mem
     q, k, v, do = g["q"], g["k"], g["v"], g["do"]
-    sh = stream.cuda_stream
     B, N, H, D = w.shape
     K = max(1, args.layers)
     dev = q.device
-    ws_j = vc.workspace(desc, dev)
-    ws_s = vc.spatial_workspace(desc, dev)
-    ws_t = vc._workspace(vc.vc_temporalattn_bwd_workspace_bytes(desc), dev)
     out = torch.empty_like(q)
-    grads = [tuple(torch.empty_like(q) for _ in range(3)) for _ in range(3)]
+    grads = tuple(tuple(torch.empty_like(q) for _ in range(3)) for _ in range(3))
+    ratios = [float(x) for x in args.ratios.split(",") if x]
 
-    def new_set():  # O, LSE of the joint, spatial and temporal branches
-        sv = []
-        for _ in range(3):
-            sv += [torch.empty_like(q), torch.empty((B, H, N), dtype=torch.float32, device=dev)]
-        return sv
+    def run(strategies):
+        bs = mem.BlockStack(desc, [(q, k, v)] * K, strategies, [out] * K, [grads] * K, text_len=tl)
+        try:
+            for _ in range(args.warmup):
+                bs.forward(stream)
+                bs.backward([do] * K, stream)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(args.steps):
+                bs.forward(stream)
+                bs.backward([do] * K, stream)
+            torch.cuda.synchronize()
+            return (time.perf_counter() - t0) * 1e3 / args.steps, bs.set_bytes
+        finally:
+            bs.close()
+            del bs
+            torch.cuda.empty_cache()
 
-    def forward(sv):
-        o_j, l_j, o_s, l_s, o_t, l_t = sv
-        vc.vc_jointattn_fwd(desc, q, k, v, tl, None, o_j, l_j, fws, fws.numel(), sh)
-        vc.vc_spatialattn_fwd(desc, q, k, v, tl, None, o_s, l_s, fws, fws.numel(), sh)
-        vc.vc_temporalattn_fwd_sum(desc, q, k, v, None, o_j, o_s, o_t, l_t, out, sh)
-
-    def backward(sv):
-        o_j, l_j, o_s, l_s, o_t, l_t = sv
-        vc.vc_jointattn_bwd(desc, q, k, v, o_j, l_j, do, tl, None, *grads[0], ws_j, ws_j.numel(), sh)
-        vc.vc_spatialattn_bwd(desc, q, k, v, o_s, l_s, do, tl, None, *grads[1], ws_s, ws_s.numel(), sh)
-        vc.vc_temporalattn_bwd(desc, q, k, v, o_t, l_t, do, None, *grads[2], ws_t, ws_t.numel(), sh)
-
-    keep_sets = [new_set() for _ in range(K)]
-    ring = keep_sets[:2] if K >= 2 else keep_sets
-    scratch = keep_sets[0]
-    n_off = max(0, K - 2)  # layers whose set leaves the device
-    host = [[torch.empty(t.shape, dtype=t.dtype, pin_memory=True) for t in ring[0]] for _ in range(n_off)]
-    off = vc.Offload()
-
-    def step_keep():
-        for i in range(K):
-            forward(keep_sets[i])
-        for i in reversed(range(K)):
-            backward(keep_sets[i])
-
-    def step_recompute():
-        for _ in range(K):
-            forward(scratch)
-        for _ in range(K):
-            forward(scratch)
-            backward(scratch)
-
-    def step_offload():
-        for i in range(K):
-            forward(ring[i % 2])
-            if i >= 1 and i - 1 < n_off:
-                off.wait()  # layer i+1 overwrites layer i-1's set: its store must be done
-            if i < n_off:
-                for hb, t in zip(host[i], ring[i % 2]):
-                    off.store(hb, t, sh)
-        for i in reversed(range(K)):
-            if 0 <= i - 1 < n_off:  # bring layer i-1 back while layer i's backward runs
-                for hb, t in zip(host[i - 1], ring[(i - 1) % 2]):
-                    off.load(t, hb, sh)
-            backward(ring[i % 2])
-            off.wait()
-
-    modes = {"keep": step_keep, "recompute": step_recompute, "offload": step_offload}
-    times = {}
-    for name, fn in modes.items():
-        for _ in range(args.warmup):
-            fn()
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(args.steps):
-            fn()
-        torch.cuda.synchronize()
-        times[name] = (time.perf_counter() - t0) * 1e3 / args.steps
-    off.close()
+    keep_ms, set_bytes = run(mem.plan(K, 0.0, "keep"))
+    runs = []
+    for ratio in ratios:
+        for mode in ("recompute", "offload", "combination"):
+            st = mem.plan(K, ratio, mode)
+            ms, _ = run(st)
+            n_off = st.count("offload")
+            runs.append({"mode": mode, "selective_ratio": ratio, "offloaded_layers": n_off,
+                         "recomputed_layers": st.count("recompute"), "ms_per_step": round(ms, 3),
+                         "overhead": round(ms / keep_ms - 1.0, 4),
+                         "device_saved_bytes": mem.device_sets(st) * set_bytes,
+                         "host_bytes": n_off * set_bytes, "pcie_bytes_per_step": 2 * n_off * set_bytes})
+            print("  %-11s ratio %.2f: %d offloaded, %d recomputed: %.2f ms (%+.1f%%)"
+                  % (mode, ratio, n_off, st.count("recompute"), ms, 100 * (ms / keep_ms - 1)), file=sys.stderr,
+                  flush=True)
     d2h, h2d = pcie_rates(dev)
 
     fj, bj = flops(w, text_len)
-    fs, bs = spatial_flops(w, text_len)
+    fs, bs_ = spatial_flops(w, text_len)
     L = w.grid_h * w.grid_w
     ft = 4.0 * w.batch * w.heads * L * w.frames * w.frames * w.head_dim  # every video query, F keys
-    block_flops = K * (fj + bj + fs + bs + 3.0 * ft)
-    value = block_flops / (times["keep"] * 1e-3) / 1e12
-    set_bytes = sum(t.numel() * t.element_size() for t in ring[0])
-    moved = 2 * n_off * set_bytes
+    block_flops = K * (fj + bj + fs + bs_ + 3.0 * ft)
+    value = block_flops / (keep_ms * 1e-3) / 1e12
     line = {
         "metric": METRIC_BLOCK, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(times["keep"], 4), "higher_is_better": True,
+        "warmup": args.warmup, "ms_per_step": round(keep_ms, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded N(0,1) q, k, v, dO of the workload's shape, shared by the layers)",
         "config": {
@@ -600,13 +566,9 @@ def block_main(args, w, g, text_len, tl, desc, fws, stream):
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(value / PEAK_BF16_TFLOPS, 4),
                      "traffic": None, "algorithmic_per_launch": block_flops},
         "memory_strategies": {
-            "saved_bytes_per_layer": set_bytes,
-            "keep": {"ms_per_step": round(times["keep"], 3), "device_saved_bytes": K * set_bytes},
-            "recompute": {"ms_per_step": round(times["recompute"], 3), "device_saved_bytes": set_bytes,
-                          "overhead": round(times["recompute"] / times["keep"] - 1.0, 4)},
-            "offload": {"ms_per_step": round(times["offload"], 3), "device_saved_bytes": len(ring) * set_bytes,
-                        "host_bytes": n_off * set_bytes, "pcie_bytes_per_step": moved,
-                        "overhead": round(times["offload"] / times["keep"] - 1.0, 4)},
+            "saved_bytes_per_layer": set_bytes, "offload_share_in_combination": mem.OFFLOAD_SHARE,
+            "keep": {"ms_per_step": round(keep_ms, 3), "device_saved_bytes": K * set_bytes},
+            "selective": runs,
             "pcie_GBps": {"d2h": round(d2h, 2), "h2d": round(h2d, 2)},
         },
         "cpu_baseline": None,

@@ -126,3 +126,48 @@ def test_keep_recompute_offload_give_identical_gradients():
             for a, b in zip(gk, go):
                 assert torch.equal(a, b), name
         log("   %s: bitwise equal to keep" % name)
+
+
+def test_selective_plans_give_identical_results():
+    """Five stacked layers with their own q, k, v and upstream gradient, run under plans that
+    recompute and/or offload a share of the layers (memory.BlockStack: one or two device
+    sets for the offloaded layers in turn, loads overlapping another layer's backward):
+    every layer's block output and the gradients of all three branches are bitwise those of
+    keeping every layer's saved outputs."""
+    import torch
+    import paper_2501_08453_amd as vc
+    from paper_2501_08453_amd import memory as mem
+    K = 5
+    assert mem.ring_size(mem.plan(K, 0.4, "offload")) == 1 and mem.ring_size(mem.plan(K, 0.6, "offload")) == 2
+    w = W.custom(1, 2, 128, 16, 4, 6, 8)
+    desc = vc.desc_for(w, deterministic=True)
+    inputs, douts = [], []
+    for i in range(K):
+        x = W.make_inputs(w, seed=3100 + i)
+        inputs.append(tuple(to_gpu_bf16(x[n]) for n in ("q", "k", "v")))
+        douts.append(to_gpu_bf16(x["do"]))
+
+    def run(strategies):
+        outs = [torch.full_like(inputs[0][0], float("nan")) for _ in range(K)]
+        grads = [tuple(tuple(torch.full_like(inputs[0][0], float("nan")) for _ in range(3)) for _ in range(3))
+                 for _ in range(K)]
+        bs = mem.BlockStack(desc, inputs, strategies, outs, grads)
+        bs.forward()
+        bs.backward(douts)
+        torch.cuda.synchronize()
+        bs.close()
+        return outs, grads
+
+    ref = run(mem.plan(K, 0.0, "keep"))
+    # offload 0.4: two spaced layers sharing one device set; 0.6 and 1.0: adjacent ones, two
+    # sets; combination: one offloaded layer and recomputed ones
+    for mode, ratio in (("recompute", 0.6), ("offload", 0.4), ("offload", 0.6), ("offload", 1.0),
+                        ("combination", 1.0), ("combination", 0.2)):
+        st = mem.plan(K, ratio, mode)
+        got = run(st)
+        for i in range(K):
+            assert torch.equal(got[0][i], ref[0][i]), (mode, ratio, i)
+            for br in range(3):
+                for a, b in zip(got[1][i][br], ref[1][i][br]):
+                    assert torch.equal(a, b), (mode, ratio, i, br)
+        log("   %s at ratio %.1f (%s): bitwise equal to keep" % (mode, ratio, ",".join(s[0] for s in st)))
