@@ -140,13 +140,30 @@ __global__ __launch_bounds__(64 * kLongWaves, 1) void temporal_long_fwd_kernel(T
     copy_rows<D>(rows_of(a.v, it), F, dst + Lds::REGION, w);
   };
 
+  // This wave's query rows (B operands: the lane's frame w*32 + l32, clamped to the last
+  // frame, dims 16*ks + 8*hi..), loaded one item ahead so that their latency overlaps the
+  // previous item's work.
+  auto load_q = [&](int i, bf16x8* dst) {
+    const PosItem it = pos_item(i, H, L);
+    const int ln = opaque_lane();
+    const size_t row = ((size_t)it.b * a.N + a.T + (size_t)min(w * 32 + (ln & 31), F - 1) * L + it.l) * tok +
+                       (size_t)it.h * D + 8 * (ln >> 5);
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) dst[ks] = *(const bf16x8*)(a.q + row + 16 * ks);
+  };
+  bf16x8 qf[D / 16], qn[D / 16];
   int buf = 0;
-  if ((int)blockIdx.x < items) issue(blockIdx.x, 0);
+  if ((int)blockIdx.x < items) {
+    issue(blockIdx.x, 0);
+    if (w < nblk) load_q(blockIdx.x, qf);
+  }
   for (int i = blockIdx.x; i < items; i += gridDim.x, buf ^= 1) {
     wait_all_memory();
     __syncthreads();  // K, V of item i are in buffer `buf`; nobody reads the other buffer
-    if (i + (int)gridDim.x < items) issue(i + gridDim.x, buf ^ 1);
+    const bool more = i + (int)gridDim.x < items;
+    if (more) issue(i + gridDim.x, buf ^ 1);
     if (w >= nblk) continue;  // no query block for this wave
+    if (more) load_q(i + gridDim.x, qn);
     const PosItem it = pos_item(i, H, L);
     const int lane = opaque_lane();
     const int l32 = lane & 31, hi = lane >> 5;
@@ -156,10 +173,6 @@ __global__ __launch_bounds__(64 * kLongWaves, 1) void temporal_long_fwd_kernel(T
     // This lane's query: frame q of the wave's block (past F: the last frame, not written).
     const int q = w * 32 + l32;
     const bool q_in = q < F;
-    const size_t qrow = ((size_t)it.b * a.N + a.T + (size_t)min(q, F - 1) * L + it.l) * tok + (size_t)it.h * D;
-    bf16x8 qf[D / 16];
-#pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks) qf[ks] = *(const bf16x8*)(a.q + qrow + 16 * ks + 8 * hi);
     f32x16 oacc[D / 32];
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) oacc[db] = zero_f32x16();
@@ -228,6 +241,8 @@ __global__ __launch_bounds__(64 * kLongWaves, 1) void temporal_long_fwd_kernel(T
         a.lse[((size_t)it.b * H + it.h) * a.N + a.T + (size_t)q * L + it.l] =
             lt > 0.0f ? (m + __log2f(lt)) * kLn2 : -INFINITY;
     }
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) qf[ks] = qn[ks];
   }
 }
 
@@ -251,10 +266,29 @@ __global__ __launch_bounds__(64 * kLongWaves, 1) void temporal_long_bwd_kernel(T
     return ((size_t)it.b * a.N + a.T + (size_t)f * L + it.l) * tok + (size_t)it.h * D;
   };
 
+  // The dQ half's per-lane inputs (query frame w*32 + l32, clamped to the last frame): Q and
+  // dO rows as B operands and the LSE, loaded one item ahead (at the end of the previous
+  // item's dK/dV half) so that their latency overlaps that work. (The O row, needed only for
+  // D, is read at the start of the half: holding it too across the dK/dV half would spill.)
+  bf16x8 qf[D / 16], dof[D / 16];
+  float lse_in = 0.0f;
+  auto load_rows = [&](int i) {
+    const PosItem it = pos_item(i, H, L);
+    const int ln = opaque_lane();
+    const int f = min(w * 32 + (ln & 31), F - 1);
+    const size_t row = row_at(it, f) + 8 * (ln >> 5);
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) {
+      qf[ks] = *(const bf16x8*)(a.q + row + 16 * ks);
+      dof[ks] = *(const bf16x8*)(a.dout + row + 16 * ks);
+    }
+    lse_in = a.lse[((size_t)it.b * H + it.h) * a.N + a.T + (size_t)f * L + it.l];
+  };
   if ((int)blockIdx.x < items) {
     const PosItem it = pos_item(blockIdx.x, H, L);
     copy_rows<D>(rows_of(a.k, it), F, bufA, w);
     copy_rows<D>(rows_of(a.v, it), F, bufA + Lds::REGION, w);
+    if (w < nblk) load_rows(blockIdx.x);
   }
   for (int i = blockIdx.x; i < items; i += gridDim.x) {
     const PosItem it = pos_item(i, H, L);
@@ -272,19 +306,18 @@ __global__ __launch_bounds__(64 * kLongWaves, 1) void temporal_long_bwd_kernel(T
     if (w < nblk) {
       const int q = w * 32 + l32;
       const bool q_in = q < F;
-      const size_t qrow = row_at(it, min(q, F - 1));
-      bf16x8 qf[D / 16], dof[D / 16];
       float dsum = 0.0f;
+      {
+        const size_t orow = row_at(it, min(q, F - 1)) + 8 * hi;
 #pragma unroll
-      for (int ks = 0; ks < D / 16; ++ks) {
-        qf[ks] = *(const bf16x8*)(a.q + qrow + 16 * ks + 8 * hi);
-        dof[ks] = *(const bf16x8*)(a.dout + qrow + 16 * ks + 8 * hi);
-        const bf16x8 of = *(const bf16x8*)(a.o_in + qrow + 16 * ks + 8 * hi);
+        for (int ks = 0; ks < D / 16; ++ks) {
+          const bf16x8 of = *(const bf16x8*)(a.o_in + orow + 16 * ks);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) dsum = fmaf((float)dof[ks][e], (float)of[e], dsum);
+          for (int e = 0; e < 8; ++e) dsum = fmaf((float)dof[ks][e], (float)of[e], dsum);
+        }
       }
       const float dd = halves_sum(dsum);  // D_q = <dO_q, O_q>
-      const float lse = a.lse[((size_t)it.b * H + it.h) * a.N + a.T + (size_t)min(q, F - 1) * L + it.l];
+      const float lse = lse_in;
       // LSE*log2e, +inf where the query has no valid key or is a padding slot past F (its
       // probabilities are then 0 in both halves; the last block's wave writes those slots)
       const float l2 = (q_in && lse != -INFINITY) ? lse * kLog2e : INFINITY;
@@ -414,9 +447,10 @@ __global__ __launch_bounds__(64 * kLongWaves, 1) void temporal_long_bwd_kernel(T
                                                  vv(dv[db][4 * jj + 2]), vv(dv[db][4 * jj + 3])};
           }
       }
+      if (i + (int)gridDim.x < items) load_rows(i + gridDim.x);  // the next item's dQ-half inputs
     }
   }
-  wait_all_memory();  // no copy of this workgroup outlives it
+  wait_all_memory();  // no copy or load of this workgroup outlives it
 }
 
 }  // namespace
