@@ -440,7 +440,11 @@ def branch_main(args, w, g, text_len, tl, desc, o, lse, dq, dk, dv, fws, ws, str
         a_fwd, a_bwd = temporal_bytes(w)
         scale, unit, peak, bound, metric = 1e9, "GB/s", PEAK_HBM_GBS, "hbm", METRIC_TEMPORAL
     value = (a_fwd + a_bwd) / (ms_step * 1e-3) / scale
-    # Dominant call: the backward (one call: preparation, dK/dV and dQ kernels).
+    # Dominant call: the backward (one call: preparation and gradient kernels; for clips of
+    # more than 32 frames one persistent kernel that forms D and LSE*log2(e) itself).
+    long_clip = args.branch == "temporal" and w.frames > 32
+    bwd_label = ("temporal backward (one persistent kernel, D and LSE*log2(e) formed inside)" if long_clip
+                 else "%s backward (prepare + gradient kernels)" % args.branch)
     bwd_rate = a_bwd / (k_bwd * 1e-3) / scale
     line = {
         "metric": metric, "value": round(value, 2), "unit": unit, "n_gpus": 1, "steps": args.steps,
@@ -455,7 +459,7 @@ def branch_main(args, w, g, text_len, tl, desc, o, lse, dq, dk, dv, fws, ws, str
         },
         "kernels_ms": {"fwd": round(k_fwd, 4), "bwd": round(k_bwd, 4)},
         "fwd_rate": round(a_fwd / (k_fwd * 1e-3) / scale, 2),
-        "roofline": {"bound": bound, "kernel": "%s backward (prepare + gradient kernels)" % args.branch,
+        "roofline": {"bound": bound, "kernel": bwd_label,
                      "achieved": round(bwd_rate, 2), "peak": peak, "unit": unit,
                      "frac": round(bwd_rate / peak, 4), "traffic": None,
                      "algorithmic_per_launch": a_bwd},
