@@ -6,7 +6,8 @@ hipcc cross-compiles the device code to assembly).
   global -> LDS instruction, and every such instruction must come from those copies.
 - Packed fp32 arithmetic is disabled at build time; no packed fp32 add, multiply or fma may
   appear in any kernel.
-- The hot joint-attention kernels fit their register budget without scratch spills.
+- The hot joint-attention kernels and the long-clip temporal kernels fit their register
+  budget without scratch spills.
 """
 import os
 import re
@@ -21,7 +22,7 @@ sys.path.insert(0, ROOT)
 
 from paper_2501_08453_amd import build as B  # noqa: E402
 
-SOURCES = ["fwd.hip", "bwd.hip", "temporal.hip", "layout.hip", "offload.hip"]
+SOURCES = ["fwd.hip", "bwd.hip", "temporal.hip", "temporal_long.hip", "layout.hip", "offload.hip"]
 
 
 @pytest.fixture(scope="module")
@@ -89,6 +90,9 @@ HOT = [
     ("bwd.hip", "bwd_dkdv_kernelILi128ELb0ELb0EE"),  # separate joint dK/dV
     ("bwd.hip", "bwd_dq_kernelILi128EE"),
     ("bwd.hip", "bwd_dq_kernelILi64EE"),
+    ("temporal_long.hip", "temporal_long_fwd_kernelILi128ELb0EE"),  # clips of 33-144 frames
+    ("temporal_long.hip", "temporal_long_fwd_kernelILi128ELb1EE"),
+    ("temporal_long.hip", "temporal_long_bwd_kernelILi128EE"),
 ]
 
 
