@@ -352,6 +352,9 @@ def main(argv=None):
         },
         "pct_of_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
         "algorithmic_tflop_per_step": round((f_fwd + f_bwd) / 1e12, 4),
+        # The FlashAttention convention counts the backward as 2.5 forwards (its recomputed
+        # Q K^T included): 14 instead of 12 flops per (query, key, dim) triple.
+        "fa_convention_tflops": round((f_fwd + 2.5 * f_fwd) / (ms_step * 1e-3) / 1e12, 2),
         "backward": "separate dK/dV and dQ passes (deterministic)" if separate
                     else "fused (dQ of the leading %.0f%% of keys by fp32 atomics in the dK/dV pass)"
                     % (100 * fused_share),
