@@ -356,6 +356,7 @@ def main(argv=None):
         # Q K^T included): 14 instead of 12 flops per (query, key, dim) triple.
         "fa_convention_tflops": round((f_fwd + 2.5 * f_fwd) / (ms_step * 1e-3) / 1e12, 2),
         "backward": "separate dK/dV and dQ passes (deterministic)" if separate
+                    else "fused (dQ of every key by fp32 atomics in the dK/dV pass)" if fused_share >= 1.0
                     else "fused (dQ of the leading %.0f%% of keys by fp32 atomics in the dK/dV pass)"
                     % (100 * fused_share),
         "kernels_ms": {"fwd": round(k_fwd, 4), "bwd_prepare": round(k_prep, 4),

@@ -59,9 +59,10 @@
 extern "C" {
 #endif
 
-/* Raised with every change of a signature, a struct or the meaning of an argument; the
- * Python binding refuses a library that reports another version. */
-#define VC_JOINTATTN_ABI_VERSION 7
+/* Raised with every change of a signature, a struct, the meaning of an argument or a
+ * documented result; the Python binding refuses a library that reports another
+ * version. */
+#define VC_JOINTATTN_ABI_VERSION 8
 
 typedef enum vc_status {
   VC_OK = 0,
@@ -162,11 +163,11 @@ size_t vc_jointattn_bwd_workspace_bytes(const vc_jointattn_desc* desc);
  * no atomics, the result is bitwise reproducible run to run (on devices with a
  * different number of compute units the split of the last round of
  * workgroups, and so the summation order of its rows, differs).
- * desc->deterministic = 0: stage 1 (token-major copy of k only),
- * vc_jointattn_bwd_fused, then stage 3 over the remaining keys; dk, dv are
- * reproducible run to run, dq only up to the rounding of its fp32 sums. When
- * vc_jointattn_fused_dq_keys(desc) is 0 (head_dim 64, where the fused pass is
- * slower) it runs the deterministic stages instead. */
+ * desc->deterministic = 0: stage 1 (token-major copy of k only, none when the
+ * fused pass carries every key), vc_jointattn_bwd_fused, then stage 3 over the
+ * remaining keys; dk, dv are reproducible run to run, dq only up to the
+ * rounding of its fp32 sums. When vc_jointattn_fused_dq_keys(desc) is 0 it
+ * runs the deterministic stages instead. */
 vc_status vc_jointattn_bwd(const vc_jointattn_desc* desc,
                            const void* q, const void* k, const void* v,
                            const void* o, const float* lse, const void* dout,
@@ -198,7 +199,8 @@ vc_status vc_jointattn_bwd_dkdv(const vc_jointattn_desc* desc,
  * same workspace, independent of stage 2. desc->deterministic = 0: completes
  * the fused backward (stage 1, then vc_jointattn_bwd_fused, on the same
  * workspace): over the keys whose blocks did not add their share of dQ in the
- * fused pass, plus that pass's fp32 accumulator. */
+ * fused pass, plus that pass's fp32 accumulator (when the fused pass carried
+ * every key, the accumulator alone). */
 vc_status vc_jointattn_bwd_dq(const vc_jointattn_desc* desc,
                               const void* q, const void* k, const void* v,
                               const void* dout,
@@ -215,9 +217,10 @@ vc_status vc_jointattn_bwd_dq(const vc_jointattn_desc* desc,
  * workspace; stage 3 (vc_jointattn_bwd_dq with desc->deterministic = 0)
  * completes dq. */
 /* Keys [0, K) whose share of dq the fused pass adds (vc_jointattn_bwd_fused);
- * stage 3 covers keys [K, N). Returns K (0 for head_dim 64: there
- * vc_jointattn_bwd runs the deterministic stages whatever desc->deterministic
- * says), or a negative vc_status if the descriptor is invalid. Host only. */
+ * stage 3 covers keys [K, N). K is the leading 65% of the 256-key blocks at
+ * head_dim 128 and every key at head_dim 64 (the fastest splits measured),
+ * never more than N. Returns K, or a negative vc_status if the descriptor is
+ * invalid. Host only. */
 int64_t vc_jointattn_fused_dq_keys(const vc_jointattn_desc* desc);
 
 vc_status vc_jointattn_bwd_fused(const vc_jointattn_desc* desc,

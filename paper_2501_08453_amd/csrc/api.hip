@@ -139,16 +139,21 @@ size_t tail_part_bytes(const vc_jointattn_desc* d, int64_t n) {
 // Fused backward: the key blocks [0, fused_dq_blocks) add their dQ share with atomics in
 // the key-stationary pass; the dQ pass covers the others. Per key block, the atomics (an
 // fp32 dQ tile per query tile) cost about what the dQ pass's recomputation of S and dP
-// costs, so the backward's time is nearly flat in the fraction between 1/2 and 7/8;
-// 65% measured fastest on the long workload. With head_dim 64 two waves share each dQ
-// block (each over half the keys), doubling the atomics, and the fused backward is slower
-// than the separate passes (medium workload: 2.6 against 2.3 ms): none, and the one-call
-// backward runs the separate passes.
-constexpr int kFusedDqPercent = 65;
+// costs at head_dim 128, so the backward's time is nearly flat in the fraction between 1/2
+// and 7/8 there; 65% measured fastest on the long workload (ragged-text and max-length
+// workloads: within 1% from 65% to 80%). At head_dim 64 fusing every key block is fastest
+// (medium workload: 1.85 ms against 2.02 at 65% and 2.11 for the separate passes); the dQ
+// pass then only converts the accumulator.
+constexpr int kFusedDqPercent128 = 65;
+constexpr int kFusedDqPercent64 = 100;
 int fused_dq_blocks(const vc_jointattn_desc* d, int64_t n) {
-  if (d->head_dim != 128) return 0;
   const int nblk = (int)((n + vcja::kDkdvKeys - 1) / vcja::kDkdvKeys);
-  return (int)(((int64_t)nblk * kFusedDqPercent + 50) / 100);
+  const int pct = d->head_dim == 128 ? kFusedDqPercent128 : kFusedDqPercent64;
+  return (int)(((int64_t)nblk * pct + 50) / 100);
+}
+// Every key block carries its dQ share: no dQ pass over key tiles (and no token-major K).
+bool all_keys_fused(const vc_jointattn_desc* d, int64_t n) {
+  return (int64_t)fused_dq_blocks(d, n) * vcja::kDkdvKeys >= n;
 }
 
 // Forward workspace: V^T tiles | split-tail partials (unnormalised O, base, sum per row).
@@ -382,7 +387,8 @@ vc_status vc_jointattn_bwd_prepare(const vc_jointattn_desc* desc, const void* q,
 namespace {
 
 // Backward stage 1; `tiles`: also the transposed token tiles of q and dout (read by the
-// separate dK/dV pass only; the fused backward reads those of k alone, in its dQ pass).
+// separate dK/dV pass only; the fused backward reads those of k alone, in its dQ pass, and
+// none when every key block carries its dQ share).
 vc_status prepare_impl(const vc_jointattn_desc* desc, const void* q, const void* k, const void* o, const float* lse,
                        const void* dout, void* workspace, size_t workspace_bytes, void* stream, bool tiles) {
   int64_t n = 0;
@@ -401,7 +407,8 @@ vc_status prepare_impl(const vc_jointattn_desc* desc, const void* q, const void*
   if (tiles && (vcja::launch_token_tiles(bf(q), w.qt, B, H, N, D, s) != hipSuccess ||
                 vcja::launch_token_tiles(bf(dout), w.dot, B, H, N, D, s) != hipSuccess))
     return VC_ERR_HIP;
-  if (vcja::launch_token_tiles(bf(k), w.kt, B, H, N, D, s) != hipSuccess) return VC_ERR_HIP;
+  if ((tiles || !all_keys_fused(desc, n)) && vcja::launch_token_tiles(bf(k), w.kt, B, H, N, D, s) != hipSuccess)
+    return VC_ERR_HIP;
   return VC_OK;
 }
 
@@ -476,8 +483,15 @@ vc_status dq_impl(const vc_jointattn_desc* desc, const void* q, const void* k, c
   const BwdWorkspace w = split_bwd_ws(desc, n, workspace);
   vcja::DqArgs a{};
   // Completing a fused backward: the key tiles of the blocks that did not add their dQ
-  // share, plus the accumulator the others filled.
+  // share, plus the accumulator the others filled; when every block added its share, the
+  // accumulator alone, scaled and rounded.
   if (fused) {
+    if (all_keys_fused(desc, n))
+      return vcja::launch_dq_from_acc(reinterpret_cast<const float*>(w.qt), static_cast<__bf16*>(dq),
+                                      (size_t)desc->batch * n * desc->heads * desc->head_dim, scale_of(desc),
+                                      as_stream(stream)) == hipSuccess
+                 ? VC_OK
+                 : VC_ERR_HIP;
     a.kt_min = fused_dq_blocks(desc, n) * (vcja::kDkdvKeys / vcja::kTileTok);
     a.dq_acc = reinterpret_cast<const float*>(w.qt);
   }

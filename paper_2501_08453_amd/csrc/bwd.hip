@@ -298,13 +298,15 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
   // visits tile phys(u).
   const int xs = (FUSED && !tail) ? (int)((blockIdx.x % kXcds) * ((a.ntile + kXcds - 1) / kXcds)) % a.ntile : 0;
   auto phys = [&](int u) { return u + xs >= a.ntile ? u + xs - a.ntile : u + xs; };
-  // Fused dQ: this wave's 32x32 block of the tile's dQ (query block dq_qb, dim block dq_db)
-  // over key steps [dq_s0, dq_s0 + DQ_STEPS) of 16 keys; when the dim blocks are fewer
-  // than the waves, several waves share a block, each over part of the keys.
+  // Fused dQ: wave w < DQ_BLOCKS forms the 32x32 block (query block dq_qb, dim block dq_db)
+  // of the tile's dQ over the workgroup's 256 keys. With fewer blocks than waves (head_dim
+  // 64: four), waves 0..3 take them, one per SIMD (wave w shares its SIMD with wave w + 4),
+  // so that each element still gets one atomic addition per key block.
   constexpr int DQ_BLOCKS = 2 * (D / 32);
-  constexpr int DQ_STEPS = kBKV / 16 / (kDkdvWaves / DQ_BLOCKS);
-  static_assert(kDkdvWaves % DQ_BLOCKS == 0, "dQ blocks per wave");
-  const int dq_qb = (w % DQ_BLOCKS) & 1, dq_db = (w % DQ_BLOCKS) >> 1, dq_s0 = (w / DQ_BLOCKS) * DQ_STEPS;
+  constexpr int DQ_STEPS = kBKV / 16;
+  static_assert(DQ_BLOCKS == kDkdvWaves || DQ_BLOCKS == kDkdvWaves / 2, "dQ blocks per wave");
+  const bool dq_wave = DQ_BLOCKS == kDkdvWaves || w < DQ_BLOCKS;  // constant for head_dim 128
+  const int dq_qb = w & 1, dq_db = (w >> 1) % (D / 32);
   f32x16 dq_blk;
   int dq_row0 = -1;  // first query row of the block awaiting its atomics, -1: none
   // The lane index as a value the compiler must treat as new at each use: per-lane
@@ -475,23 +477,25 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
           }
         }
         __syncthreads();  // dS^T of both query blocks complete
-        // dQ block: A = dS (queries x keys) by transposing reads of dS^T (this wave's query
-        // block's region), B = K from K^T. Lane l of 16-lane group G supplies key
-        // 16*st + 8*hi + (l%16)/4 (+4), i.e. row 32*(st/2) + 4*(st%2) + 8*((l%16)/4) + 2*hi
-        // (+1), and unit 4*(G%2) + l%4 of that row (k-steps counted from the wave's first).
-        const VC_LDS char* ds_src = dq_qb ? (const VC_LDS char*)stage : (const VC_LDS char*)ds_own;
-        const int arow = dq_s0 * 16 + 8 * ((ln & 15) >> 2) + 2 * (ln >> 5), aunit = 4 * ((ln >> 4) & 1) + (ln & 3);
-        const VC_LDS char* b_base = (const VC_LDS char*)smem + Lds::KT_OFF + (dq_db * 32 + (ln & 31)) * Lds::KTS +
-                                    (dq_s0 * 16 + 8 * (ln >> 5)) * 2;
-        dq_blk = zero_f32x16();
+        if (dq_wave) {
+          // dQ block: A = dS (queries x keys) by transposing reads of dS^T (this wave's query
+          // block's region), B = K from K^T. Lane l of 16-lane group G supplies key
+          // 16*st + 8*hi + (l%16)/4 (+4), i.e. row 32*(st/2) + 4*(st%2) + 8*((l%16)/4) + 2*hi
+          // (+1), and unit 4*(G%2) + l%4 of that row.
+          const VC_LDS char* ds_src = dq_qb ? (const VC_LDS char*)stage : (const VC_LDS char*)ds_own;
+          const int arow = 8 * ((ln & 15) >> 2) + 2 * (ln >> 5), aunit = 4 * ((ln >> 4) & 1) + (ln & 3);
+          const VC_LDS char* b_base =
+              (const VC_LDS char*)smem + Lds::KT_OFF + (dq_db * 32 + (ln & 31)) * Lds::KTS + 8 * (ln >> 5) * 2;
+          dq_blk = zero_f32x16();
   #pragma unroll
-        for (int st = 0; st < DQ_STEPS; ++st) {
-          const int j = arow + 32 * (st >> 1) + 4 * (st & 1);
-          const bf16x8 da = cat4(lds_read_tr(ds_src + Lds::ds_at(j, aunit)), lds_read_tr(ds_src + Lds::ds_at(j + 1, aunit)));
-          const bf16x8 kb8 = *(const VC_LDS bf16x8*)(b_base + st * 32);
-          dq_blk = mfma32(da, kb8, dq_blk);
+          for (int st = 0; st < DQ_STEPS; ++st) {
+            const int j = arow + 32 * (st >> 1) + 4 * (st & 1);
+            const bf16x8 da = cat4(lds_read_tr(ds_src + Lds::ds_at(j, aunit)), lds_read_tr(ds_src + Lds::ds_at(j + 1, aunit)));
+            const bf16x8 kb8 = *(const VC_LDS bf16x8*)(b_base + st * 32);
+            dq_blk = mfma32(da, kb8, dq_blk);
+          }
+          dq_row0 = q0 + dq_qb * 32;
         }
-        dq_row0 = q0 + dq_qb * 32;
       }
       qt = qn;
     }
@@ -815,6 +819,15 @@ __global__ void tail_reduce_dq_kernel(const float* part, __bf16* dq, int B, int 
   *(bf16x4*)(dq + off) = bf16x4{(__bf16)s[0], (__bf16)s[1], (__bf16)s[2], (__bf16)s[3]};
 }
 
+// dq = bf16(scale * acc), four elements per thread.
+__global__ void dq_from_acc_kernel(const float* acc, __bf16* dq, size_t n4, float scale) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n4) return;
+  const f32x4 x = ((const f32x4*)acc)[i];
+  ((bf16x4*)dq)[i] = bf16x4{(__bf16)(x[0] * scale), (__bf16)(x[1] * scale), (__bf16)(x[2] * scale),
+                            (__bf16)(x[3] * scale)};
+}
+
 // Fused dQ: zeroes the fp32 accumulator (a kernel, not a memset, so that a captured graph
 // replays it like any other node). n4 = elements / 4.
 __global__ void zero_f32_kernel(float* x, size_t n4) {
@@ -880,6 +893,12 @@ hipError_t launch_bwd_dkdv(const DkdvArgs& a, int head_dim, hipStream_t s) {
       hipLaunchKernelGGL(text_reduce_kernel<64>, rgrid, dim3(256), 0, s, a.text_part, a.dk, a.dv, a.B, a.H, a.N,
                          rows, nrow, a.text_chunks);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_dq_from_acc(const float* acc, __bf16* dq, size_t n, float scale, hipStream_t s) {
+  const size_t n4 = n / 4;
+  if (n4) hipLaunchKernelGGL(dq_from_acc_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s, acc, dq, n4, scale);
   return hipGetLastError();
 }
 

@@ -417,6 +417,9 @@ hipError_t launch_bwd_prepare(const __bf16* o, const float* lse, const __bf16* d
                               int H, int N, int Npad, int head_dim, hipStream_t s);
 hipError_t launch_bwd_dkdv(const DkdvArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_bwd_dq(const DqArgs& a, int head_dim, hipStream_t s);
+// dq = bf16(scale * acc) over n elements (a fused backward whose key blocks all added their
+// dQ share to the fp32 accumulator acc, [B, N, H, D] like dq). n a multiple of 4.
+hipError_t launch_dq_from_acc(const float* acc, __bf16* dq, size_t n, float scale, hipStream_t s);
 hipError_t launch_temporal_fwd(const TemporalArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_temporal_bwd(const TemporalArgs& a, int head_dim, hipStream_t s);
 // Long clips (F > 32): persistent grid of at most `cus` workgroups; the backward forms

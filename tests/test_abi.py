@@ -94,9 +94,8 @@ def test_null_descriptor_and_pointers(lib):
 
 def test_fused_dq_keys():
     """Keys whose dQ share the fused pass carries: head_dim 128, the leading 65% of the
-    256-key blocks, rounded to whole blocks, never more than N; head_dim 64 none (the
-    one-call backward then runs the separate passes); an invalid descriptor gives its
-    status."""
+    256-key blocks, rounded to whole blocks, never more than N; head_dim 64 every key; an
+    invalid descriptor gives its status."""
     long720p = vc.make_desc(1, 24, 128, 256, 16, 45, 80)  # 57,856 tokens, 226 blocks
     assert vc.vc_jointattn_fused_dq_keys(long720p) == 147 * 256
     tiny = vc.make_desc(1, 1, 128, 0, 1, 1, 5)  # 5 tokens, one block
@@ -106,7 +105,8 @@ def test_fused_dq_keys():
         k = vc.vc_jointattn_fused_dq_keys(d)
         assert k % 256 == 0 and 0 <= k <= 256 * n_blocks
         assert k == 256 * ((n_blocks * 65 + 50) // 100)
-        assert vc.vc_jointattn_fused_dq_keys(vc.make_desc(1, 1, 64, 0, 1, 1, 256 * n_blocks)) == 0
+        assert vc.vc_jointattn_fused_dq_keys(vc.make_desc(1, 1, 64, 0, 1, 1, 256 * n_blocks)) == 256 * n_blocks
+        assert vc.vc_jointattn_fused_dq_keys(vc.make_desc(1, 1, 64, 0, 1, 1, 256 * n_blocks - 3)) == 256 * n_blocks - 3
     assert vc.vc_jointattn_fused_dq_keys(vc.make_desc(1, 1, 96, 0, 1, 1, 5)) == -3  # head_dim
 
 
