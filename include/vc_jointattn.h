@@ -259,7 +259,11 @@ vc_status vc_spatialattn_fwd(const vc_jointattn_desc* desc,
 
 /* Spatial backward: dq, dk, dv from q, k, v, the spatial forward's o and lse, and
  * dout; workspace of vc_spatialattn_bwd_workspace_bytes (smaller: VC_ERR_WORKSPACE,
- * nothing launched). Bitwise reproducible, no atomics. */
+ * nothing launched). desc->deterministic = 1: separate dK/dV and dQ passes, bitwise
+ * reproducible, no atomics. desc->deterministic = 0: one key-stationary pass also
+ * adds every key block's share of dq to an fp32 accumulator with atomics (a video
+ * query row gets the shares of its frame's key blocks and of the text block); dk,
+ * dv are reproducible run to run, dq only up to the rounding of its fp32 sums. */
 vc_status vc_spatialattn_bwd(const vc_jointattn_desc* desc,
                              const void* q, const void* k, const void* v,
                              const void* o, const float* lse, const void* dout,

@@ -5,6 +5,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <limits>
 #include <mutex>
 
 #include "common.hpp"
@@ -300,8 +301,11 @@ size_t vc_spatialattn_bwd_workspace_bytes(const vc_jointattn_desc* desc) {
 
 namespace {
 
+// Token-major copies a backward's stage 1 makes: none (every key's dQ share added in the
+// key-stationary pass), of k (read by the dQ pass), or of q, dout and k (the separate passes).
+enum class StageTiles { kNone, kKeys, kAll };
 vc_status prepare_impl(const vc_jointattn_desc* desc, const void* q, const void* k, const void* o, const float* lse,
-                       const void* dout, void* workspace, size_t workspace_bytes, void* stream, bool tiles);
+                       const void* dout, void* workspace, size_t workspace_bytes, void* stream, StageTiles tiles);
 
 // Joint attention (frame_len 0) or the spatial branch (frame_len = tokens per frame).
 vc_status fwd_impl(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
@@ -379,18 +383,23 @@ vc_status vc_spatialattn_fwd(const vc_jointattn_desc* desc, const void* q, const
 vc_status vc_jointattn_bwd_prepare(const vc_jointattn_desc* desc, const void* q, const void* k, const void* o,
                                    const float* lse, const void* dout, void* workspace, size_t workspace_bytes,
                                    void* stream) {
-  return prepare_impl(desc, q, k, o, lse, dout, workspace, workspace_bytes, stream, desc && desc->deterministic);
+  int64_t n = 0;
+  const vc_status st = check_desc(desc, &n);
+  if (st != VC_OK) return st;
+  const StageTiles tiles = desc->deterministic     ? StageTiles::kAll
+                           : all_keys_fused(desc, n) ? StageTiles::kNone
+                                                     : StageTiles::kKeys;
+  return prepare_impl(desc, q, k, o, lse, dout, workspace, workspace_bytes, stream, tiles);
 }
 
 }  // extern "C"
 
 namespace {
 
-// Backward stage 1; `tiles`: also the transposed token tiles of q and dout (read by the
-// separate dK/dV pass only; the fused backward reads those of k alone, in its dQ pass, and
-// none when every key block carries its dQ share).
+// Backward stage 1 and the token-major copies `tiles` asks for: those of q and dout are read
+// by the separate dK/dV pass only, that of k by a dQ pass over key tiles.
 vc_status prepare_impl(const vc_jointattn_desc* desc, const void* q, const void* k, const void* o, const float* lse,
-                       const void* dout, void* workspace, size_t workspace_bytes, void* stream, bool tiles) {
+                       const void* dout, void* workspace, size_t workspace_bytes, void* stream, StageTiles tiles) {
   int64_t n = 0;
   vc_status st = check_desc(desc, &n);
   if (st != VC_OK) return st;
@@ -404,10 +413,10 @@ vc_status prepare_impl(const vc_jointattn_desc* desc, const void* q, const void*
   if (vcja::launch_bwd_prepare(bf(o), lse, bf(dout), w.dd, w.lse2, B, H, N, ntiles(n) * vcja::kTileTok, D, s) !=
       hipSuccess)
     return VC_ERR_HIP;
-  if (tiles && (vcja::launch_token_tiles(bf(q), w.qt, B, H, N, D, s) != hipSuccess ||
-                vcja::launch_token_tiles(bf(dout), w.dot, B, H, N, D, s) != hipSuccess))
+  if (tiles == StageTiles::kAll && (vcja::launch_token_tiles(bf(q), w.qt, B, H, N, D, s) != hipSuccess ||
+                                    vcja::launch_token_tiles(bf(dout), w.dot, B, H, N, D, s) != hipSuccess))
     return VC_ERR_HIP;
-  if ((tiles || !all_keys_fused(desc, n)) && vcja::launch_token_tiles(bf(k), w.kt, B, H, N, D, s) != hipSuccess)
+  if (tiles != StageTiles::kNone && vcja::launch_token_tiles(bf(k), w.kt, B, H, N, D, s) != hipSuccess)
     return VC_ERR_HIP;
   return VC_OK;
 }
@@ -457,7 +466,7 @@ vc_status dkdv_impl(const vc_jointattn_desc* desc, const void* q, const void* k,
   // Fused dQ: the fp32 accumulator takes the place of the transposed Q and dO tiles, which
   // the fused backward does not make (2 tile sets >= 4 bytes per element of dq).
   a.dq_acc = fused ? reinterpret_cast<float*>(w.qt) : nullptr;
-  a.dq_blocks = fused ? fused_dq_blocks(desc, n) : 0;
+  a.dq_blocks = !fused ? 0 : spatial ? std::numeric_limits<int>::max() : fused_dq_blocks(desc, n);
   a.B = desc->batch;
   a.H = desc->heads;
   a.N = (int)n;
@@ -486,12 +495,18 @@ vc_status dq_impl(const vc_jointattn_desc* desc, const void* q, const void* k, c
   // share, plus the accumulator the others filled; when every block added its share, the
   // accumulator alone, scaled and rounded.
   if (fused) {
-    if (all_keys_fused(desc, n))
-      return vcja::launch_dq_from_acc(reinterpret_cast<const float*>(w.qt), static_cast<__bf16*>(dq),
-                                      (size_t)desc->batch * n * desc->heads * desc->head_dim, scale_of(desc),
-                                      as_stream(stream)) == hipSuccess
-                 ? VC_OK
-                 : VC_ERR_HIP;
+    if (spatial || all_keys_fused(desc, n)) {
+      hipStream_t s = as_stream(stream);
+      if (vcja::launch_dq_from_acc(reinterpret_cast<const float*>(w.qt), static_cast<__bf16*>(dq),
+                                   (size_t)desc->batch * n * desc->heads * desc->head_dim, scale_of(desc),
+                                   s) != hipSuccess)
+        return VC_ERR_HIP;
+      // Spatial branch: text rows are not queries; their dq is zero.
+      if (spatial && vcja::launch_text_rows(static_cast<__bf16*>(dq), nullptr, nullptr, nullptr, desc->batch,
+                                            desc->heads, (int)n, desc->text_slot, desc->head_dim, s) != hipSuccess)
+        return VC_ERR_HIP;
+      return VC_OK;
+    }
     a.kt_min = fused_dq_blocks(desc, n) * (vcja::kDkdvKeys / vcja::kTileTok);
     a.dq_acc = reinterpret_cast<const float*>(w.qt);
   }
@@ -533,16 +548,20 @@ vc_status bwd_impl(const vc_jointattn_desc* desc, const void* q, const void* k, 
   if (st != VC_OK) return st;
   if (!q || !k || !v || !o || !lse || !dout || !dq || !dk || !dv) return VC_ERR_NULL;
   if (spatial && (st = check_ws(workspace, workspace_bytes, spatial_bwd_ws_bytes(desc, n))) != VC_OK) return st;
-  // Joint attention: dQ partly fused into the key-stationary kernel (atomics), unless the
-  // caller asks for bitwise reproducible results or the fused pass would carry no keys.
-  if (!spatial && !desc->deterministic && fused_dq_blocks(desc, n) > 0) {
-    if ((st = prepare_impl(desc, q, k, o, lse, dout, workspace, workspace_bytes, stream, false)) != VC_OK ||
-        (st = vc_jointattn_bwd_fused(desc, q, k, v, dout, text_len, key_mask, dk, dv, workspace, workspace_bytes,
-                                     stream)) != VC_OK)
+  // dQ fused into the key-stationary kernel (atomics) unless the caller asks for bitwise
+  // reproducible results: joint attention for its leading key blocks (the dQ pass covers
+  // the others), the spatial branch for every key block (a video query row gets the shares
+  // of 16 key blocks at 720p, so the atomics are few).
+  if (!desc->deterministic && (spatial || fused_dq_blocks(desc, n) > 0)) {
+    const StageTiles tiles = (spatial || all_keys_fused(desc, n)) ? StageTiles::kNone : StageTiles::kKeys;
+    if ((st = prepare_impl(desc, q, k, o, lse, dout, workspace, workspace_bytes, stream, tiles)) != VC_OK ||
+        (st = dkdv_impl(desc, q, k, v, dout, text_len, key_mask, dk, dv, workspace, workspace_bytes, stream,
+                        spatial, true)) != VC_OK)
       return st;
-    return dq_impl(desc, q, k, v, dout, text_len, key_mask, dq, workspace, workspace_bytes, stream, false, true);
+    return dq_impl(desc, q, k, v, dout, text_len, key_mask, dq, workspace, workspace_bytes, stream, spatial, true);
   }
-  if ((st = prepare_impl(desc, q, k, o, lse, dout, workspace, workspace_bytes, stream, true)) != VC_OK) return st;
+  if ((st = prepare_impl(desc, q, k, o, lse, dout, workspace, workspace_bytes, stream, StageTiles::kAll)) != VC_OK)
+    return st;
   if ((st = dkdv_impl(desc, q, k, v, dout, text_len, key_mask, dk, dv, workspace, workspace_bytes, stream,
                       spatial)) != VC_OK)
     return st;

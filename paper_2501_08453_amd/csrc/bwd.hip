@@ -121,7 +121,6 @@ struct DkdvLds {
 
 template <int D, bool SPATIAL, bool FUSED>
 __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a) {
-  static_assert(!(SPATIAL && FUSED), "dQ is fused for joint attention only");
   using Lds = DkdvLds<D, FUSED>;
   constexpr int RT = Lds::RT;                 // row-major Q or dO tile bytes
   constexpr int RS = RowTile<D>::kStride;     // their row stride
@@ -296,7 +295,7 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
   // their walk over the query tiles at a different eighth of them, so that the atomics
   // of concurrent workgroups land on different rows of the accumulator. Walk position u
   // visits tile phys(u).
-  const int xs = (FUSED && !tail) ? (int)((blockIdx.x % kXcds) * ((a.ntile + kXcds - 1) / kXcds)) % a.ntile : 0;
+  const int xs = (FUSED && !SPATIAL && !tail) ? (int)((blockIdx.x % kXcds) * ((a.ntile + kXcds - 1) / kXcds)) % a.ntile : 0;
   auto phys = [&](int u) { return u + xs >= a.ntile ? u + xs - a.ntile : u + xs; };
   // Fused dQ: wave w < DQ_BLOCKS forms the 32x32 block (query block dq_qb, dim block dq_db)
   // of the tile's dQ over the workgroup's 256 keys. With fewer blocks than waves (head_dim
@@ -855,16 +854,20 @@ hipError_t launch_bwd_dkdv(const DkdvArgs& a, int head_dim, hipStream_t s) {
   // Spatial: 3-D grid renumbered by XCD. Joint: 1-D grid of items, the split tail last.
   dim3 grid = spatial ? dim3(nblk + (split ? (a.text_chunks - 1) * a.text_blocks : 0), a.H, a.B)
                       : dim3(nblk * a.H * a.B + a.tail_blocks * (a.tail_chunks - 1));
-  const bool fused = !spatial && a.dq_acc;
+  const bool fused = a.dq_acc != nullptr;
   const size_t dq4 = (size_t)a.B * a.N * a.H * head_dim / 4;
   const dim3 egrid((unsigned)((dq4 + 255) / 256));
   if (fused) hipLaunchKernelGGL(zero_f32_kernel, egrid, dim3(256), 0, s, a.dq_acc, dq4);
-  if (head_dim == 128 && spatial)
+  if (head_dim == 128 && spatial && fused)
+    hipLaunchKernelGGL((bwd_dkdv_kernel<128, true, true>), grid, dim3(64 * kDkdvWaves), 0, s, a);
+  else if (head_dim == 128 && spatial)
     hipLaunchKernelGGL((bwd_dkdv_kernel<128, true, false>), grid, dim3(64 * kDkdvWaves), 0, s, a);
   else if (head_dim == 128 && fused)
     hipLaunchKernelGGL((bwd_dkdv_kernel<128, false, true>), grid, dim3(64 * kDkdvWaves), 0, s, a);
   else if (head_dim == 128)
     hipLaunchKernelGGL((bwd_dkdv_kernel<128, false, false>), grid, dim3(64 * kDkdvWaves), 0, s, a);
+  else if (spatial && fused)
+    hipLaunchKernelGGL((bwd_dkdv_kernel<64, true, true>), grid, dim3(64 * kDkdvWaves), 0, s, a);
   else if (spatial)
     hipLaunchKernelGGL((bwd_dkdv_kernel<64, true, false>), grid, dim3(64 * kDkdvWaves), 0, s, a);
   else if (fused)
