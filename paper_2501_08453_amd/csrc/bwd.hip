@@ -222,18 +222,34 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
   // LSE (+inf) makes their probabilities zero.
   auto issue = [&](int qt, int st) {
     VC_LDS char* sq = (VC_LDS char*)smem + st * STAGE;
+    // Spatial branch at head_dim 128: the lane index made opaque, so that the per-lane parts
+    // of the copy addresses are formed here instead of held across the walk; at 256
+    // registers they would be spilled, and the reload's wait, at the head of this loop,
+    // would make every copy wait for the previous one.
+    int cl = lane;
+    if constexpr (SPATIAL && D == 128) asm volatile("" : "+v"(cl));
     for (int idx = w; idx < RCOPIES; idx += kDkdvWaves) {
-      copy_row_tile<D, true, FUSED>(a.q + base, tok, qt * kBQ, N, sq, idx, lane);  // fused: perm_row order
-      copy_row_tile<D, true, FUSED>(a.dout + base, tok, qt * kBQ, N, sq + RT, idx, lane);
+      copy_row_tile<D, true, FUSED>(a.q + base, tok, qt * kBQ, N, sq, idx, cl);  // fused: perm_row order
+      copy_row_tile<D, true, FUSED>(a.dout + base, tok, qt * kBQ, N, sq + RT, idx, cl);
     }
     if constexpr (!FUSED) {
       const size_t toff = (bh * a.ntile + qt) * tile_elems(D);
       for (int idx = w; idx < TCOPIES; idx += kDkdvWaves) {
-        copy16_to_lds_opaque(a.qt + toff + idx * 512 + lane * 8, sq + 2 * RT + idx * 1024);
-        copy16_to_lds_opaque(a.dot + toff + idx * 512 + lane * 8, sq + 2 * RT + TT + idx * 1024);
+        copy16_to_lds_opaque(a.qt + toff + idx * 512 + cl * 8, sq + 2 * RT + idx * 1024);
+        copy16_to_lds_opaque(a.dot + toff + idx * 512 + cl * 8, sq + 2 * RT + TT + idx * 1024);
       }
     }
-    if (w == kDkdvWaves - 1 && lane < 32) {
+    // LSE*log2e by lanes 0-15, -D by lanes 16-31 of the last wave. Spatial branch: two
+    // copies from uniform bases, so that no per-lane pointer is held across the walk.
+    if constexpr (SPATIAL) {
+      if (w == kDkdvWaves - 1) {
+        const size_t r0 = bh * npad + qt * kBQ;
+        if (cl < 16)
+          copy16_to_lds_opaque(a.lse2 + r0 + 4 * cl, sq + 2 * RT + 2 * TT);
+        else if (cl < 32)
+          copy16_to_lds_opaque(a.dd + r0 + 4 * (cl - 16), sq + 2 * RT + 2 * TT);
+      }
+    } else if (w == kDkdvWaves - 1 && lane < 32) {
       const float* src = (lane < 16 ? a.lse2 : a.dd) + bh * npad + qt * kBQ + 4 * (lane & 15);
       copy16_to_lds_opaque(src, sq + 2 * RT + 2 * TT);
     }

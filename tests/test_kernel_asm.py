@@ -7,7 +7,10 @@ hipcc cross-compiles the device code to assembly).
 - Packed fp32 arithmetic is disabled at build time; no packed fp32 add, multiply or fma may
   appear in any kernel.
 - The hot joint-attention kernels and the long-clip temporal kernels fit their register
-  budget without scratch spills.
+  budget without scratch spills; the spatial dK/dV instances, at the limit, touch scratch
+  only outside the blocks that issue matrix-core work or LDS copies.
+- No kernel waits for vector memory between the LDS copies of a batch: a compiler-inserted
+  wait there (e.g. for a spill reload) would make each copy wait for the previous one.
 """
 import os
 import re
@@ -102,3 +105,41 @@ def test_hot_kernels_do_not_spill(device_asm, fn, kernel):
     m = re.search(r"\.name:\s+_Z\w*%s\w*\n(?:.*\n){0,40}?\s+\.vgpr_spill_count:\s+(\d+)" % kernel, text)
     assert m, kernel
     assert int(m.group(1)) == 0, (kernel, "spills", m.group(1))
+
+
+def basic_blocks(body):
+    return re.split(r"\n\.LBB\d+_\d+:", body)
+
+
+def test_no_vector_memory_wait_among_lds_copies(device_asm):
+    """In a basic block that issues LDS copies, the only vector-memory waits are the full
+    waits right before a barrier (the kernels' own wait for a stage's copies). Any other
+    vmcnt wait there, e.g. one the compiler inserts for a spill reload at the head of a
+    copy loop, waits for every copy in flight, the ones just issued included."""
+    checked = 0
+    for fn, text in device_asm.items():
+        for name, body in kernels(text):
+            for blk in basic_blocks(body):
+                ins = list(instructions(blk))
+                if not any(l.startswith("global_load_lds") for l in ins):
+                    continue
+                checked += 1
+                for i, line in enumerate(ins):
+                    if line.startswith("s_waitcnt") and "vmcnt" in line:
+                        nxt = ins[i + 1] if i + 1 < len(ins) else ""
+                        assert nxt.startswith("s_barrier"), (fn, name, line, ins[max(0, i - 3):i + 3])
+    assert checked > 0
+
+
+@pytest.mark.parametrize("kernel", ["bwd_dkdv_kernelILi128ELb1ELb1EE", "bwd_dkdv_kernelILi128ELb1ELb0EE"])
+def test_spatial_dkdv_scratch_outside_hot_blocks(device_asm, kernel):
+    """The spatial dK/dV instances (the default fused one and the deterministic one) use all
+    256 registers; what they spill is set up and read back outside the walk's blocks: no
+    basic block holds both a scratch access and a matrix-core op or an LDS copy."""
+    text = device_asm["bwd.hip"]
+    bodies = [b for n, b in kernels(text) if kernel in n]
+    assert len(bodies) == 1, kernel
+    for blk in basic_blocks(bodies[0]):
+        ins = list(instructions(blk))
+        if any(l.startswith("scratch_") for l in ins):
+            assert not any(l.startswith("v_mfma") or l.startswith("global_load_lds") for l in ins), (kernel, ins[:8])
