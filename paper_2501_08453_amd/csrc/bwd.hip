@@ -623,7 +623,9 @@ __global__ void tail_reduce_kernel(const float* part, __bf16* dk, __bf16* dv, in
   *(bf16x4*)(dv + o) = bf16x4{(__bf16)sv[0], (__bf16)sv[1], (__bf16)sv[2], (__bf16)sv[3]};
 }
 
-template <int D>
+// KM: a key mask is given (a separate instance, so that the unmasked one carries none of
+// its per-tile work).
+template <int D, bool KM>
 __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
   constexpr int RT = RowTile<D>::kBytes;      // row-major K or V tile bytes
   constexpr int RS = RowTile<D>::kStride;
@@ -682,7 +684,7 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
   rule.T = a.T;
   rule.tl = a.text_len ? min(max(a.text_len[b], 0), a.T) : a.T;
   rule.L = a.frame_len;
-  rule.km = a.key_mask ? a.key_mask + (size_t)b * N : nullptr;
+  rule.km = a.key_mask ? a.key_mask + (size_t)b * N : nullptr;  // non-null exactly when KM
   // This wave's queries (past the end of a short block: its last row).
   const int qw0 = min(rb.r0 + w * 32, rb.r1 - 1), qw1 = min(rb.r0 + w * 32 + 31, rb.r1 - 1);
   const bool wave_all_video = qw0 >= a.T && qw1 < N;
@@ -724,11 +726,18 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
 
   int kt = next_tile(max(kt0, a.kt_min));  // completing a fused backward: keys >= kt_min only
   if (kt < a.ntile) issue(kt, 0);
+  // Key-mask bytes of each tile loaded a step ahead (waited for at the barrier with the
+  // tile's copies), turned into the tile's bits there.
+  int kmb = KM && kt < a.ntile ? rule.key_mask_byte(kt, lane) : 1;
   int st = 0;
   while (kt < a.ntile) {
     const int kn = next_tile(kt + 1);
     wait_all_memory();
     __syncthreads();
+    const unsigned long long kbits = KM ? key_mask_bits(kmb) : ~0ull;
+    if (KM && kn < a.ntile) kmb = rule.key_mask_byte(kn, lane);
+    // a joint tile whose keys are all real (no padding, no text cut): masked by its bits only
+    const bool plain_tile = KM && rule.L == 0 && kt * kBN + kBN <= N && (kt * kBN >= a.T || kt * kBN + kBN <= rule.tl);
     const VC_LDS char* k_lds = (const VC_LDS char*)smem + st * STAGE;
     const VC_LDS char* v_lds = k_lds + RT;
     const VC_LDS char* kt_lds = k_lds + 2 * RT;
@@ -761,11 +770,15 @@ __global__ __launch_bounds__(64 * kDqWaves, 1) void bwd_dq_kernel(DqArgs a) {
       float ds[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) ds[r] = fast_exp2(fmaf(s[r], a.scale_log2, -lse2));
-      if (need_mask) {  // branch-free per element; the mask byte is loaded unconditionally
+      if (need_mask && plain_tile) {  // joint tile of real keys: the key mask's bits alone
+        const unsigned bits = (unsigned)(kbits >> (32 * kb)) >> (4 * hi);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) ds[r] = ((bits >> (8 * (r >> 2) + (r & 3))) & 1u) ? ds[r] : 0.0f;
+      } else if (need_mask) {  // branch-free per element; the key mask from the tile's bits
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int key = k0 + kb * 32 + acc_row(r, hi);
-          bool ok = rule.key_valid(key);
+          bool ok = KM ? rule.key_valid_bits(key, k0, kbits) : rule.key_valid(key);
           if (rule.L) ok = ok & qrange.ok(key, a.T);
           ds[r] = ok ? ds[r] : 0.0f;
         }
@@ -925,10 +938,15 @@ hipError_t launch_bwd_dq(const DqArgs& a, int head_dim, hipStream_t s) {
   const int nblk = row_blocks(a.N, a.T, a.frame_len, kDqBM, false);
   // Spatial: 3-D grid renumbered by XCD. Joint: 1-D grid of items, the split tail last.
   dim3 grid = a.frame_len ? dim3(nblk, a.H, a.B) : dim3(nblk * a.H * a.B + a.tail_blocks * (a.tail_chunks - 1));
-  if (head_dim == 128)
-    hipLaunchKernelGGL(bwd_dq_kernel<128>, grid, dim3(64 * kDqWaves), 0, s, a);
+  const bool km = a.key_mask != nullptr;
+  if (head_dim == 128 && km)
+    hipLaunchKernelGGL((bwd_dq_kernel<128, true>), grid, dim3(64 * kDqWaves), 0, s, a);
+  else if (head_dim == 128)
+    hipLaunchKernelGGL((bwd_dq_kernel<128, false>), grid, dim3(64 * kDqWaves), 0, s, a);
+  else if (km)
+    hipLaunchKernelGGL((bwd_dq_kernel<64, true>), grid, dim3(64 * kDqWaves), 0, s, a);
   else
-    hipLaunchKernelGGL(bwd_dq_kernel<64>, grid, dim3(64 * kDqWaves), 0, s, a);
+    hipLaunchKernelGGL((bwd_dq_kernel<64, false>), grid, dim3(64 * kDqWaves), 0, s, a);
   if (!a.frame_len && a.tail_blocks > 0) {
     const size_t threads = (size_t)a.tail_blocks * kDqBM * (head_dim / 4);
     dim3 rgrid((unsigned)((threads + 255) / 256));

@@ -140,6 +140,10 @@ __device__ __forceinline__ void interleave_mfma_valu() {
   }
 }
 
+// Bits of a tile's key mask from the lanes' bytes (AttendRule::key_mask_byte): bit i = the
+// byte of lane i is non-zero. Wave-uniform.
+__device__ __forceinline__ unsigned long long key_mask_bits(int byte) { return __ballot(byte != 0); }
+
 // Value of lane l^32 (the other half of the wave).
 __device__ __forceinline__ float swap_halves(float x) { return __shfl_xor(x, 32, 64); }
 
@@ -245,6 +249,18 @@ struct AttendRule {
     bool ok = (j < N) & ((j >= T) | (j < tl));
     if (km) ok = ok & (km[min(j, N - 1)] != 0);  // unconditional clamped load
     return ok;
+  }
+  // The same for key j of the 64-key tile starting at k0, with the key mask of that tile
+  // given as bits (bit i: key k0 + i kept; all ones without a mask), so that a per-element
+  // test needs no load.
+  __device__ __forceinline__ bool key_valid_bits(int j, int k0, unsigned long long bits) const {
+    return (j < N) & ((j >= T) | (j < tl)) & (((bits >> (j - k0)) & 1ull) != 0);
+  }
+  // Lane `lane`'s byte of the key mask of tile kt (key kt*64 + lane, clamped to N-1), for
+  // key_mask_bits; 1 without a mask (no load). Loaded a tile ahead of its use, so that its
+  // wait is the one before the barrier at which that tile's copies have landed.
+  __device__ __forceinline__ int key_mask_byte(int kt, int lane) const {
+    return km ? (int)km[min(kt * kTileTok + lane, N - 1)] : 1;
   }
   // Key tiles a workgroup of queries [q0, q1) visits; uniform across the workgroup. Joint:
   // all but tiles of padded text only (when there is no key_mask). Spatial: the real text

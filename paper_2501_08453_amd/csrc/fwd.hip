@@ -115,15 +115,27 @@ struct KeyMask {
     return !(wave_one_frame && k0 >= wqs && k0 + kBN <= wqs + r.L);
   }
   // Sets scores of keys this lane's query does not attend to to -inf. Branch-free per
-  // element: the tests are plain arithmetic and the optional mask byte is loaded
-  // unconditionally (clamped index).
-  __device__ __forceinline__ void apply(f32x16* s, int k0, int hi) const {
+  // element: the tests are plain arithmetic, the key mask the tile's bits
+  // (key_mask_bits).
+  template <bool KM>
+  __device__ __forceinline__ void apply(f32x16* s, int k0, int hi, unsigned long long kbits) const {
+    if (KM && rule.L == 0 && k0 + kBN <= rule.N && (k0 >= rule.T || k0 + kBN <= rule.tl)) {
+      // Joint tile of real keys (no padding, no text cut): the key mask's bits alone.
+      // Register r of key block kb holds key kb*32 + 8*(r/4) + 4*hi + r%4 of the tile.
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const unsigned bits = (unsigned)(kbits >> (32 * kb)) >> (4 * hi);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[kb][r] = ((bits >> (8 * (r >> 2) + (r & 3))) & 1u) ? s[kb][r] : -INFINITY;
+      }
+      return;
+    }
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int key = k0 + kb * 32 + acc_row(r, hi);
-        bool ok = rule.key_valid(key);
+        bool ok = KM ? rule.key_valid_bits(key, k0, kbits) : rule.key_valid(key);
         if (rule.L) ok = ok & qr.ok(key, rule.T);
         s[kb][r] = ok ? s[kb][r] : -INFINITY;
       }
@@ -182,7 +194,9 @@ __device__ __forceinline__ void load_vt_chunk(const VC_LDS char* vt_lds, int c, 
     f[db] = *(const VC_LDS bf16x8*)(vt_lds + ((db * 32 + l32) * kTileRow + (c >> 1) * 32 + 16 * (c & 1) + 8 * hi) * 2);
 }
 
-template <int D>
+// KM: a key mask is given (a separate instance, so that the unmasked one carries none of
+// its per-tile work).
+template <int D, bool KM>
 __global__ __launch_bounds__(64 * kWaves, kWavesPerSimd * 4 / kWaves) void fwd_kernel(FwdArgs a) {
   constexpr int KT = FwdTile<D>::KT;
   constexpr int VTB = FwdTile<D>::VTB;
@@ -234,7 +248,7 @@ __global__ __launch_bounds__(64 * kWaves, kWavesPerSimd * 4 / kWaves) void fwd_k
   mask.rule.T = a.T;
   mask.rule.tl = a.text_len ? min(max(a.text_len[b], 0), a.T) : a.T;
   mask.rule.L = a.frame_len;
-  mask.rule.km = a.key_mask ? a.key_mask + (size_t)b * N : nullptr;
+  mask.rule.km = a.key_mask ? a.key_mask + (size_t)b * N : nullptr;  // non-null exactly when KM
   mask.qr = query_range(mask.rule, qi);
   {
     // This wave's queries; a wave past the end of a short block takes its last row, so that
@@ -297,13 +311,18 @@ __global__ __launch_bounds__(64 * kWaves, kWavesPerSimd * 4 / kWaves) void fwd_k
     issue_k(cur, 0);
     issue_v(cur, 0);
     if (nxt < a.ntile) issue_k(nxt, 1);
+    // Key-mask bytes of `cur` now and of each next tile a step ahead: their waits are the
+    // ones before the barriers (a byte loaded and used in the same step would wait for the
+    // step's tile copies too).
+    const int kmb_cur = KM ? mask.rule.key_mask_byte(cur, lane) : 1;
+    int kmb_nxt = KM && nxt < a.ntile ? mask.rule.key_mask_byte(nxt, lane) : 1;
     wait_all_memory();
     __syncthreads();
     // Prologue: scores and softmax of the first tile.
     {
       f32x16 s[2];
       scores<D>(k_slot(0), qf, l32, hi, s);
-      if (mask.tile_needs_mask(cur * kBN)) mask.apply(s, cur * kBN, hi);
+      if (mask.tile_needs_mask(cur * kBN)) mask.apply<KM>(s, cur * kBN, hi, KM ? key_mask_bits(kmb_cur) : ~0ull);
       raise_base(s, a.scale_log2, true, m, pb, l);
     }
     // Pending rescale of O: probabilities computed against a raised base must only be
@@ -319,6 +338,8 @@ __global__ __launch_bounds__(64 * kWaves, kWavesPerSimd * 4 / kWaves) void fwd_k
       wait_all_memory();
       __syncthreads();  // K of `nxt` and V^T of `cur` landed; K of `cur` and V^T of the
                         // previous tile are no longer read by any wave
+      const unsigned long long kbits = KM ? key_mask_bits(kmb_nxt) : ~0ull;  // key mask of `nxt`
+      if (KM && nn < a.ntile) kmb_nxt = mask.rule.key_mask_byte(nn, lane);
       if (__any(raise)) {
 #pragma unroll
         for (int i = 0; i < D / 32; ++i) oacc[i] *= alpha;
@@ -330,7 +351,7 @@ __global__ __launch_bounds__(64 * kWaves, kWavesPerSimd * 4 / kWaves) void fwd_k
         if (nn < a.ntile) k_copy(j, nn, par);
         v_copy(j, nxt, par ^ 1);
       });
-      if (mask.tile_needs_mask(nxt * kBN)) mask.apply(s, nxt * kBN, hi);
+      if (mask.tile_needs_mask(nxt * kBN)) mask.apply<KM>(s, nxt * kBN, hi, kbits);
       // P V of `cur` in four chunks of D/32 products; between them the vector ALUs do
       // the softmax of `nxt`: first its new base, then one operand's probabilities per
       // chunk. Fragments of the next chunk are read one chunk ahead.
@@ -458,10 +479,15 @@ hipError_t launch_fwd(const FwdArgs& a, int head_dim, hipStream_t s) {
   const int nblk = row_blocks(a.N, a.T, a.frame_len, kBM, false);
   // Spatial: 3-D grid renumbered by XCD. Joint: 1-D grid of items, the split tail last.
   dim3 grid = a.frame_len ? dim3(nblk, a.H, a.B) : dim3(nblk * a.H * a.B + a.tail_blocks * (a.tail_chunks - 1));
-  if (head_dim == 128)
-    hipLaunchKernelGGL(fwd_kernel<128>, grid, dim3(64 * kWaves), 0, s, a);
+  const bool km = a.key_mask != nullptr;
+  if (head_dim == 128 && km)
+    hipLaunchKernelGGL((fwd_kernel<128, true>), grid, dim3(64 * kWaves), 0, s, a);
+  else if (head_dim == 128)
+    hipLaunchKernelGGL((fwd_kernel<128, false>), grid, dim3(64 * kWaves), 0, s, a);
+  else if (km)
+    hipLaunchKernelGGL((fwd_kernel<64, true>), grid, dim3(64 * kWaves), 0, s, a);
   else
-    hipLaunchKernelGGL(fwd_kernel<64>, grid, dim3(64 * kWaves), 0, s, a);
+    hipLaunchKernelGGL((fwd_kernel<64, false>), grid, dim3(64 * kWaves), 0, s, a);
   if (!a.frame_len && a.tail_blocks > 0) {
     const size_t threads = (size_t)a.tail_blocks * kBM * (head_dim / 4);
     dim3 rgrid((unsigned)((threads + 255) / 256));

@@ -87,12 +87,14 @@ def test_no_packed_fp32_arithmetic(device_asm):
 
 
 HOT = [
-    ("fwd.hip", "fwd_kernelILi128EE"),
-    ("fwd.hip", "fwd_kernelILi64EE"),
+    ("fwd.hip", "fwd_kernelILi128ELb0EE"),
+    ("fwd.hip", "fwd_kernelILi64ELb0EE"),
+    ("fwd.hip", "fwd_kernelILi128ELb1EE"),  # with a key mask
     ("bwd.hip", "bwd_dkdv_kernelILi128ELb0ELb1EE"),  # fused joint dK/dV (+dQ)
     ("bwd.hip", "bwd_dkdv_kernelILi128ELb0ELb0EE"),  # separate joint dK/dV
-    ("bwd.hip", "bwd_dq_kernelILi128EE"),
-    ("bwd.hip", "bwd_dq_kernelILi64EE"),
+    ("bwd.hip", "bwd_dq_kernelILi128ELb0EE"),
+    ("bwd.hip", "bwd_dq_kernelILi64ELb0EE"),
+    ("bwd.hip", "bwd_dq_kernelILi128ELb1EE"),
     ("temporal_long.hip", "temporal_long_fwd_kernelILi128ELb0EE"),  # clips of 33-144 frames
     ("temporal_long.hip", "temporal_long_fwd_kernelILi128ELb1EE"),
     ("temporal_long.hip", "temporal_long_bwd_kernelILi128EE"),
