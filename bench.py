@@ -172,12 +172,11 @@ def cpu_baseline(w, g, text_len, target_s):
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_bwd_dkdv_long720p.json")
 KERNEL_SOURCES = ["paper_2501_08453_amd/csrc/bwd.hip", "paper_2501_08453_amd/csrc/common.hpp"]
-# Traffic records of the temporal backward, per workload: the short-clip kernel (with its
-# preparation pass) at the long workload, the long-clip kernel at the 144-frame clip.
+# Traffic records of the temporal backward, per workload: the short-clip kernel at the long
+# workload, the long-clip kernel at the 144-frame clip.
 TEMPORAL_TRAFFIC = {
     3: (os.path.join(ROOT, "profiles", "traffic_temporal_bwd_long720p.json"),
-        ["paper_2501_08453_amd/csrc/temporal.hip", "paper_2501_08453_amd/csrc/bwd.hip",
-         "paper_2501_08453_amd/csrc/common.hpp"]),
+        ["paper_2501_08453_amd/csrc/temporal.hip", "paper_2501_08453_amd/csrc/common.hpp"]),
     6: (os.path.join(ROOT, "profiles", "traffic_temporal_bwd_clip144f.json"),
         ["paper_2501_08453_amd/csrc/temporal_long.hip", "paper_2501_08453_amd/csrc/common.hpp"]),
 }
@@ -407,8 +406,6 @@ def branch_main(args, w, g, text_len, tl, desc, o, lse, dq, dk, dv, fws, ws, str
     q, k, v, do = g["q"], g["k"], g["v"], g["do"]
     sh = stream.cuda_stream
     B, N, H, D = w.shape
-    if args.branch == "temporal":
-        tws = vc._workspace(vc.vc_temporalattn_bwd_workspace_bytes(desc), q.device)
 
     def step(ev=None):
         if ev:
@@ -422,7 +419,7 @@ def branch_main(args, w, g, text_len, tl, desc, o, lse, dq, dk, dv, fws, ws, str
         if args.branch == "spatial":
             vc.vc_spatialattn_bwd(desc, q, k, v, o, lse, do, tl, None, dq, dk, dv, ws, ws.numel(), sh)
         else:
-            vc.vc_temporalattn_bwd(desc, q, k, v, o, lse, do, None, dq, dk, dv, tws, tws.numel(), sh)
+            vc.vc_temporalattn_bwd(desc, q, k, v, o, lse, do, None, dq, dk, dv, None, 0, sh)
         if ev:
             ev[2].record(stream)
 
@@ -444,11 +441,15 @@ def branch_main(args, w, g, text_len, tl, desc, o, lse, dq, dk, dv, fws, ws, str
         a_fwd, a_bwd = temporal_bytes(w)
         scale, unit, peak, bound, metric = 1e9, "GB/s", PEAK_HBM_GBS, "hbm", METRIC_TEMPORAL
     value = (a_fwd + a_bwd) / (ms_step * 1e-3) / scale
-    # Dominant call: the backward (one call: preparation and gradient kernels; for clips of
-    # more than 32 frames one persistent kernel that forms D and LSE*log2(e) itself).
-    long_clip = args.branch == "temporal" and w.frames > 32
-    bwd_label = ("temporal backward (one persistent kernel, D and LSE*log2(e) formed inside)" if long_clip
-                 else "%s backward (prepare + gradient kernels)" % args.branch)
+    # Dominant call: the backward (spatial: preparation and gradient kernels; temporal: one
+    # gradient kernel that forms D and LSE*log2(e) itself, persistent for clips of more than
+    # 32 frames, after the text-row fill).
+    if args.branch == "spatial":
+        bwd_label = "spatial backward (prepare + gradient kernels)"
+    elif w.frames > 32:
+        bwd_label = "temporal backward (one persistent kernel, D and LSE*log2(e) formed inside)"
+    else:
+        bwd_label = "temporal backward (gradient kernel, D and LSE*log2(e) formed inside)"
     bwd_rate = a_bwd / (k_bwd * 1e-3) / scale
     line = {
         "metric": metric, "value": round(value, 2), "unit": unit, "n_gpus": 1, "steps": args.steps,

@@ -62,7 +62,7 @@ extern "C" {
 /* Raised with every change of a signature, a struct, the meaning of an argument or a
  * documented result; the Python binding refuses a library that reports another
  * version. */
-#define VC_JOINTATTN_ABI_VERSION 8
+#define VC_JOINTATTN_ABI_VERSION 9
 
 typedef enum vc_status {
   VC_OK = 0,
@@ -305,15 +305,16 @@ vc_status vc_temporalattn_fwd_sum(const vc_jointattn_desc* desc,
                                   const void* o_joint, const void* o_spatial,
                                   void* o, float* lse, void* out, void* stream);
 
-/* Bytes of device workspace the temporal backward needs: per row fp32 -D and
- * LSE*log2(e) ([B,H,Npad]). 0 for an invalid descriptor. Host only. With F > 32
- * the backward forms both inside its kernel and neither reads nor checks the
- * workspace (it may be NULL). */
+/* Bytes of device workspace the temporal backward was documented to need (per
+ * row fp32 -D and LSE*log2(e), [B,H,Npad]); 0 for an invalid descriptor. Host
+ * only. Kept for callers that size the argument with it: the backward forms both
+ * values inside its kernels and neither reads nor checks the workspace (it may be
+ * NULL). */
 size_t vc_temporalattn_bwd_workspace_bytes(const vc_jointattn_desc* desc);
 
 /* Temporal backward: dq, dk, dv from q, k, v, the temporal forward's o and lse
- * and dout. `workspace`: caller-owned device memory of at least
- * vc_temporalattn_bwd_workspace_bytes(desc) bytes, 256-byte aligned. */
+ * and dout. `workspace` and `workspace_bytes` are not used (any value, NULL
+ * included). */
 vc_status vc_temporalattn_bwd(const vc_jointattn_desc* desc,
                               const void* q, const void* k, const void* v,
                               const void* o, const float* lse, const void* dout,

@@ -18,7 +18,7 @@ HEADER = os.path.join(os.path.dirname(PKG_DIR), "include", "vc_jointattn.h")
 # The ABI the signatures below describe (VC_JOINTATTN_ABI_VERSION of include/vc_jointattn.h);
 # a library reporting another version is refused, so that no call can reach an entry point
 # whose arguments differ from what this binding passes.
-ABI_VERSION = 8
+ABI_VERSION = 9
 # Bytes of the no-allocation forward's fixed scratch array (VC_JOINTATTN_NOALLOC_SCRATCH_BYTES).
 NOALLOC_SCRATCH_BYTES = 256 << 20
 
@@ -466,9 +466,9 @@ def temporal_bwd(q, k, v, o, lse, dout, desc, key_mask=None, ws=None):
     """Temporal branch (dq, dk, dv)."""
     import torch
     _check_joint_inputs(desc, (("q", q), ("k", k), ("v", v), ("o", o), ("dout", dout)), None, key_mask, lse)
-    ws = _workspace(vc_temporalattn_bwd_workspace_bytes(desc), q.device) if ws is None else ws
     dq, dk, dv = (torch.empty_like(q) for _ in range(3))
-    vc_temporalattn_bwd(desc, q, k, v, o, lse, dout, key_mask, dq, dk, dv, ws, ws.numel())
+    # the library reads no workspace for this branch; one passed in is handed through unused
+    vc_temporalattn_bwd(desc, q, k, v, o, lse, dout, key_mask, dq, dk, dv, ws, 0 if ws is None else ws.numel())
     return dq, dk, dv
 
 

@@ -687,7 +687,8 @@ size_t vc_temporalattn_bwd_workspace_bytes(const vc_jointattn_desc* desc) {
 
 vc_status vc_temporalattn_bwd(const vc_jointattn_desc* desc, const void* q, const void* k, const void* v,
                               const void* o, const float* lse, const void* dout, const uint8_t* key_mask, void* dq,
-                              void* dk, void* dv, void* workspace, size_t workspace_bytes, void* stream) {
+                              void* dk, void* dv, void* /*workspace*/, size_t /*workspace_bytes*/,
+                              void* stream) {
   int64_t n = 0;
   vc_status st = check_desc(desc, &n);
   if (st != VC_OK) return st;
@@ -697,8 +698,6 @@ vc_status vc_temporalattn_bwd(const vc_jointattn_desc* desc, const void* q, cons
       !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
     return VC_ERR_ALIGN;
   const bool long_clip = desc->frames > vcja::kMaxTemporalFramesShort;
-  const size_t rb = rows_bytes(desc, n);
-  if (!long_clip && (st = check_ws(workspace, workspace_bytes, 2 * rb)) != VC_OK) return st;
   if ((st = check_device()) != VC_OK) return st;
   vcja::TemporalArgs a = temporal_args(desc, n);
   a.q = bf(q);
@@ -712,20 +711,12 @@ vc_status vc_temporalattn_bwd(const vc_jointattn_desc* desc, const void* q, cons
   hipStream_t s = as_stream(stream);
   if (vcja::launch_text_rows(a.o, a.dk, a.dv, nullptr, a.B, a.H, a.N, a.T, desc->head_dim, s) != hipSuccess)
     return VC_ERR_HIP;
-  if (long_clip) {  // -D and LSE*log2(e) are formed inside the kernel: no workspace
-    a.lse = const_cast<float*>(lse);
-    a.o_in = bf(o);
+  // -D and LSE*log2(e) are formed inside the kernels from o and lse: no workspace.
+  a.lse = const_cast<float*>(lse);
+  a.o_in = bf(o);
+  if (long_clip)
     return vcja::launch_temporal_long_bwd(a, desc->head_dim, device_cus(), s) == hipSuccess ? VC_OK : VC_ERR_HIP;
-  }
-  float* dd = static_cast<float*>(workspace);
-  float* lse2 = reinterpret_cast<float*>(static_cast<char*>(workspace) + rb);
-  a.lse2 = lse2;
-  a.dd = dd;
-  if (vcja::launch_bwd_prepare(bf(o), lse, bf(dout), dd, lse2, a.B, a.H, a.N, a.npad, desc->head_dim, s) !=
-          hipSuccess ||
-      vcja::launch_temporal_bwd(a, desc->head_dim, s) != hipSuccess)
-    return VC_ERR_HIP;
-  return VC_OK;
+  return vcja::launch_temporal_bwd(a, desc->head_dim, s) == hipSuccess ? VC_OK : VC_ERR_HIP;
 }
 
 }  // extern "C"

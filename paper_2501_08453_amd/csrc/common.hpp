@@ -405,11 +405,9 @@ struct TemporalArgs {
   const __bf16* v;
   const __bf16* dout;   // backward only
   const uint8_t* key_mask;
-  const float* lse2;    // backward: LSE * log2(e) per token, +inf where there is none, [B, H, Npad]
-  const float* dd;      // backward: -D = -rowsum(dO o O), [B, H, Npad]
   __bf16* o;            // forward output / backward dQ
-  float* lse;           // forward output; backward of long clips: the forward's LSE (input)
-  const __bf16* o_in;   // backward of long clips: the forward's O (for D = rowsum(dO o O))
+  float* lse;           // forward output; backward: the forward's LSE (input)
+  const __bf16* o_in;   // backward: the forward's O (for D = rowsum(dO o O))
   __bf16* dk;           // backward
   __bf16* dv;           // backward
   // Forward with the branch sum fused into the epilogue (sum_out non-NULL): also writes
@@ -438,8 +436,8 @@ hipError_t launch_bwd_dq(const DqArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_dq_from_acc(const float* acc, __bf16* dq, size_t n, float scale, hipStream_t s);
 hipError_t launch_temporal_fwd(const TemporalArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_temporal_bwd(const TemporalArgs& a, int head_dim, hipStream_t s);
-// Long clips (F > 32): persistent grid of at most `cus` workgroups; the backward forms
-// -D and LSE*log2(e) itself (no lse2 / dd inputs).
+// Long clips (F > 32): persistent grid of at most `cus` workgroups. The backwards (both
+// lengths) form -D and LSE*log2(e) themselves from o_in and lse.
 hipError_t launch_temporal_long_fwd(const TemporalArgs& a, int head_dim, int cus, hipStream_t s);
 hipError_t launch_temporal_long_bwd(const TemporalArgs& a, int head_dim, int cus, hipStream_t s);
 // out = a + b + c over rows [0, rows) of every sample of [B, N, H, D] tensors (row_elems =

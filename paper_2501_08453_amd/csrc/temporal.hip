@@ -212,7 +212,6 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_bwd_kernel(Tempo
   if (sm.l0 >= a.L) return;  // whole wave
   const size_t tok = (size_t)a.H * D;
   const size_t base = (size_t)b * a.N * tok + (size_t)h * D;
-  const size_t rbase = ((size_t)b * a.H + h) * a.npad;
   const uint8_t* km = a.key_mask ? a.key_mask + (size_t)b * a.N : nullptr;
 
   const int s = l32;  // this lane's slot (query in one orientation, key in the other)
@@ -220,6 +219,7 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_bwd_kernel(Tempo
   const bool s_ok = sm.ok(s);
   const int n = sm.token(s);
   bf16x8 qf[D / 16], kf[D / 16], vf[D / 16], dof[D / 16];
+  float dsum = 0.0f;  // this half's share of D = <dO, O> of the slot's token
 #pragma unroll
   for (int ks = 0; ks < D / 16; ++ks) {
     const size_t off = base + (size_t)n * tok + 16 * ks + 8 * hi;
@@ -227,13 +227,22 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_bwd_kernel(Tempo
     kf[ks] = *(const bf16x8*)(a.k + off);
     vf[ks] = *(const bf16x8*)(a.v + off);
     dof[ks] = *(const bf16x8*)(a.dout + off);
+    const bf16x8 of = *(const bf16x8*)(a.o_in + off);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) dsum = fmaf((float)dof[ks][e], (float)of[e], dsum);
     const int e = s * (D + kRowPad) + 16 * ks + 8 * hi;
     *(VC_LDS bf16x8*)(k_rows + e) = kf[ks];
     *(VC_LDS bf16x8*)(do_rows + e) = dof[ks];
   }
+  // -D and LSE*log2(e) of the slot's token, formed here from O and the forward's LSE (no
+  // preparation pass): LSE*log2(e) is +inf where the token has no valid key or the slot
+  // none, so that its probabilities vanish.
+  const float lse_n = a.lse[((size_t)b * a.H + h) * a.N + n];
+  const float l2 = (s_ok && lse_n != -INFINITY) ? lse_n * kLog2e : INFINITY;
+  const float d = s_ok ? -halves_sum(dsum) : 0.0f;
   if (hi == 0) {
-    lse_slot[s] = a.lse2[rbase + n];
-    nd_slot[s] = a.dd[rbase + n];
+    lse_slot[s] = l2;
+    nd_slot[s] = d;
   }
   // LDS rows of the slots an operand element t of k-step st refers to.
   int grow[2][8];
@@ -250,8 +259,6 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_bwd_kernel(Tempo
       sacc = mfma32(kf[ks], qf[ks], sacc);
       pacc = mfma32(vf[ks], dof[ks], pacc);
     }
-    const float l2 = s_ok ? a.lse2[rbase + n] : INFINITY;
-    const float d = s_ok ? a.dd[rbase + n] : 0.0f;
     float ds[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {

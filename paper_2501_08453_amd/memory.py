@@ -158,7 +158,6 @@ class BlockStack:
         self.fws = vc.fwd_workspace(desc, dev)
         self.ws_j = vc.workspace(desc, dev)
         self.ws_s = vc.spatial_workspace(desc, dev)
-        self.ws_t = vc._workspace(vc.vc_temporalattn_bwd_workspace_bytes(desc), dev)
 
         def new_set():  # O, LSE of the joint, spatial and temporal branches
             s = []
@@ -203,7 +202,7 @@ class BlockStack:
         sh = stream.cuda_stream
         vc.vc_jointattn_bwd(d, q, k, v, o_j, l_j, dout, self.tl, self.km, *g[0], self.ws_j, self.ws_j.numel(), sh)
         vc.vc_spatialattn_bwd(d, q, k, v, o_s, l_s, dout, self.tl, self.km, *g[1], self.ws_s, self.ws_s.numel(), sh)
-        vc.vc_temporalattn_bwd(d, q, k, v, o_t, l_t, dout, self.km, *g[2], self.ws_t, self.ws_t.numel(), sh)
+        vc.vc_temporalattn_bwd(d, q, k, v, o_t, l_t, dout, self.km, *g[2], None, 0, sh)
 
     def _store(self, i, stream):
         for h, t in zip(self.host[i], self.sets[i]):
