@@ -232,8 +232,8 @@ vc_status vc_jointattn_bwd_fused(const vc_jointattn_desc* desc,
 
 /* ---------------------------------------------------------------------------
  * Spatial attention branch (Sec. III-B: the video sequence [B, F, L, ...]
- * regrouped as [B*F, L, ...], L = Hp*Wp, each frame on its own; text tokens are
- * concatenated to the spatial sequence for attention, Sec. V-B). Computed in
+ * regrouped as [B*F, L, ...], L = Hp*Wp, each frame on its own; the text tokens
+ * join every frame's keys, Sec. V-B). Computed in
  * place on the joint layout: a video query of frame f attends to the valid text
  * keys and the valid keys of frame f, rows [T + f*L, T + (f+1)*L) (validity as
  * for the joint branch: text_len, key_mask). Text rows are not queries of this
@@ -323,9 +323,8 @@ vc_status vc_temporalattn_bwd(const vc_jointattn_desc* desc,
                               void* workspace, size_t workspace_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
- * Branch sum (Sec. III-B: the outputs of the spatial, temporal and
- * full-sequence branches are added element-wise to form the block's attention
- * output). The backward of the sum needs no kernel: every branch's backward
+ * Branch sum (Sec. III-B: a block's attention output is the element-wise sum
+ * of its three branch results, spatial, temporal and joint). The backward of the sum needs no kernel: every branch's backward
  * takes the same dout.
  * ------------------------------------------------------------------------- */
 

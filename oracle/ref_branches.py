@@ -9,9 +9,10 @@ block has a spatial and a temporal attention branch, obtained by regrouping
 the video tokens of the [B, F, L, ...] video sequence (F frames of L tokens):
 spatial attention runs on [B*F, L, ...] (each frame on its own) and temporal
 attention on [B*L, F, ...] (each spatial position across the frames); the
-three branch outputs are then added element-wise. Text tokens are
-concatenated to the spatial sequence for attention (Sec. V-B, intra-node
-sequence-parallel workflow).
+three branch outputs are then added element-wise. The spatial branch also
+attends to the text tokens, which join each frame's key set (Sec. V-B,
+intra-node sequence-parallel workflow, where text is sharded together with the
+spatial sequence for that reason).
 
 Both branches act on the joint layout [B, N, H, D], N = T + F*L, with the
 text slot first and video tokens frame-major (token T + f*L + l is frame f,

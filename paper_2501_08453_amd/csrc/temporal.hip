@@ -185,170 +185,235 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_fwd_kernel(Tempo
   }
 }
 
-// Backward. LSE*log2(e) and -D = -rowsum(dO o O) per token come from the preparation pass
-// ([B, H, npad], +inf / 0 where a row has no key). Two orientations of the same block:
-// lane = query (S^T, dP^T, dS^T) gives dQ^T = c K^T dS^T; lane = key (S, dP, dS) gives
-// dV^T = dO^T P and dK^T = c Q^T dS. The transposed A operands are gathered in the slot
-// order the accumulator layout produces.
+// Row tiles of a group's 32 slots in LDS, for the backward: slot s sits in row perm_row(s)
+// (the permuted order of the joint backward, so that the transposing reads of four
+// consecutive slots hit distinct banks) with one 16-byte pad chunk per row (the rows one
+// quarter-wave reads at a common column fall on distinct banks), filled by whole 1 KiB wave
+// copies in which 64 lanes read consecutive 16-byte chunks of a few token rows.
 template <int D>
-__global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_bwd_kernel(TemporalArgs a) {
-  // Per wave: K rows of its 32 slots (the dQ part), later Q rows in the same place (the
-  // dK/dV part), dO rows; then LSE*log2e and -D of the slots. Two workgroups fit a CU.
-  __shared__ __attribute__((aligned(16))) __bf16 stage[kWavesPerBlock * 2 * stage_elems<D>()];
-  __shared__ float stat[kWavesPerBlock * 2 * kSlots];
+struct SlotTile {
+  static constexpr int CH = D / 8 + 1;                     // 16-byte chunks per row, pad included
+  static constexpr int RS = CH * 16;                       // row stride (bytes)
+  static constexpr int COPIES = (kSlots * CH + 63) / 64;   // wave copies per tensor
+  static constexpr int REGION = COPIES * 1024;             // LDS bytes per tensor
+};
+
+// Issues wave copy `idx` of the 32 slot rows of one tensor (token row n at src + n*tok) into
+// `dst`. `tk` holds the token row of slot l32 in lane l32. Lanes past the last row repeat
+// one of its chunks (their bytes land in the region's tail, which nothing reads); the pad
+// chunk of a row repeats the row's last chunk.
+template <int D>
+__device__ __forceinline__ void copy_slot_rows(const __bf16* src, size_t tok, int tk, VC_LDS char* dst, int idx,
+                                               int lane) {
+  constexpr int CH = SlotTile<D>::CH;
+  const int lin = idx * 64 + lane;
+  const int r = lin / CH;
+  const int c = min(lin - r * CH, CH - 2);
+  const int n = __shfl(tk, perm_row(min(r, kSlots - 1)));
+  copy16_to_lds_opaque(src + (size_t)n * tok + c * 8, dst + idx * 1024);
+}
+
+// MFMA operand from slot rows (m = slot l32, k = dims 16*ks + 8*hi .. +7).
+template <int D>
+__device__ __forceinline__ bf16x8 slot_rows(const VC_LDS char* t, int ks, int lane) {
+  return *(const VC_LDS bf16x8*)(t + perm_row(lane & 31) * SlotTile<D>::RS + (2 * ks + (lane >> 5)) * 16);
+}
+
+// MFMA operand whose contraction runs over slots (m = dim db*32 + l32, k = slots
+// 16*st + 8*(t/4) + 4*hi + t%4, the order an accumulator column holds them): two transposing
+// reads of 4 slots each; lane 4e+g of a group of 16 supplies the address of slot r0 + e and
+// 4 dims.
+template <int D>
+__device__ __forceinline__ bf16x8 slot_cols(const VC_LDS char* t, int st, int db, int lane) {
+  const int e = (lane & 15) >> 2;
+  const int col = (db * 32 + 16 * ((lane >> 4) & 1) + 4 * (lane & 3)) * 2;
+  const int r0 = 16 * st + 4 * (lane >> 5) + e;
+  const bf16x4 x = lds_read_tr(t + perm_row(r0) * SlotTile<D>::RS + col);
+  const bf16x4 y = lds_read_tr(t + perm_row(r0 + 8) * SlotTile<D>::RS + col);
+  return cat4(x, y);
+}
+
+// Backward: one workgroup of two waves per group of G positions (32 slots) of one (sample,
+// head), head fastest over the grid, so that concurrent workgroups read whole token rows.
+// Q, K, V and dO rows are copied into LDS row tiles by whole-row wave copies; D = <dO, O>
+// (O read as whole rows) and LSE*log2(e) of every slot are formed first and shared through
+// LDS. Wave 0 takes the lane-per-query orientation (S^T = K Q^T, dP^T = V dO^T, dS^T) and
+// forms dQ^T = c K^T dS^T; wave 1 the lane-per-key one (S, dP, dS) and forms dV^T = dO^T P
+// and dK^T = c Q^T dS. The results go back through the tiles so that every global store is
+// a whole 16-byte chunk of a row.
+template <int D>
+__global__ __launch_bounds__(128) void temporal_bwd_kernel(TemporalArgs a) {
+  using Tile = SlotTile<D>;
+  constexpr int LPR = D / 8;   // lanes per row in a whole-row access
+  constexpr int RPI = 64 / LPR;  // rows per whole-row wave access
+  __shared__ __attribute__((aligned(1024))) char smem[4 * Tile::REGION + 2 * kSlots * 4];
+  VC_LDS char* const q_t = (VC_LDS char*)smem;
+  VC_LDS char* const k_t = q_t + Tile::REGION;
+  VC_LDS char* const v_t = k_t + Tile::REGION;
+  VC_LDS char* const do_t = v_t + Tile::REGION;
+  VC_LDS float* const lse_slot = (VC_LDS float*)(do_t + Tile::REGION);  // LSE*log2(e), +inf if none
+  VC_LDS float* const nd_slot = lse_slot + kSlots;                      // -D, 0 if none
+
   const int lane = threadIdx.x & 63;
   const int l32 = lane & 31;
   const int hi = lane >> 5;
-  const int wave = threadIdx.x >> 6;
-  VC_LDS __bf16* k_rows = (VC_LDS __bf16*)stage + wave * 2 * stage_elems<D>();
-  VC_LDS __bf16* q_rows = k_rows;  // once the dQ part has read K
-  VC_LDS __bf16* do_rows = k_rows + stage_elems<D>();
-  VC_LDS float* lse_slot = (VC_LDS float*)stat + wave * 2 * kSlots;
-  VC_LDS float* nd_slot = lse_slot + kSlots;
-  const int blk = blockIdx.x * kWavesPerBlock + wave;
-  const int h = blockIdx.y;
-  const int b = blockIdx.z;
-  SlotMap sm{a.T, a.F, a.L, a.G, blk * a.G};
-  if (sm.l0 >= a.L) return;  // whole wave
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nblk = (a.L + a.G - 1) / a.G;
+  const int h = (int)(blockIdx.x % a.H);
+  const int pb = (int)(blockIdx.x / a.H) % nblk;
+  const int b = (int)(blockIdx.x / a.H) / nblk;
+  const SlotMap sm{a.T, a.F, a.L, a.G, pb * a.G};
   const size_t tok = (size_t)a.H * D;
   const size_t base = (size_t)b * a.N * tok + (size_t)h * D;
-  const uint8_t* km = a.key_mask ? a.key_mask + (size_t)b * a.N : nullptr;
+  const int tk = sm.token(l32);  // token row of slot l32 (lanes l32 and l32 + 32 alike)
+  const unsigned vbits = (unsigned)__ballot(sm.ok(l32));  // valid slots
 
-  const int s = l32;  // this lane's slot (query in one orientation, key in the other)
-  const int lo = (s / a.F) * a.F;
-  const bool s_ok = sm.ok(s);
-  const int n = sm.token(s);
-  bf16x8 qf[D / 16], kf[D / 16], vf[D / 16], dof[D / 16];
-  float dsum = 0.0f;  // this half's share of D = <dO, O> of the slot's token
-#pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks) {
-    const size_t off = base + (size_t)n * tok + 16 * ks + 8 * hi;
-    qf[ks] = *(const bf16x8*)(a.q + off);
-    kf[ks] = *(const bf16x8*)(a.k + off);
-    vf[ks] = *(const bf16x8*)(a.v + off);
-    dof[ks] = *(const bf16x8*)(a.dout + off);
-    const bf16x8 of = *(const bf16x8*)(a.o_in + off);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) dsum = fmaf((float)dof[ks][e], (float)of[e], dsum);
-    const int e = s * (D + kRowPad) + 16 * ks + 8 * hi;
-    *(VC_LDS bf16x8*)(k_rows + e) = kf[ks];
-    *(VC_LDS bf16x8*)(do_rows + e) = dof[ks];
-  }
-  // -D and LSE*log2(e) of the slot's token, formed here from O and the forward's LSE (no
-  // preparation pass): LSE*log2(e) is +inf where the token has no valid key or the slot
-  // none, so that its probabilities vanish.
-  const float lse_n = a.lse[((size_t)b * a.H + h) * a.N + n];
-  const float l2 = (s_ok && lse_n != -INFINITY) ? lse_n * kLog2e : INFINITY;
-  const float d = s_ok ? -halves_sum(dsum) : 0.0f;
-  if (hi == 0) {
-    lse_slot[s] = l2;
-    nd_slot[s] = d;
-  }
-  // LDS rows of the slots an operand element t of k-step st refers to.
-  int grow[2][8];
-#pragma unroll
-  for (int st = 0; st < 2; ++st)
-#pragma unroll
-    for (int t = 0; t < 8; ++t) grow[st][t] = op_slot(st, t, hi) * (D + kRowPad);
-
-  // ---- lane = query: dQ ----
+  // Row copies: wave 0 Q and K, wave 1 V and dO.
   {
+    const __bf16* s0 = (w == 0 ? a.q : a.v) + base;
+    const __bf16* s1 = (w == 0 ? a.k : a.dout) + base;
+    VC_LDS char* d0 = w == 0 ? q_t : v_t;
+    VC_LDS char* d1 = w == 0 ? k_t : do_t;
+#pragma unroll
+    for (int idx = 0; idx < Tile::COPIES; ++idx) {
+      copy_slot_rows<D>(s0, tok, tk, d0, idx, lane);
+      copy_slot_rows<D>(s1, tok, tk, d1, idx, lane);
+    }
+  }
+  // This wave's 16 slots of D = <dO, O>: O rows as whole-row loads.
+  constexpr int NI = 16 / RPI;
+  const int ch = lane % LPR;
+  bf16x8 of[NI];
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    const int n = __shfl(tk, 16 * w + RPI * i + lane / LPR);
+    of[i] = *(const bf16x8*)(a.o_in + base + (size_t)n * tok + ch * 8);
+  }
+  const int n16 = __shfl(tk, 16 * w + (lane & 15));
+  const float lse_v = a.lse[((size_t)b * a.H + h) * a.N + n16];
+  // Key-mask byte of slot l32, loaded unconditionally (from any readable byte if there is no
+  // mask) so that no branch waits for it among the copies.
+  int kmb = *(a.key_mask ? a.key_mask + (size_t)b * a.N + tk : (const uint8_t*)a.lse);
+  // Every load above is used only after this full wait: a wait for any one of them would
+  // wait for the row copies issued before it too.
+  wait_all_memory();
+  asm volatile("" : "+v"(kmb));  // the mask test stays after the wait
+  __syncthreads();               // every row copy has landed
+  const unsigned kbits = (unsigned)__ballot(!a.key_mask || kmb != 0) & vbits;  // valid, unmasked keys
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    const int sl = 16 * w + RPI * i + lane / LPR;
+    const bf16x8 dv = *(const VC_LDS bf16x8*)(do_t + perm_row(sl) * Tile::RS + ch * 16);
+    float acc = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc = fmaf((float)dv[e], (float)of[i][e], acc);
+#pragma unroll
+    for (int m = 1; m < LPR; m <<= 1) acc += __shfl_xor(acc, m);
+    if (ch == 0) nd_slot[sl] = (vbits >> sl) & 1 ? -acc : 0.0f;
+  }
+  if (lane < 16) {
+    const int sl = 16 * w + lane;
+    lse_slot[sl] = ((vbits >> sl) & 1) && lse_v != -INFINITY ? lse_v * kLog2e : INFINITY;
+  }
+  __syncthreads();  // statistics of every slot are in LDS
+
+  // Slots of this lane's group (the position of slot l32): [lo, lo + F).
+  const int lo = (l32 / a.F) * a.F;
+  const unsigned group = a.F == kSlots ? ~0u : ((1u << a.F) - 1u) << lo;
+  bf16x4 res[2][D / 32][4];  // wave 0: dQ^T in res[0]; wave 1: dV^T in res[0], dK^T in res[1]
+  if (w == 0) {
+    // lane = query l32; register r = key acc_row(r, hi)
     f32x16 sacc = zero_f32x16(), pacc = zero_f32x16();
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) {
-      sacc = mfma32(kf[ks], qf[ks], sacc);
-      pacc = mfma32(vf[ks], dof[ks], pacc);
+      sacc = mfma32(slot_rows<D>(k_t, ks, lane), slot_rows<D>(q_t, ks, lane), sacc);
+      pacc = mfma32(slot_rows<D>(v_t, ks, lane), slot_rows<D>(do_t, ks, lane), pacc);
     }
+    const unsigned allow = (((vbits >> l32) & 1) ? group & kbits : 0u) >> (4 * hi);
+    const float l2 = lse_slot[l32];
+    const float d = nd_slot[l32];
     float ds[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int j = acc_slot(r, hi);
-      bool ok = s_ok & (j >= lo) & (j < lo + a.F);
-      if (km) ok = ok & (km[sm.token(j)] != 0);
+      const bool ok = (allow >> (8 * (r >> 2) + (r & 3))) & 1;
       const float p = ok ? fast_exp2(fmaf(sacc[r], a.scale_log2, -l2)) : 0.0f;
       ds[r] = p * (pacc[r] + d);
     }
-    bf16x8 sb[2];
-    sb[0] = to_bf16x8(&ds[0]);
-    sb[1] = to_bf16x8(&ds[8]);
-    __bf16* dqp = a.o + base + (size_t)n * tok;
+    const bf16x8 sb0 = to_bf16x8(&ds[0]), sb1 = to_bf16x8(&ds[8]);
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) {
       f32x16 acc = zero_f32x16();
+      acc = mfma32(slot_cols<D>(k_t, 0, db, lane), sb0, acc);
+      acc = mfma32(slot_cols<D>(k_t, 1, db, lane), sb1, acc);
 #pragma unroll
-      for (int st = 0; st < 2; ++st) {
-        bf16x8 kt;
-#pragma unroll
-        for (int t = 0; t < 8; ++t) kt[t] = k_rows[grow[st][t] + db * 32 + l32];
-        acc = mfma32(kt, sb[st], acc);
-      }
-      if (s_ok) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          bf16x4 o4 = {(__bf16)(acc[4 * j + 0] * a.scale), (__bf16)(acc[4 * j + 1] * a.scale),
-                       (__bf16)(acc[4 * j + 2] * a.scale), (__bf16)(acc[4 * j + 3] * a.scale)};
-          *(bf16x4*)(dqp + db * 32 + 8 * j + 4 * hi) = o4;
-        }
-      }
+      for (int j = 0; j < 4; ++j)
+        res[0][db][j] = bf16x4{(__bf16)(acc[4 * j] * a.scale), (__bf16)(acc[4 * j + 1] * a.scale),
+                               (__bf16)(acc[4 * j + 2] * a.scale), (__bf16)(acc[4 * j + 3] * a.scale)};
     }
-  }
-  // ---- lane = key: dK, dV ----
-  // Q rows replace the K rows (LDS operations of a wave complete in order, so every read
-  // of K above precedes these writes).
-#pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks) *(VC_LDS bf16x8*)(q_rows + s * (D + kRowPad) + 16 * ks + 8 * hi) = qf[ks];
-  {
+  } else {
+    // lane = key l32; register r = query acc_row(r, hi)
     f32x16 sacc = zero_f32x16(), pacc = zero_f32x16();
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) {
-      sacc = mfma32(qf[ks], kf[ks], sacc);
-      pacc = mfma32(dof[ks], vf[ks], pacc);
+      sacc = mfma32(slot_rows<D>(q_t, ks, lane), slot_rows<D>(k_t, ks, lane), sacc);
+      pacc = mfma32(slot_rows<D>(do_t, ks, lane), slot_rows<D>(v_t, ks, lane), pacc);
     }
-    bool k_ok = s_ok;
-    if (km) k_ok = k_ok & (km[n] != 0);
+    const unsigned allow = (((kbits >> l32) & 1) ? group & vbits : 0u) >> (4 * hi);
     float p[16], ds[16];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int i = acc_slot(r, hi);  // query slot
-      const bool ok = k_ok & (i >= lo) & (i < lo + a.F) & sm.ok(i);
-      const float l2 = lse_slot[i];
-      const float d = nd_slot[i];
-      p[r] = ok ? fast_exp2(fmaf(sacc[r], a.scale_log2, -l2)) : 0.0f;
-      ds[r] = p[r] * (pacc[r] + d);
+    for (int m = 0; m < 4; ++m) {
+      const f32x4 l2 = *(const VC_LDS f32x4*)(lse_slot + 8 * m + 4 * hi);
+      const f32x4 d = *(const VC_LDS f32x4*)(nd_slot + 8 * m + 4 * hi);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = 4 * m + i;
+        const bool ok = (allow >> (8 * m + i)) & 1;
+        p[r] = ok ? fast_exp2(fmaf(sacc[r], a.scale_log2, -l2[i])) : 0.0f;
+        ds[r] = p[r] * (pacc[r] + d[i]);
+      }
     }
-    bf16x8 pb[2], sb[2];
-    pb[0] = to_bf16x8(&p[0]);
-    pb[1] = to_bf16x8(&p[8]);
-    sb[0] = to_bf16x8(&ds[0]);
-    sb[1] = to_bf16x8(&ds[8]);
-    __bf16* dkp = a.dk + base + (size_t)n * tok;
-    __bf16* dvp = a.dv + base + (size_t)n * tok;
+    const bf16x8 pb0 = to_bf16x8(&p[0]), pb1 = to_bf16x8(&p[8]);
+    const bf16x8 sb0 = to_bf16x8(&ds[0]), sb1 = to_bf16x8(&ds[8]);
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) {
       f32x16 vacc = zero_f32x16(), kacc = zero_f32x16();
+      vacc = mfma32(slot_cols<D>(do_t, 0, db, lane), pb0, vacc);
+      kacc = mfma32(slot_cols<D>(q_t, 0, db, lane), sb0, kacc);
+      vacc = mfma32(slot_cols<D>(do_t, 1, db, lane), pb1, vacc);
+      kacc = mfma32(slot_cols<D>(q_t, 1, db, lane), sb1, kacc);
 #pragma unroll
-      for (int st = 0; st < 2; ++st) {
-        bf16x8 dot, qt;
-#pragma unroll
-        for (int t = 0; t < 8; ++t) {
-          dot[t] = do_rows[grow[st][t] + db * 32 + l32];
-          qt[t] = q_rows[grow[st][t] + db * 32 + l32];
-        }
-        vacc = mfma32(dot, pb[st], vacc);
-        kacc = mfma32(qt, sb[st], kacc);
-      }
-      if (s_ok) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          bf16x4 v4 = {(__bf16)vacc[4 * j + 0], (__bf16)vacc[4 * j + 1], (__bf16)vacc[4 * j + 2],
-                       (__bf16)vacc[4 * j + 3]};
-          bf16x4 k4 = {(__bf16)(kacc[4 * j + 0] * a.scale), (__bf16)(kacc[4 * j + 1] * a.scale),
-                       (__bf16)(kacc[4 * j + 2] * a.scale), (__bf16)(kacc[4 * j + 3] * a.scale)};
-          *(bf16x4*)(dvp + db * 32 + 8 * j + 4 * hi) = v4;
-          *(bf16x4*)(dkp + db * 32 + 8 * j + 4 * hi) = k4;
-        }
+      for (int j = 0; j < 4; ++j) {
+        res[0][db][j] = bf16x4{(__bf16)vacc[4 * j], (__bf16)vacc[4 * j + 1], (__bf16)vacc[4 * j + 2],
+                               (__bf16)vacc[4 * j + 3]};
+        res[1][db][j] = bf16x4{(__bf16)(kacc[4 * j] * a.scale), (__bf16)(kacc[4 * j + 1] * a.scale),
+                               (__bf16)(kacc[4 * j + 2] * a.scale), (__bf16)(kacc[4 * j + 3] * a.scale)};
       }
     }
+  }
+  __syncthreads();  // every tile read of both waves is done: the tiles take the results
+
+  // Results as rows (slot l32's row, dims db*32 + 8j + 4hi .. +3), then whole-row stores of
+  // the valid slots: wave 0 dQ through the K tile, wave 1 dV through the V tile and dK
+  // through the Q tile.
+  auto put = [&](VC_LDS char* t, __bf16* out, const bf16x4 (&r)[D / 32][4]) {
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        *(VC_LDS bf16x4*)(t + perm_row(l32) * Tile::RS + (db * 32 + 8 * j + 4 * hi) * 2) = r[db][j];
+#pragma unroll
+    for (int i = 0; i < kSlots / RPI; ++i) {
+      const int sl = RPI * i + lane / LPR;
+      const int n = __shfl(tk, sl);
+      const bf16x8 row = *(const VC_LDS bf16x8*)(t + perm_row(sl) * Tile::RS + ch * 16);
+      if ((vbits >> sl) & 1) *(bf16x8*)(out + (size_t)n * tok + ch * 8) = row;
+    }
+  };
+  if (w == 0) {
+    put(k_t, a.o + base, res[0]);
+  } else {
+    put(v_t, a.dv + base, res[0]);
+    put(q_t, a.dk + base, res[1]);
   }
 }
 
@@ -419,11 +484,11 @@ hipError_t launch_branch_sum(const __bf16* a, const __bf16* b, const __bf16* c, 
 
 hipError_t launch_temporal_bwd(const TemporalArgs& a, int head_dim, hipStream_t s) {
   const int nblk = (a.L + a.G - 1) / a.G;
-  dim3 grid((nblk + kWavesPerBlock - 1) / kWavesPerBlock, a.H, a.B);
+  const dim3 grid((unsigned)((size_t)a.B * nblk * a.H));
   if (head_dim == 128)
-    hipLaunchKernelGGL(temporal_bwd_kernel<128>, grid, dim3(64 * kWavesPerBlock), 0, s, a);
+    hipLaunchKernelGGL(temporal_bwd_kernel<128>, grid, dim3(128), 0, s, a);
   else
-    hipLaunchKernelGGL(temporal_bwd_kernel<64>, grid, dim3(64 * kWavesPerBlock), 0, s, a);
+    hipLaunchKernelGGL(temporal_bwd_kernel<64>, grid, dim3(128), 0, s, a);
   return hipGetLastError();
 }
 
