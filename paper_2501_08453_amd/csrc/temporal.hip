@@ -2,29 +2,22 @@
 // frames (the [B*L, F, ...] regrouping of the multimodal diffusion block), read in
 // place from the joint [B, N, H, D] layout where video token (f, l) is row T + f*L + l.
 //
-// Sequences are short (F <= 32), so one wave packs G = floor(32/F) consecutive
-// positions of one (sample, head) into the 32 slots of a 32x32x16 matrix-core
-// block: slot s holds frame s % F of position l0 + s / F; slots past G*F are
-// padding. Rows of Q, K (and dO, V in the backward) are read as 16-byte chunks, one
-// slot per lane; the rows whose transposes are MFMA operands (V^T in the forward,
-// K^T, Q^T, dO^T in the backward) are also written to LDS, and the transposed
-// fragments read from there element by element in the key order the accumulator
-// layout produces. A key is valid for a query if it belongs to the
-// same position (same group of F slots) and key_mask keeps it. The work is small
-// and bound by memory traffic.
+// Sequences are short (F <= 32), so one workgroup packs G = floor(32/F) consecutive
+// positions of one (sample, head) into the 32 slots of a 32x32x16 matrix-core block:
+// slot s holds frame s % F of position l0 + s / F; slots past G*F are padding. The
+// rows of the slots are copied into LDS row tiles by whole-row wave copies (64 lanes
+// read consecutive 16-byte chunks of a few token rows: one slot per lane would make
+// every lane's chunk its own cache access), the MFMA operands are read from there
+// (transposing reads where the contraction runs over slots), and the results go back
+// through a tile so that they too are stored as whole rows. A key is valid for a query
+// if it belongs to the same position (same group of F slots) and key_mask keeps it. The
+// work is small and bound by memory traffic.
 #include "common.hpp"
 
 namespace vcja {
 namespace {
 
 constexpr int kSlots = 32;
-constexpr int kWavesPerBlock = 4;
-// Rows of a wave's 32 slots staged in LDS (row-major, padded by 8 elements so that the
-// rows of a 16-byte write fall in different banks): transposed operands are read from
-// there two bytes at a time instead of being gathered from memory.
-constexpr int kRowPad = 8;
-template <int D>
-constexpr int stage_elems() { return kSlots * (D + kRowPad); }
 
 // Token row of slot s in the block starting at position l0 (clamped into range for
 // padding slots, whose probabilities are zero).
@@ -38,13 +31,6 @@ struct SlotMap {
     return T + f * L + l;
   }
 };
-
-// Slot held by register r of a lane of half hi in a 32x32 accumulator (row index).
-__device__ __forceinline__ int acc_slot(int r, int hi) { return acc_row(r, hi); }
-
-// Slot of operand element t of k-step st for a lane of half hi: the order in which the
-// accumulator rows of 8 consecutive registers are numbered.
-__device__ __forceinline__ int op_slot(int st, int t, int hi) { return 16 * st + 8 * (t >> 2) + 4 * hi + (t & 3); }
 
 // Sum of three bf16 values in fp32, in argument order, rounded once (a NULL source counts as
 // zero): the arithmetic shared by the branch-sum kernel and the fused epilogue.
@@ -63,129 +49,7 @@ __device__ __forceinline__ void add_bf16x8(f32x4& lo, f32x4& hi, bf16x8 x) {
   }
 }
 
-// One wave: attention of the G positions starting at sm.l0 (sm.l0 < L) of head h, sample b.
-template <int D>
-__device__ __forceinline__ void temporal_fwd_wave(const TemporalArgs& a, const SlotMap& sm, int h, int b,
-                                                  VC_LDS __bf16* vs) {
-  const int lane = threadIdx.x & 63;
-  const int l32 = lane & 31;
-  const int hi = lane >> 5;
-  const size_t tok = (size_t)a.H * D;
-  const size_t base = (size_t)b * a.N * tok + (size_t)h * D;
-
-  // This lane's slot as query (B operand column) and as key (A operand row).
-  const int s = l32;
-  const int g = s / a.F;
-  const bool q_ok = sm.ok(s);
-  const int n = sm.token(s);
-  bf16x8 qf[D / 16], kf[D / 16];
-#pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks) {
-    qf[ks] = *(const bf16x8*)(a.q + base + (size_t)n * tok + 16 * ks + 8 * hi);
-    kf[ks] = *(const bf16x8*)(a.k + base + (size_t)n * tok + 16 * ks + 8 * hi);
-    *(VC_LDS bf16x8*)(vs + s * (D + kRowPad) + 16 * ks + 8 * hi) =
-        *(const bf16x8*)(a.v + base + (size_t)n * tok + 16 * ks + 8 * hi);
-  }
-  // S^T = K Q^T: lane column = query slot s, register r = key slot acc_slot(r, hi).
-  f32x16 sacc = zero_f32x16();
-#pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks) sacc = mfma32(kf[ks], qf[ks], sacc);
-
-  // Keys of the same group (position) only; padding and masked keys excluded.
-  const int lo = g * a.F;
-  const uint8_t* km = a.key_mask ? a.key_mask + (size_t)b * a.N : nullptr;
-  float mx = -INFINITY;
-#pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int j = acc_slot(r, hi);
-    bool ok = q_ok & (j >= lo) & (j < lo + a.F);
-    if (km) ok = ok & (km[sm.token(j)] != 0);
-    sacc[r] = ok ? sacc[r] : -INFINITY;
-    mx = fmaxf(mx, sacc[r]);
-  }
-  mx = halves_max(mx);
-  const float m2 = mx == -INFINITY ? 0.0f : mx * a.scale_log2;
-  float p[16], sum = 0.0f;
-#pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    p[r] = fast_exp2(fmaf(sacc[r], a.scale_log2, -m2));
-    sum += p[r];
-  }
-  sum = halves_sum(sum);
-
-  // O^T = V^T P^T over the 32 key slots (two k-steps of 16).
-  bf16x8 pb[2];
-  pb[0] = to_bf16x8(&p[0]);
-  pb[1] = to_bf16x8(&p[8]);
-  int vrow[2][8];  // LDS rows of the key slots of operand element t, k-step st
-#pragma unroll
-  for (int st = 0; st < 2; ++st)
-#pragma unroll
-    for (int t = 0; t < 8; ++t) vrow[st][t] = op_slot(st, t, hi) * (D + kRowPad);
-  const float inv = sum > 0.0f ? 1.0f / sum : 0.0f;
-  __bf16* op = a.o + base + (size_t)n * tok;
-#pragma unroll
-  for (int db = 0; db < D / 32; ++db) {
-    f32x16 oacc = zero_f32x16();
-#pragma unroll
-    for (int st = 0; st < 2; ++st) {
-      bf16x8 vt;
-#pragma unroll
-      for (int t = 0; t < 8; ++t) vt[t] = vs[vrow[st][t] + db * 32 + l32];
-      oacc = mfma32(vt, pb[st], oacc);
-    }
-    if (q_ok) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        bf16x4 o4 = {(__bf16)(oacc[4 * j + 0] * inv), (__bf16)(oacc[4 * j + 1] * inv),
-                     (__bf16)(oacc[4 * j + 2] * inv), (__bf16)(oacc[4 * j + 3] * inv)};
-        *(bf16x4*)(op + db * 32 + 8 * j + 4 * hi) = o4;
-      }
-    }
-  }
-  if (q_ok && hi == 0)
-    a.lse[((size_t)b * a.H + h) * a.N + n] = sum > 0.0f ? (m2 + __log2f(sum)) * kLn2 : -INFINITY;
-}
-
-// Forward: one wave per G positions. With SUM, the workgroup then writes the branch sum
-// sum_out = (sum_a + sum_b) + o of the rows it produced, reading o back after a barrier
-// so that every access is a whole 16-byte chunk of a row (the accumulator layout would
-// scatter 8-byte pieces over 32 rows per instruction).
-template <int D, bool SUM>
-__global__ __launch_bounds__(64 * kWavesPerBlock) void temporal_fwd_kernel(TemporalArgs a) {
-  const int h = blockIdx.y;
-  const int b = blockIdx.z;
-  __shared__ __attribute__((aligned(16))) __bf16 stage[kWavesPerBlock * stage_elems<D>()];
-  const int wave = threadIdx.x >> 6;
-  SlotMap sm{a.T, a.F, a.L, a.G, (int)(blockIdx.x * kWavesPerBlock + wave) * a.G};
-  if (sm.l0 < a.L) temporal_fwd_wave<D>(a, sm, h, b, (VC_LDS __bf16*)stage + wave * stage_elems<D>());
-  if (SUM) {
-    __syncthreads();  // this workgroup's rows of o are written
-    const int wl0 = (int)blockIdx.x * kWavesPerBlock * a.G;  // first position of the workgroup
-    const int npos = min(kWavesPerBlock * a.G, a.L - wl0);
-    constexpr int kChunks = D / 8;  // 16-byte chunks per row
-    const size_t tok = (size_t)a.H * D;
-    const size_t base = (size_t)b * a.N * tok + (size_t)h * D;
-    for (int i = threadIdx.x; i < a.F * npos * kChunks; i += blockDim.x) {
-      const int r = i / kChunks;
-      const int f = r / npos;
-      const size_t off = base + (size_t)(a.T + f * a.L + wl0 + (r - f * npos)) * tok + (i % kChunks) * 8;
-      f32x4 lo = {0.0f, 0.0f, 0.0f, 0.0f}, hi = lo;
-      if (a.sum_a) add_bf16x8(lo, hi, *(const bf16x8*)(a.sum_a + off));
-      if (a.sum_b) add_bf16x8(lo, hi, *(const bf16x8*)(a.sum_b + off));
-      add_bf16x8(lo, hi, *(const bf16x8*)(a.o + off));
-      bf16x8 r8;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        r8[e] = (__bf16)lo[e];
-        r8[4 + e] = (__bf16)hi[e];
-      }
-      *(bf16x8*)(a.sum_out + off) = r8;
-    }
-  }
-}
-
-// Row tiles of a group's 32 slots in LDS, for the backward: slot s sits in row perm_row(s)
+// Row tiles of a group's 32 slots in LDS: slot s sits in row perm_row(s)
 // (the permuted order of the joint backward, so that the transposing reads of four
 // consecutive slots hit distinct banks) with one 16-byte pad chunk per row (the rows one
 // quarter-wave reads at a common column fall on distinct banks), filled by whole 1 KiB wave
@@ -231,6 +95,133 @@ __device__ __forceinline__ bf16x8 slot_cols(const VC_LDS char* t, int st, int db
   const bf16x4 x = lds_read_tr(t + perm_row(r0) * SlotTile<D>::RS + col);
   const bf16x4 y = lds_read_tr(t + perm_row(r0 + 8) * SlotTile<D>::RS + col);
   return cat4(x, y);
+}
+
+// Forward: one wave per group of G positions (32 slots) of one (sample, head), head fastest
+// over the grid, so that concurrent workgroups read whole token rows. Q, K and V rows are
+// copied into LDS row tiles; lane = query: S^T = K Q^T, the softmax over the lane's group
+// with fp32 sums, O^T = V^T P^T (P rounded to bf16 for the product). O goes back through
+// the Q tile so that it is stored as whole rows; with SUM the same rows of the branch sum
+// sum_out = (sum_a + sum_b) + o are formed from them and written too.
+template <int D, bool SUM>
+__global__ __launch_bounds__(64) void temporal_fwd_kernel(TemporalArgs a) {
+  using Tile = SlotTile<D>;
+  constexpr int LPR = D / 8;     // lanes per row in a whole-row access
+  constexpr int RPI = 64 / LPR;  // rows per whole-row wave access
+  constexpr int NR = kSlots / RPI;
+  __shared__ __attribute__((aligned(1024))) char smem[3 * Tile::REGION];
+  VC_LDS char* const q_t = (VC_LDS char*)smem;
+  VC_LDS char* const k_t = q_t + Tile::REGION;
+  VC_LDS char* const v_t = k_t + Tile::REGION;
+
+  const int lane = threadIdx.x & 63;
+  const int l32 = lane & 31;
+  const int hi = lane >> 5;
+  const int nblk = (a.L + a.G - 1) / a.G;
+  const int h = (int)(blockIdx.x % a.H);
+  const int pb = (int)(blockIdx.x / a.H) % nblk;
+  const int b = (int)(blockIdx.x / a.H) / nblk;
+  const SlotMap sm{a.T, a.F, a.L, a.G, pb * a.G};
+  const size_t tok = (size_t)a.H * D;
+  const size_t base = (size_t)b * a.N * tok + (size_t)h * D;
+  const int tk = sm.token(l32);  // token row of slot l32 (lanes l32 and l32 + 32 alike)
+  const unsigned vbits = (unsigned)__ballot(sm.ok(l32));  // valid slots
+  const int ch = lane % LPR;
+#pragma unroll
+  for (int idx = 0; idx < Tile::COPIES; ++idx) {
+    copy_slot_rows<D>(a.q + base, tok, tk, q_t, idx, lane);
+    copy_slot_rows<D>(a.k + base, tok, tk, k_t, idx, lane);
+    copy_slot_rows<D>(a.v + base, tok, tk, v_t, idx, lane);
+  }
+  // With SUM, the rows of the other two branch outputs this lane adds, as whole-row loads
+  // (from q in place of a missing one: any readable bytes, replaced by zero below).
+  bf16x8 ra[SUM ? NR : 1], rb[SUM ? NR : 1];
+  if constexpr (SUM) {
+#pragma unroll
+    for (int i = 0; i < NR; ++i) {
+      const size_t off = base + (size_t)__shfl(tk, RPI * i + lane / LPR) * tok + ch * 8;
+      ra[i] = *(const bf16x8*)((a.sum_a ? a.sum_a : a.q) + off);
+      rb[i] = *(const bf16x8*)((a.sum_b ? a.sum_b : a.q) + off);
+    }
+  }
+  // Key-mask byte of slot l32, loaded unconditionally (from any readable byte if there is no
+  // mask) so that no branch waits for it among the copies.
+  int kmb = *(a.key_mask ? a.key_mask + (size_t)b * a.N + tk : (const uint8_t*)a.q);
+  // Every load above is used only after this full wait (one wave: its copies are then in
+  // LDS); a wait for any one of them would wait for the copies issued before it too.
+  wait_all_memory();
+  asm volatile("" : "+v"(kmb));  // the mask test stays after the wait
+  const unsigned kbits = (unsigned)__ballot(!a.key_mask || kmb != 0) & vbits;  // valid, unmasked keys
+
+  // lane = query l32; register r = key acc_row(r, hi). Keys of the query's own position
+  // (its group of F slots) only.
+  const int lo = (l32 / a.F) * a.F;
+  const unsigned group = a.F == kSlots ? ~0u : ((1u << a.F) - 1u) << lo;
+  const bool q_ok = (vbits >> l32) & 1;
+  const unsigned allow = (q_ok ? group & kbits : 0u) >> (4 * hi);
+  f32x16 sacc = zero_f32x16();
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) sacc = mfma32(slot_rows<D>(k_t, ks, lane), slot_rows<D>(q_t, ks, lane), sacc);
+  float mx = -INFINITY;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const bool ok = (allow >> (8 * (r >> 2) + (r & 3))) & 1;
+    sacc[r] = ok ? sacc[r] : -INFINITY;
+    mx = fmaxf(mx, sacc[r]);
+  }
+  mx = halves_max(mx);
+  const float m2 = mx == -INFINITY ? 0.0f : mx * a.scale_log2;
+  float p[16], sum = 0.0f;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    p[r] = fast_exp2(fmaf(sacc[r], a.scale_log2, -m2));
+    sum += p[r];
+  }
+  sum = halves_sum(sum);
+  const bf16x8 pb0 = to_bf16x8(&p[0]), pb1 = to_bf16x8(&p[8]);
+  const float inv = sum > 0.0f ? 1.0f / sum : 0.0f;
+  bf16x4 res[D / 32][4];
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db) {
+    f32x16 oacc = zero_f32x16();
+    oacc = mfma32(slot_cols<D>(v_t, 0, db, lane), pb0, oacc);
+    oacc = mfma32(slot_cols<D>(v_t, 1, db, lane), pb1, oacc);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      res[db][j] = bf16x4{(__bf16)(oacc[4 * j] * inv), (__bf16)(oacc[4 * j + 1] * inv),
+                          (__bf16)(oacc[4 * j + 2] * inv), (__bf16)(oacc[4 * j + 3] * inv)};
+  }
+  if (q_ok && hi == 0)
+    a.lse[((size_t)b * a.H + h) * a.N + tk] = sum > 0.0f ? (m2 + __log2f(sum)) * kLn2 : -INFINITY;
+  // O rows through the Q tile (every read of it above precedes these writes: LDS operations
+  // of a wave complete in order), then whole-row stores of the valid slots.
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      *(VC_LDS bf16x4*)(q_t + perm_row(l32) * Tile::RS + (db * 32 + 8 * j + 4 * hi) * 2) = res[db][j];
+#pragma unroll
+  for (int i = 0; i < NR; ++i) {
+    const int sl = RPI * i + lane / LPR;
+    const size_t off = base + (size_t)__shfl(tk, sl) * tok + ch * 8;
+    const bf16x8 row = *(const VC_LDS bf16x8*)(q_t + perm_row(sl) * Tile::RS + ch * 16);
+    if ((vbits >> sl) & 1) {
+      *(bf16x8*)(a.o + off) = row;
+      if constexpr (SUM) {
+        f32x4 lo4 = {0.0f, 0.0f, 0.0f, 0.0f}, hi4 = lo4;
+        add_bf16x8(lo4, hi4, a.sum_a ? ra[i] : zero_bf16x8());
+        add_bf16x8(lo4, hi4, a.sum_b ? rb[i] : zero_bf16x8());
+        add_bf16x8(lo4, hi4, row);
+        bf16x8 r8;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          r8[e] = (__bf16)lo4[e];
+          r8[4 + e] = (__bf16)hi4[e];
+        }
+        *(bf16x8*)(a.sum_out + off) = r8;
+      }
+    }
+  }
 }
 
 // Backward: one workgroup of two waves per group of G positions (32 slots) of one (sample,
@@ -460,16 +451,16 @@ __global__ __launch_bounds__(256) void text_rows_kernel(__bf16* x0, __bf16* x1, 
 
 hipError_t launch_temporal_fwd(const TemporalArgs& a, int head_dim, hipStream_t s) {
   const int nblk = (a.L + a.G - 1) / a.G;
-  dim3 grid((nblk + kWavesPerBlock - 1) / kWavesPerBlock, a.H, a.B);
+  const dim3 grid((unsigned)((size_t)a.B * nblk * a.H));
   const bool sum = a.sum_out != nullptr;
   if (head_dim == 128 && sum)
-    hipLaunchKernelGGL((temporal_fwd_kernel<128, true>), grid, dim3(64 * kWavesPerBlock), 0, s, a);
+    hipLaunchKernelGGL((temporal_fwd_kernel<128, true>), grid, dim3(64), 0, s, a);
   else if (head_dim == 128)
-    hipLaunchKernelGGL((temporal_fwd_kernel<128, false>), grid, dim3(64 * kWavesPerBlock), 0, s, a);
+    hipLaunchKernelGGL((temporal_fwd_kernel<128, false>), grid, dim3(64), 0, s, a);
   else if (sum)
-    hipLaunchKernelGGL((temporal_fwd_kernel<64, true>), grid, dim3(64 * kWavesPerBlock), 0, s, a);
+    hipLaunchKernelGGL((temporal_fwd_kernel<64, true>), grid, dim3(64), 0, s, a);
   else
-    hipLaunchKernelGGL((temporal_fwd_kernel<64, false>), grid, dim3(64 * kWavesPerBlock), 0, s, a);
+    hipLaunchKernelGGL((temporal_fwd_kernel<64, false>), grid, dim3(64), 0, s, a);
   return hipGetLastError();
 }
 

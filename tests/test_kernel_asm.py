@@ -114,10 +114,12 @@ def basic_blocks(body):
 
 
 def test_no_vector_memory_wait_among_lds_copies(device_asm):
-    """In a basic block that issues LDS copies, the only vector-memory waits are the full
-    waits right before a barrier (the kernels' own wait for a stage's copies). Any other
-    vmcnt wait there, e.g. one the compiler inserts for a spill reload at the head of a
-    copy loop, waits for every copy in flight, the ones just issued included."""
+    """In a basic block that issues LDS copies, the only vector-memory waits are the
+    kernels' own waits for a stage's copies: full waits right before a barrier, or the
+    explicit wait for every counter (s_waitcnt 0, which names expcnt) of a one-wave
+    workgroup. Any other vmcnt wait there, e.g. one the compiler inserts for a spill reload
+    at the head of a copy loop, waits for every copy in flight, the ones just issued
+    included."""
     checked = 0
     for fn, text in device_asm.items():
         for name, body in kernels(text):
@@ -129,7 +131,8 @@ def test_no_vector_memory_wait_among_lds_copies(device_asm):
                 for i, line in enumerate(ins):
                     if line.startswith("s_waitcnt") and "vmcnt" in line:
                         nxt = ins[i + 1] if i + 1 < len(ins) else ""
-                        assert nxt.startswith("s_barrier"), (fn, name, line, ins[max(0, i - 3):i + 3])
+                        explicit = all(c in line for c in ("vmcnt(0)", "expcnt(0)", "lgkmcnt(0)"))
+                        assert nxt.startswith("s_barrier") or explicit, (fn, name, line, ins[max(0, i - 3):i + 3])
     assert checked > 0
 
 
