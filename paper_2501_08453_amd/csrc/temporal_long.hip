@@ -61,13 +61,13 @@ struct PosRows {
 
 // Issues this wave's share of the copies of rows [0, round_up(F, 16)) into `dst` in
 // permuted order (LDS row r holds frame perm_row(r), clamped to the last frame).
-template <int D>
+template <int D, int NW = kLongWaves>
 __device__ __forceinline__ void copy_rows(PosRows pr, int F, VC_LDS char* dst, int w) {
   constexpr int CH = LongLds<D>::CH;
   const int lane = opaque_lane();
   const int rows = (F + 15) & ~15;
   const int copies = (rows * CH + 63) / 64;
-  for (int idx = w; idx < copies; idx += kLongWaves) {
+  for (int idx = w; idx < copies; idx += NW) {
     const int lin = idx * 64 + lane;
     const int r = lin / CH;
     const int c = min(lin - r * CH, CH - 2);
@@ -246,208 +246,285 @@ __global__ __launch_bounds__(64 * kLongWaves, 1) void temporal_long_fwd_kernel(T
   }
 }
 
+// Result rows of frame block `blk` (lane l32's frame blk*32 + l32, dims db*32 + 8j + 4hi ..
+// +3 in res[db][j]) into a tile, then whole-row stores of the block's frames < F to
+// dst + f*fstride. The wave reads back only rows it wrote (LDS operations of a wave complete
+// in order).
+template <int D>
+__device__ __forceinline__ void put_block_rows(VC_LDS char* t, __bf16* dst, size_t fstride, int blk, int F,
+                                               const bf16x4 (&res)[D / 32][4]) {
+  constexpr int LPR = D / 8, RPI = 64 / LPR;
+  int lane = opaque_lane();
+  const int f = blk * 32 + (lane & 31);
+  if (f < F) {
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        *(VC_LDS bf16x4*)(t + row_off<D>(f, F) + (db * 32 + 8 * j + 4 * (lane >> 5)) * 2) = res[db][j];
+  }
+  lane = opaque_lane();
+#pragma unroll
+  for (int i = 0; i < 32 / RPI; ++i) {
+    const int fr = blk * 32 + RPI * i + lane / LPR;
+    if (fr < F)
+      *(bf16x8*)(dst + (size_t)fr * fstride + (lane % LPR) * 8) =
+          *(const VC_LDS bf16x8*)(t + row_off<D>(fr, F) + (lane % LPR) * 16);
+  }
+}
+
+// Backward: one position at a time per workgroup (persistent), all four row tiles Q | K | V
+// | dO of the position resident in LDS. D = <dO, O> (O read as whole rows while the tiles
+// fill), LSE*log2(e) and the valid-key bits of every frame are formed first and shared
+// through LDS. Wave j < 5 forms dK, dV of key block j (lane = key: S, dP from -D,
+// dV^T += dO^T P, dK^T += Q^T dS over the query blocks); waves 5, 6, 7 form dQ of query
+// blocks j - 5 and j - 2 (lane = query: S^T, dP^T, dS^T, dQ^T += K^T dS^T over the key
+// blocks), so that each SIMD carries about the same matrix work. The results go back
+// through the tiles (dQ through K, dK through Q, dV through V) so that every global store
+// is a whole 16-byte chunk of a row; the next position's copies go out once every wave has
+// read its rows back, so they overlap those stores. One full wait per position.
 template <int D>
 __global__ __launch_bounds__(64 * kLongWaves, 1) void temporal_long_bwd_kernel(TemporalArgs a) {
   using Lds = LongLds<D>;
-  __shared__ __attribute__((aligned(1024))) char smem[Lds::BYTES];
+  constexpr int NW = kLongWaves;
+  constexpr int LPR = D / 8;     // lanes per row in a whole-row access
+  constexpr int RPI = 64 / LPR;  // rows per whole-row wave access
+  constexpr int NOI = ((kLongPadRows + RPI - 1) / RPI + NW - 1) / NW;  // O row loads per wave
+  constexpr int KBW = 32 * kLongMaxBlocks / 16;  // words of valid-key bits (16 frames each)
+  __shared__ __attribute__((aligned(1024))) char smem[Lds::BYTES + 4 * KBW];
+  VC_LDS char* const q_t = (VC_LDS char*)smem;
+  VC_LDS char* const k_t = q_t + Lds::REGION;
+  VC_LDS char* const v_t = k_t + Lds::REGION;
+  VC_LDS char* const do_t = v_t + Lds::REGION;
+  VC_LDS float* const lse_s = (VC_LDS float*)(smem + 4 * Lds::REGION);  // LSE*log2e per frame slot
+  VC_LDS float* const nd_s = lse_s + 32 * kLongMaxBlocks;               // -D per frame slot
+  VC_LDS unsigned* const kbits = (VC_LDS unsigned*)(smem + Lds::BYTES);  // valid keys, 16 frames per word
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int F = a.F, L = a.L, H = a.H;
   const int nblk = (F + 31) / 32;
   const size_t tok = (size_t)H * D;
+  const size_t fstride = (size_t)L * tok;  // frame stride of a position's rows
   const int items = a.B * L * H;
-  VC_LDS char* const bufA = (VC_LDS char*)smem;                  // K | V
-  VC_LDS char* const bufB = (VC_LDS char*)smem + 2 * Lds::REGION;  // Q | dO
-  VC_LDS float* const lse_s = (VC_LDS float*)(smem + 4 * Lds::REGION);  // LSE*log2e per query slot
-  VC_LDS float* const nd_s = lse_s + 32 * kLongMaxBlocks;              // -D per query slot
-  auto rows_of = [&](const __bf16* t, PosItem it) {
-    return PosRows{t + ((size_t)it.b * a.N + a.T + it.l) * tok + (size_t)it.h * D, (size_t)L * tok};
-  };
-  auto row_at = [&](PosItem it, int f) {
-    return ((size_t)it.b * a.N + a.T + (size_t)f * L + it.l) * tok + (size_t)it.h * D;
-  };
+  const bool kv_role = w < kLongMaxBlocks;  // dK, dV of key block w; else dQ of blocks m, m + 3
+  const int m = w - kLongMaxBlocks;
+  auto block_bits = [&](int blk) { return kbits[2 * blk] | (kbits[2 * blk + 1] << 16); };
 
-  // The dQ half's per-lane inputs (query frame w*32 + l32, clamped to the last frame): Q and
-  // dO rows as B operands and the LSE, loaded one item ahead (at the end of the previous
-  // item's dK/dV half) so that their latency overlaps that work. (The O row, needed only for
-  // D, is read at the start of the half: holding it too across the dK/dV half would spill.)
-  bf16x8 qf[D / 16], dof[D / 16];
-  float lse_in = 0.0f;
-  auto load_rows = [&](int i) {
-    const PosItem it = pos_item(i, H, L);
-    const int ln = opaque_lane();
-    const int f = min(w * 32 + (ln & 31), F - 1);
-    const size_t row = row_at(it, f) + 8 * (ln >> 5);
-#pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks) {
-      qf[ks] = *(const bf16x8*)(a.q + row + 16 * ks);
-      dof[ks] = *(const bf16x8*)(a.dout + row + 16 * ks);
-    }
-    lse_in = a.lse[((size_t)it.b * H + it.h) * a.N + a.T + (size_t)f * L + it.l];
-  };
-  if ((int)blockIdx.x < items) {
-    const PosItem it = pos_item(blockIdx.x, H, L);
-    copy_rows<D>(rows_of(a.k, it), F, bufA, w);
-    copy_rows<D>(rows_of(a.v, it), F, bufA + Lds::REGION, w);
-    if (w < nblk) load_rows(blockIdx.x);
-  }
   for (int i = blockIdx.x; i < items; i += gridDim.x) {
     const PosItem it = pos_item(i, H, L);
-    const uint8_t* km = a.key_mask ? a.key_mask + (size_t)it.b * a.N + a.T + it.l : nullptr;
-    // per-lane values formed anew for each position (nothing per-lane held across the loop)
-    const int lane = opaque_lane();
+    const size_t base = ((size_t)it.b * a.N + a.T + it.l) * tok + (size_t)it.h * D;  // frame 0's row
+    const size_t rbase = ((size_t)it.b * H + it.h) * a.N + a.T + it.l;              // frame 0's LSE
+    __syncthreads();  // every wave has read back the previous position's results
+    copy_rows<D, NW>(PosRows{a.q + base, fstride}, F, q_t, w);
+    copy_rows<D, NW>(PosRows{a.k + base, fstride}, F, k_t, w);
+    copy_rows<D, NW>(PosRows{a.v + base, fstride}, F, v_t, w);
+    copy_rows<D, NW>(PosRows{a.dout + base, fstride}, F, do_t, w);
+    // O rows (whole-row loads; frames past F clamped, their D unused), and the LSE and
+    // key-mask byte of frames 16w .. 16w + 15 and, past 16*NW, 16(w + NW) .. (clamped
+    // likewise; the mask byte from any readable byte if there is no mask). Every load here
+    // is used only after the full wait below.
+    int lane = opaque_lane();
+    const int ch = lane % LPR;
+    bf16x8 of[NOI];
+#pragma unroll
+    for (int j = 0; j < NOI; ++j) {
+      const int r = min((w + NW * j) * RPI + lane / LPR, F - 1);
+      of[j] = *(const bf16x8*)(a.o_in + base + (size_t)r * fstride + ch * 8);
+    }
+    constexpr int NF = (KBW + NW - 1) / NW;  // 16-frame groups per wave
+    float lse_v[NF];
+    int kmb[NF];
+#pragma unroll
+    for (int g = 0; g < NF; ++g) {
+      const int f = min(16 * (w + NW * g) + (lane & 15), F - 1);
+      lse_v[g] = a.lse[rbase + (size_t)f * L];
+      kmb[g] = *(a.key_mask ? a.key_mask + (size_t)it.b * a.N + a.T + it.l + (size_t)f * L : (const uint8_t*)a.lse);
+    }
+    wait_all_memory();
+#pragma unroll
+    for (int g = 0; g < NF; ++g) asm volatile("" : "+v"(kmb[g]), "+v"(lse_v[g]));  // uses stay after the wait
+    __syncthreads();  // the position's rows are in LDS
+    lane = opaque_lane();
+    // -D per frame slot (0 past F), LSE*log2e (+inf past F or where a frame has no valid
+    // key), valid-key bits
+#pragma unroll
+    for (int j = 0; j < NOI; ++j) {
+      const int r = (w + NW * j) * RPI + lane / LPR;
+      if (r < 32 * nblk) {  // whole groups of LPR lanes
+        float acc = 0.0f;
+        if (r < F) {
+          const bf16x8 dv = *(const VC_LDS bf16x8*)(do_t + row_off<D>(r, F) + ch * 16);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc = fmaf((float)dv[e], (float)of[j][e], acc);
+        }
+#pragma unroll
+        for (int s = 1; s < LPR; s <<= 1) acc += __shfl_xor(acc, s);
+        if (ch == 0) nd_s[r] = r < F ? -acc : 0.0f;
+      }
+    }
+#pragma unroll
+    for (int g = 0; g < NF; ++g) {
+      const int grp = w + NW * g;
+      const int f = 16 * grp + (lane & 15);
+      if (grp < KBW) {
+        if (lane < 16 && f < 32 * nblk) lse_s[f] = (f < F && lse_v[g] != -INFINITY) ? lse_v[g] * kLog2e : INFINITY;
+        const unsigned kb = (unsigned)__ballot(f < F && (!a.key_mask || kmb[g] != 0)) & 0xffffu;
+        if (lane == 0) kbits[grp] = kb;
+      }
+    }
+    __syncthreads();  // statistics and key bits of every frame are in LDS
+
     const int l32 = lane & 31, hi = lane >> 5;
-    wait_all_memory();
-    __syncthreads();  // K, V of item i in A; every wave is done with B and the slot stats
-    copy_rows<D>(rows_of(a.q, it), F, bufB, w);
-    copy_rows<D>(rows_of(a.dout, it), F, bufB + Lds::REGION, w);
-
-    // ---- lane = query: dQ^T = c K^T dS^T over the key blocks (A: K, V rows) ----
-    bf16x8 kf[D / 16], vf[D / 16];  // the dK/dV half's K, V (key block w), read from A now
-    if (w < nblk) {
-      const int q = w * 32 + l32;
-      const bool q_in = q < F;
-      float dsum = 0.0f;
-      {
-        const size_t orow = row_at(it, min(q, F - 1)) + 8 * hi;
+    bf16x4 r0[D / 32][4], r1[D / 32][4];  // key waves: dK, dV; query waves: dQ of block m in r0
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) r0[db][j] = r1[db][j] = bf16x4{};
+    if (kv_role) {
+      if (w < nblk) {
+        // ---- lane = key w*32 + l32 ----
+        const bool valid = ((block_bits(w) >> l32) & 1u) != 0;
+        bf16x8 kf[D / 16], vf[D / 16];
 #pragma unroll
         for (int ks = 0; ks < D / 16; ++ks) {
-          const bf16x8 of = *(const bf16x8*)(a.o_in + orow + 16 * ks);
-#pragma unroll
-          for (int e = 0; e < 8; ++e) dsum = fmaf((float)dof[ks][e], (float)of[e], dsum);
+          kf[ks] = rows_operand<D>(k_t, w, ks, F, lane);
+          vf[ks] = rows_operand<D>(v_t, w, ks, F, lane);
         }
-      }
-      const float dd = halves_sum(dsum);  // D_q = <dO_q, O_q>
-      const float lse = lse_in;
-      // LSE*log2e, +inf where the query has no valid key or is a padding slot past F (its
-      // probabilities are then 0 in both halves; the last block's wave writes those slots)
-      const float l2 = (q_in && lse != -INFINITY) ? lse * kLog2e : INFINITY;
-      if (hi == 0) {
-        lse_s[q] = l2;
-        nd_s[q] = q_in ? -dd : 0.0f;
-      }
-      f32x16 dq[D / 32];
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db) dq[db] = zero_f32x16();
-      for (int kb = 0; kb < nblk; ++kb) {
-        const unsigned bits = key_bits(km, 0, L, F, kb, lane);
-        if (bits == 0) continue;
-        const int ln = opaque_lane();
-        f32x16 s = zero_f32x16(), dp = zero_f32x16();
-#pragma unroll
-        for (int ks = 0; ks < D / 16; ++ks) {
-          s = mfma32(rows_operand<D>(bufA, kb, ks, F, ln), qf[ks], s);
-          dp = mfma32(rows_operand<D>(bufA + Lds::REGION, kb, ks, F, ln), dof[ks], dp);
-        }
-        float ds[16];
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = ((bits >> acc_row(r, hi)) & 1u) ? fast_exp2(fmaf(s[r], a.scale_log2, -l2)) : 0.0f;
-          ds[r] = p * (dp[r] - dd);
-        }
-        const bf16x8 sb0 = to_bf16x8(&ds[0]), sb1 = to_bf16x8(&ds[8]);
+        f32x16 dk[D / 32], dv[D / 32];
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) {
-          dq[db] = mfma32(frames_operand<D>(bufA, kb, 0, db, F, ln), sb0, dq[db]);
-          dq[db] = mfma32(frames_operand<D>(bufA, kb, 1, db, F, ln), sb1, dq[db]);
+          dk[db] = zero_f32x16();
+          dv[db] = zero_f32x16();
         }
-      }
-      if (q_in) {
-        const size_t orow = row_at(it, q);
+        for (int qb = 0; qb < nblk; ++qb) {
+          const int ln = opaque_lane();
+          f32x16 s = zero_f32x16(), dp;
 #pragma unroll
-        for (int db = 0; db < D / 32; ++db)
+          for (int jj = 0; jj < 4; ++jj) {  // dP accumulates on top of -D of its query rows
+            const f32x4 nd = *(const VC_LDS f32x4*)(nd_s + qb * 32 + 8 * jj + 4 * hi);
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
-            *(bf16x4*)(a.o + orow + db * 32 + 8 * j + 4 * hi) =
-                bf16x4{(__bf16)(dq[db][4 * j + 0] * a.scale), (__bf16)(dq[db][4 * j + 1] * a.scale),
-                       (__bf16)(dq[db][4 * j + 2] * a.scale), (__bf16)(dq[db][4 * j + 3] * a.scale)};
-      }
-      const int ln = opaque_lane();
-#pragma unroll
-      for (int ks = 0; ks < D / 16; ++ks) {
-        kf[ks] = rows_operand<D>(bufA, w, ks, F, ln);
-        vf[ks] = rows_operand<D>(bufA + Lds::REGION, w, ks, F, ln);
-      }
-    }
-    wait_all_memory();
-    __syncthreads();  // Q, dO of item i in B; slot stats written; nobody reads A any more
-    if (i + (int)gridDim.x < items) {
-      const PosItem nx = pos_item(i + gridDim.x, H, L);
-      copy_rows<D>(rows_of(a.k, nx), F, bufA, w);
-      copy_rows<D>(rows_of(a.v, nx), F, bufA + Lds::REGION, w);
-    }
-
-    // ---- lane = key: dV^T = dO^T P, dK^T = c Q^T dS over the query blocks (B: Q, dO) ----
-    if (w < nblk) {
-      const int j = w * 32 + l32;  // this lane's key frame
-      bool valid = j < F;
-      if (km) valid = valid & (km[(size_t)min(j, F - 1) * L] != 0);
-      f32x16 dk[D / 32], dv[D / 32];
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db) {
-        dk[db] = zero_f32x16();
-        dv[db] = zero_f32x16();
-      }
-      for (int qb = 0; qb < nblk; ++qb) {
-        const int ln = opaque_lane();
-        f32x16 s = zero_f32x16(), dp;
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {  // dP accumulates on top of -D of its query rows
-          const f32x4 nd = *(const VC_LDS f32x4*)(nd_s + qb * 32 + 8 * jj + 4 * hi);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) dp[4 * jj + e] = nd[e];
-        }
-#pragma unroll
-        for (int ks = 0; ks < D / 16; ++ks) {
-          s = mfma32(rows_operand<D>(bufB, qb, ks, F, ln), kf[ks], s);
-          dp = mfma32(rows_operand<D>(bufB + Lds::REGION, qb, ks, F, ln), vf[ks], dp);
-        }
-        // An invalid key's P and dS reach only its own lane's dK, dV, written as zero.
-        bf16x8 pb[2], sb[2];
-#pragma unroll
-        for (int h2 = 0; h2 < 2; ++h2) {
-          float p[8], ds[8];
-#pragma unroll
-          for (int jj = 0; jj < 2; ++jj) {
-            const f32x4 l2 = *(const VC_LDS f32x4*)(lse_s + qb * 32 + 8 * (2 * h2 + jj) + 4 * hi);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const int r = 8 * h2 + 4 * jj + e;
-              p[4 * jj + e] = fast_exp2(fmaf(s[r], a.scale_log2, -l2[e]));
-              ds[4 * jj + e] = p[4 * jj + e] * dp[r];
-            }
+            for (int e = 0; e < 4; ++e) dp[4 * jj + e] = nd[e];
           }
-          pb[h2] = to_bf16x8(p);
-          sb[h2] = to_bf16x8(ds);
-        }
-        sched_fence();
 #pragma unroll
-        for (int db = 0; db < D / 32; ++db) {
-          dv[db] = mfma32(frames_operand<D>(bufB + Lds::REGION, qb, 0, db, F, ln), pb[0], dv[db]);
-          dv[db] = mfma32(frames_operand<D>(bufB + Lds::REGION, qb, 1, db, F, ln), pb[1], dv[db]);
-        }
-        sched_fence();
+          for (int ks = 0; ks < D / 16; ++ks) {
+            s = mfma32(rows_operand<D>(q_t, qb, ks, F, ln), kf[ks], s);
+            dp = mfma32(rows_operand<D>(do_t, qb, ks, F, ln), vf[ks], dp);
+          }
+          // An invalid key's P and dS reach only its own lane's dK, dV, written as zero.
+          bf16x8 pb[2], sb[2];
 #pragma unroll
-        for (int db = 0; db < D / 32; ++db) {
-          dk[db] = mfma32(frames_operand<D>(bufB, qb, 0, db, F, ln), sb[0], dk[db]);
-          dk[db] = mfma32(frames_operand<D>(bufB, qb, 1, db, F, ln), sb[1], dk[db]);
+          for (int h2 = 0; h2 < 2; ++h2) {
+            float p[8], ds[8];
+#pragma unroll
+            for (int jj = 0; jj < 2; ++jj) {
+              const f32x4 l2 = *(const VC_LDS f32x4*)(lse_s + qb * 32 + 8 * (2 * h2 + jj) + 4 * hi);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const int r = 8 * h2 + 4 * jj + e;
+                p[4 * jj + e] = fast_exp2(fmaf(s[r], a.scale_log2, -l2[e]));
+                ds[4 * jj + e] = p[4 * jj + e] * dp[r];
+              }
+            }
+            pb[h2] = to_bf16x8(p);
+            sb[h2] = to_bf16x8(ds);
+          }
+          sched_fence();
+#pragma unroll
+          for (int db = 0; db < D / 32; ++db) {
+            dv[db] = mfma32(frames_operand<D>(do_t, qb, 0, db, F, ln), pb[0], dv[db]);
+            dv[db] = mfma32(frames_operand<D>(do_t, qb, 1, db, F, ln), pb[1], dv[db]);
+          }
+          sched_fence();
+#pragma unroll
+          for (int db = 0; db < D / 32; ++db) {
+            dk[db] = mfma32(frames_operand<D>(q_t, qb, 0, db, F, ln), sb[0], dk[db]);
+            dk[db] = mfma32(frames_operand<D>(q_t, qb, 1, db, F, ln), sb[1], dk[db]);
+          }
         }
-      }
-      if (j < F) {
-        const size_t krow = row_at(it, j);
-        auto kv = [&](float x) { return (__bf16)(valid ? x * a.scale : 0.0f); };
-        auto vv = [&](float x) { return (__bf16)(valid ? x : 0.0f); };
+        const float ks_ = valid ? a.scale : 0.0f, vs_ = valid ? 1.0f : 0.0f;
 #pragma unroll
         for (int db = 0; db < D / 32; ++db)
 #pragma unroll
           for (int jj = 0; jj < 4; ++jj) {
-            const int d = db * 32 + 8 * jj + 4 * hi;
-            *(bf16x4*)(a.dk + krow + d) = bf16x4{kv(dk[db][4 * jj + 0]), kv(dk[db][4 * jj + 1]),
-                                                 kv(dk[db][4 * jj + 2]), kv(dk[db][4 * jj + 3])};
-            *(bf16x4*)(a.dv + krow + d) = bf16x4{vv(dv[db][4 * jj + 0]), vv(dv[db][4 * jj + 1]),
-                                                 vv(dv[db][4 * jj + 2]), vv(dv[db][4 * jj + 3])};
+            r0[db][jj] = bf16x4{(__bf16)(dk[db][4 * jj] * ks_), (__bf16)(dk[db][4 * jj + 1] * ks_),
+                                (__bf16)(dk[db][4 * jj + 2] * ks_), (__bf16)(dk[db][4 * jj + 3] * ks_)};
+            r1[db][jj] = bf16x4{(__bf16)(dv[db][4 * jj] * vs_), (__bf16)(dv[db][4 * jj + 1] * vs_),
+                                (__bf16)(dv[db][4 * jj + 2] * vs_), (__bf16)(dv[db][4 * jj + 3] * vs_)};
           }
       }
-      if (i + (int)gridDim.x < items) load_rows(i + gridDim.x);  // the next item's dQ-half inputs
+    } else {
+      // ---- lane = query qb*32 + l32, qb = m and m + 3 ----
+      auto dq_block = [&](int qb, f32x16 (&dq)[D / 32]) {
+        const int q = qb * 32 + l32;
+        bf16x8 qf[D / 16], dof[D / 16];
+#pragma unroll
+        for (int ks = 0; ks < D / 16; ++ks) {
+          qf[ks] = rows_operand<D>(q_t, qb, ks, F, lane);
+          dof[ks] = rows_operand<D>(do_t, qb, ks, F, lane);
+        }
+        const float l2 = lse_s[q];
+        const float nd = nd_s[q];
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) dq[db] = zero_f32x16();
+        for (int kb = 0; kb < nblk; ++kb) {
+          const unsigned bits = block_bits(kb);
+          if (bits == 0) continue;  // no valid key in this block (uniform)
+          const int ln = opaque_lane();
+          f32x16 s = zero_f32x16(), dp = zero_f32x16();
+#pragma unroll
+          for (int ks = 0; ks < D / 16; ++ks) {
+            s = mfma32(rows_operand<D>(k_t, kb, ks, F, ln), qf[ks], s);
+            dp = mfma32(rows_operand<D>(v_t, kb, ks, F, ln), dof[ks], dp);
+          }
+          float ds[16];
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const float p = ((bits >> acc_row(r, hi)) & 1u) ? fast_exp2(fmaf(s[r], a.scale_log2, -l2)) : 0.0f;
+            ds[r] = p * (dp[r] + nd);
+          }
+          const bf16x8 sb0 = to_bf16x8(&ds[0]), sb1 = to_bf16x8(&ds[8]);
+#pragma unroll
+          for (int db = 0; db < D / 32; ++db) {
+            dq[db] = mfma32(frames_operand<D>(k_t, kb, 0, db, F, ln), sb0, dq[db]);
+            dq[db] = mfma32(frames_operand<D>(k_t, kb, 1, db, F, ln), sb1, dq[db]);
+          }
+        }
+      };
+      // Block m + 3 first, stored straight from the accumulator (8-byte pieces), so that
+      // only block m's results are held across the barrier below.
+      if (m + 3 < nblk) {
+        f32x16 dq[D / 32];
+        dq_block(m + 3, dq);
+        const int q = (m + 3) * 32 + l32;
+        if (q < F) {
+#pragma unroll
+          for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+              *(bf16x4*)(a.o + base + (size_t)q * fstride + db * 32 + 8 * j + 4 * hi) =
+                  bf16x4{(__bf16)(dq[db][4 * j] * a.scale), (__bf16)(dq[db][4 * j + 1] * a.scale),
+                         (__bf16)(dq[db][4 * j + 2] * a.scale), (__bf16)(dq[db][4 * j + 3] * a.scale)};
+        }
+      }
+      if (m < nblk) {
+        f32x16 dq[D / 32];
+        dq_block(m, dq);
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            r0[db][j] = bf16x4{(__bf16)(dq[db][4 * j] * a.scale), (__bf16)(dq[db][4 * j + 1] * a.scale),
+                               (__bf16)(dq[db][4 * j + 2] * a.scale), (__bf16)(dq[db][4 * j + 3] * a.scale)};
+      }
+    }
+    __syncthreads();  // every wave is done reading the tiles: they take the results
+
+    if (kv_role) {
+      if (w < nblk) {
+        put_block_rows<D>(q_t, a.dk + base, fstride, w, F, r0);
+        put_block_rows<D>(v_t, a.dv + base, fstride, w, F, r1);
+      }
+    } else if (m < nblk) {
+      put_block_rows<D>(k_t, a.o + base, fstride, m, F, r0);
     }
   }
   wait_all_memory();  // no copy or load of this workgroup outlives it

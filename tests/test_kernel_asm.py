@@ -70,7 +70,7 @@ def test_m0_is_set_only_by_the_lds_copies(device_asm):
             ins = list(instructions(body))
             for i, line in enumerate(ins):
                 if re.search(r"\bm0\b", line):
-                    assert re.match(r"s_mov_b32 m0, s\d+$", line), (fn, name, line)
+                    assert re.match(r"s_mov_b32 m0, (s\d+|vcc_lo|vcc_hi)$", line), (fn, name, line)  # an SGPR
                     nxt = [x for x in ins[i + 1:i + 3] if not x.startswith("s_nop")]
                     assert nxt and nxt[0].startswith("global_load_lds_dwordx4"), (fn, name, ins[i:i + 3])
                 if line.startswith("global_load_lds") or re.match(r"buffer_load\w*.*\blds\b", line):
