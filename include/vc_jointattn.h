@@ -62,7 +62,7 @@ extern "C" {
 /* Raised with every change of a signature, a struct, the meaning of an argument or a
  * documented result; the Python binding refuses a library that reports another
  * version. */
-#define VC_JOINTATTN_ABI_VERSION 9
+#define VC_JOINTATTN_ABI_VERSION 10
 
 typedef enum vc_status {
   VC_OK = 0,
@@ -219,8 +219,9 @@ vc_status vc_jointattn_bwd_dq(const vc_jointattn_desc* desc,
 /* Keys [0, K) whose share of dq the fused pass adds (vc_jointattn_bwd_fused);
  * stage 3 covers keys [K, N). K is the leading 65% of the 256-key blocks at
  * head_dim 128 and every key at head_dim 64 (the fastest splits measured),
- * never more than N. Returns K, or a negative vc_status if the descriptor is
- * invalid. Host only. */
+ * never more than N; 0 when a sample's N*H*D elements reach 2^32 (the fused
+ * pass addresses its accumulator with 32-bit offsets). Returns K, or a negative
+ * vc_status if the descriptor is invalid. Host only. */
 int64_t vc_jointattn_fused_dq_keys(const vc_jointattn_desc* desc);
 
 vc_status vc_jointattn_bwd_fused(const vc_jointattn_desc* desc,
@@ -263,7 +264,9 @@ vc_status vc_spatialattn_fwd(const vc_jointattn_desc* desc,
  * reproducible, no atomics. desc->deterministic = 0: one key-stationary pass also
  * adds every key block's share of dq to an fp32 accumulator with atomics (a video
  * query row gets the shares of its frame's key blocks and of the text block); dk,
- * dv are reproducible run to run, dq only up to the rounding of its fp32 sums. */
+ * dv are reproducible run to run, dq only up to the rounding of its fp32 sums.
+ * When a sample's N*H*D elements reach 2^32 the separate passes run for either
+ * value of the flag. */
 vc_status vc_spatialattn_bwd(const vc_jointattn_desc* desc,
                              const void* q, const void* k, const void* v,
                              const void* o, const float* lse, const void* dout,

@@ -18,7 +18,7 @@ HEADER = os.path.join(os.path.dirname(PKG_DIR), "include", "vc_jointattn.h")
 # The ABI the signatures below describe (VC_JOINTATTN_ABI_VERSION of include/vc_jointattn.h);
 # a library reporting another version is refused, so that no call can reach an entry point
 # whose arguments differ from what this binding passes.
-ABI_VERSION = 9
+ABI_VERSION = 10
 # Bytes of the no-allocation forward's fixed scratch array (VC_JOINTATTN_NOALLOC_SCRATCH_BYTES).
 NOALLOC_SCRATCH_BYTES = 256 << 20
 

@@ -147,7 +147,14 @@ size_t tail_part_bytes(const vc_jointattn_desc* d, int64_t n) {
 // pass then only converts the accumulator.
 constexpr int kFusedDqPercent128 = 65;
 constexpr int kFusedDqPercent64 = 100;
+// The fused pass addresses a sample's fp32 dQ accumulator with 32-bit element offsets, so it
+// runs only while a sample's N*H*D elements fit in 32 bits; larger inputs take the separate
+// passes.
+bool dq_offsets_fit(const vc_jointattn_desc* d, int64_t n) {
+  return n * d->heads * d->head_dim < ((int64_t)1 << 32);
+}
 int fused_dq_blocks(const vc_jointattn_desc* d, int64_t n) {
+  if (!dq_offsets_fit(d, n)) return 0;
   const int nblk = (int)((n + vcja::kDkdvKeys - 1) / vcja::kDkdvKeys);
   const int pct = d->head_dim == 128 ? kFusedDqPercent128 : kFusedDqPercent64;
   return (int)(((int64_t)nblk * pct + 50) / 100);
@@ -551,8 +558,8 @@ vc_status bwd_impl(const vc_jointattn_desc* desc, const void* q, const void* k, 
   // dQ fused into the key-stationary kernel (atomics) unless the caller asks for bitwise
   // reproducible results: joint attention for its leading key blocks (the dQ pass covers
   // the others), the spatial branch for every key block (a video query row gets the shares
-  // of 16 key blocks at 720p, so the atomics are few).
-  if (!desc->deterministic && (spatial || fused_dq_blocks(desc, n) > 0)) {
+  // of 16 key blocks at 720p, so the atomics are few); neither past 32-bit dQ offsets.
+  if (!desc->deterministic && (spatial ? dq_offsets_fit(desc, n) : fused_dq_blocks(desc, n) > 0)) {
     const StageTiles tiles = (spatial || all_keys_fused(desc, n)) ? StageTiles::kNone : StageTiles::kKeys;
     if ((st = prepare_impl(desc, q, k, o, lse, dout, workspace, workspace_bytes, stream, tiles)) != VC_OK ||
         (st = dkdv_impl(desc, q, k, v, dout, text_len, key_mask, dk, dv, workspace, workspace_bytes, stream,

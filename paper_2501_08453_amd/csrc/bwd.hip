@@ -333,7 +333,8 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
     return x;
   };
   // Adds the pending dQ block to the accumulator (rows past N are padding): a uniform base
-  // plus a 32-bit per-lane offset.
+  // plus a 32-bit per-lane offset (the host launches the fused pass only when a sample's
+  // N*H*D elements fit in 32 bits).
   float* const dq_dst = FUSED ? a.dq_acc + (size_t)b * N * tok + (size_t)h * D + dq_db * 32 : nullptr;
   auto flush_dq = [&]() {
     if (dq_row0 < 0) return;
@@ -342,7 +343,7 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(DkdvArgs a
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int qrow = dq_row0 + acc_row(r, half);
-      if (qrow < N) atomicAdd(dq_dst + (unsigned)(qrow * (int)tok + col), dq_blk[r]);
+      if (qrow < N) atomicAdd(dq_dst + ((unsigned)qrow * (unsigned)tok + (unsigned)col), dq_blk[r]);
     }
     dq_row0 = -1;
   };

@@ -108,6 +108,15 @@ def test_fused_dq_keys():
         assert vc.vc_jointattn_fused_dq_keys(vc.make_desc(1, 1, 64, 0, 1, 1, 256 * n_blocks)) == 256 * n_blocks
         assert vc.vc_jointattn_fused_dq_keys(vc.make_desc(1, 1, 64, 0, 1, 1, 256 * n_blocks - 3)) == 256 * n_blocks - 3
     assert vc.vc_jointattn_fused_dq_keys(vc.make_desc(1, 1, 96, 0, 1, 1, 5)) == -3  # head_dim
+    # The fused pass addresses a sample's dQ accumulator with 32-bit offsets: none of it
+    # once N*H*D reaches 2^32 (here 1,166,656 tokens, 144 frames of 8,100 like the paper's
+    # 1.16M-token clip, at 32 heads; at 8 heads it stays below)
+    big = vc.make_desc(1, 32, 128, 256, 144, 90, 90)
+    n = vc.vc_jointattn_tokens(big)
+    assert n * 32 * 128 >= 1 << 32 and vc.vc_jointattn_fused_dq_keys(big) == 0
+    below = vc.make_desc(1, 8, 128, 256, 144, 90, 90)
+    assert vc.vc_jointattn_tokens(below) * 8 * 128 < 1 << 32
+    assert vc.vc_jointattn_fused_dq_keys(below) > 0
 
 
 def test_misaligned_pointers(lib):
