@@ -49,6 +49,10 @@ SMALL = [
     ("F16-ragged", 1, 3, 128, 12, 16, 3, 3, True),
     ("F32", 1, 2, 64, 4, 32, 2, 3, False),
     ("F13-d128", 1, 1, 128, 0, 13, 5, 3, True),
+    # one position per group with many padding slots, and a ragged last group
+    ("F17-masked", 2, 2, 128, 8, 17, 3, 5, True),
+    ("F11-d64", 1, 3, 64, 4, 11, 5, 5, False),
+    ("F31-d64", 1, 2, 64, 0, 31, 2, 4, True),
 ]
 
 
@@ -60,6 +64,8 @@ LONG = [
     ("F100-d128", 1, 1, 128, 40, 100, 4, 4, False),
     ("F144-d128-masked", 1, 2, 128, 12, 144, 2, 5, True),
     ("F144-d64", 1, 3, 64, 0, 144, 3, 3, False),
+    ("F129-d128-one-frame-last-block", 1, 2, 128, 8, 129, 2, 2, True),
+    ("F97-d64", 2, 1, 64, 0, 97, 1, 3, False),
 ]
 
 
