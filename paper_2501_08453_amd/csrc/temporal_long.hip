@@ -465,28 +465,53 @@ __global__ __launch_bounds__(64 * kLongWaves, 1) void temporal_long_bwd_kernel(T
         const float nd = nd_s[q];
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) dq[db] = zero_f32x16();
-        for (int kb = 0; kb < nblk; ++kb) {
+        // Key blocks two at a time (their products interleaved, so that each chain of
+        // matrix-core ops has the other's to overlap), then the odd one.
+        auto sdp = [&](int kb, f32x16& s, f32x16& dp, int ln, int ks) {
+          s = mfma32(rows_operand<D>(k_t, kb, ks, F, ln), qf[ks], s);
+          dp = mfma32(rows_operand<D>(v_t, kb, ks, F, ln), dof[ks], dp);
+        };
+        auto grad = [&](int kb, const f32x16& s, const f32x16& dp, bf16x8& sb0, bf16x8& sb1) {
           const unsigned bits = block_bits(kb);
-          if (bits == 0) continue;  // no valid key in this block (uniform)
-          const int ln = opaque_lane();
-          f32x16 s = zero_f32x16(), dp = zero_f32x16();
-#pragma unroll
-          for (int ks = 0; ks < D / 16; ++ks) {
-            s = mfma32(rows_operand<D>(k_t, kb, ks, F, ln), qf[ks], s);
-            dp = mfma32(rows_operand<D>(v_t, kb, ks, F, ln), dof[ks], dp);
-          }
           float ds[16];
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const float p = ((bits >> acc_row(r, hi)) & 1u) ? fast_exp2(fmaf(s[r], a.scale_log2, -l2)) : 0.0f;
             ds[r] = p * (dp[r] + nd);
           }
-          const bf16x8 sb0 = to_bf16x8(&ds[0]), sb1 = to_bf16x8(&ds[8]);
+          sb0 = to_bf16x8(&ds[0]);
+          sb1 = to_bf16x8(&ds[8]);
+        };
+        auto acc = [&](int kb, bf16x8 sb0, bf16x8 sb1, int ln) {
 #pragma unroll
           for (int db = 0; db < D / 32; ++db) {
             dq[db] = mfma32(frames_operand<D>(k_t, kb, 0, db, F, ln), sb0, dq[db]);
             dq[db] = mfma32(frames_operand<D>(k_t, kb, 1, db, F, ln), sb1, dq[db]);
           }
+        };
+        int kb = 0;
+        for (; kb + 1 < nblk; kb += 2) {
+          const int ln = opaque_lane();
+          f32x16 s0 = zero_f32x16(), dp0 = zero_f32x16(), s1 = zero_f32x16(), dp1 = zero_f32x16();
+#pragma unroll
+          for (int ks = 0; ks < D / 16; ++ks) {
+            sdp(kb, s0, dp0, ln, ks);
+            sdp(kb + 1, s1, dp1, ln, ks);
+          }
+          bf16x8 a0, a1, b0, b1;
+          grad(kb, s0, dp0, a0, a1);
+          grad(kb + 1, s1, dp1, b0, b1);
+          acc(kb, a0, a1, ln);
+          acc(kb + 1, b0, b1, ln);
+        }
+        if (kb < nblk) {
+          const int ln = opaque_lane();
+          f32x16 s0 = zero_f32x16(), dp0 = zero_f32x16();
+#pragma unroll
+          for (int ks = 0; ks < D / 16; ++ks) sdp(kb, s0, dp0, ln, ks);
+          bf16x8 a0, a1;
+          grad(kb, s0, dp0, a0, a1);
+          acc(kb, a0, a1, ln);
         }
       };
       // Block m + 3 first, stored straight from the accumulator (8-byte pieces), so that
