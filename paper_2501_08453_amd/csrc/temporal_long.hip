@@ -177,24 +177,24 @@ __global__ __launch_bounds__(64 * kLongWaves, 1) void temporal_long_fwd_kernel(T
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) oacc[db] = zero_f32x16();
     float m = -INFINITY, l = 0.0f;  // base (log2 units) and this half's sum
-    for (int kb = 0; kb < nblk; ++kb) {
-      const unsigned bits = key_bits(km, 0, L, F, kb, lane);
-      if (bits == 0) continue;  // no valid key in this block (uniform)
-      f32x16 s = zero_f32x16();
-#pragma unroll
-      for (int ks = 0; ks < D / 16; ++ks) s = mfma32(rows_operand<D>(kr, kb, ks, F, lane), qf[ks], s);
-      float mx = -INFINITY;
+    // Key blocks two at a time (the score products of both interleaved, one rescale of the
+    // running base for the pair), then the odd one.
+    auto scores = [&](int kb, unsigned bits, f32x16& s, float& mx) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         s[r] = ((bits >> acc_row(r, hi)) & 1u) ? s[r] * a.scale_log2 : -INFINITY;
         mx = fmaxf(mx, s[r]);
       }
+    };
+    auto rebase = [&](float mx) {
       const float m_new = fmaxf(m, halves_max(mx));
       const float alpha = fast_exp2(m - m_new);  // m = -inf at the first block: 0
       m = m_new;
       l *= alpha;
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) oacc[db] *= alpha;
+    };
+    auto pv = [&](int kb, const f32x16& s) {
       float p[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
@@ -206,6 +206,35 @@ __global__ __launch_bounds__(64 * kLongWaves, 1) void temporal_long_fwd_kernel(T
       for (int db = 0; db < D / 32; ++db) {
         oacc[db] = mfma32(frames_operand<D>(vr, kb, 0, db, F, lane), pb0, oacc[db]);
         oacc[db] = mfma32(frames_operand<D>(vr, kb, 1, db, F, lane), pb1, oacc[db]);
+      }
+    };
+    int kb = 0;
+    for (; kb + 1 < nblk; kb += 2) {
+      const unsigned bits0 = key_bits(km, 0, L, F, kb, lane), bits1 = key_bits(km, 0, L, F, kb + 1, lane);
+      if ((bits0 | bits1) == 0) continue;  // no valid key in either block (uniform)
+      f32x16 s0 = zero_f32x16(), s1 = zero_f32x16();
+#pragma unroll
+      for (int ks = 0; ks < D / 16; ++ks) {
+        s0 = mfma32(rows_operand<D>(kr, kb, ks, F, lane), qf[ks], s0);
+        s1 = mfma32(rows_operand<D>(kr, kb + 1, ks, F, lane), qf[ks], s1);
+      }
+      float mx = -INFINITY;
+      scores(kb, bits0, s0, mx);
+      scores(kb + 1, bits1, s1, mx);
+      rebase(mx);
+      pv(kb, s0);
+      pv(kb + 1, s1);
+    }
+    if (kb < nblk) {
+      const unsigned bits = key_bits(km, 0, L, F, kb, lane);
+      if (bits != 0) {
+        f32x16 s = zero_f32x16();
+#pragma unroll
+        for (int ks = 0; ks < D / 16; ++ks) s = mfma32(rows_operand<D>(kr, kb, ks, F, lane), qf[ks], s);
+        float mx = -INFINITY;
+        scores(kb, bits, s, mx);
+        rebase(mx);
+        pv(kb, s);
       }
     }
     const float lt = halves_sum(l);
