@@ -3,21 +3,22 @@
 // Each spatial position l of a (sample, head) attends across its F frames, the rows
 // T + f*L + l of the joint [B, N, H, D] layout (Sec. III-B regroups [B, F, L, ...] as
 // [B*L, F, ...]). Sequences this long no longer fit one 32-slot matrix-core block, so a
-// workgroup takes one position at a time and splits its frames into blocks of 32:
-// wave j owns query (or key) block j, and walks over the other side's blocks.
+// workgroup takes one position at a time and splits its frames into blocks of 32, each
+// wave walking the other side's blocks for its own block(s), two at a time with the
+// products of the pair interleaved (one block's chain of matrix-core ops alone leaves
+// the loop bound by its latency).
 //
 // The work is bound by memory traffic (about 0.25 KiB per row and head each way against
-// a few hundred flops per byte of matrix work), so the kernels are built to keep HBM
-// busy: a persistent workgroup per compute unit walks a strided sequence of positions
-// (head fastest, so that concurrent workgroups read whole token rows together) and
-// stages the rows the next step reads in LDS while the current step computes.
+// a few hundred flops per byte of matrix work). A persistent workgroup per compute unit
+// walks a strided sequence of positions (head fastest, so that concurrent workgroups read
+// whole token rows together).
 //   Forward: two buffers of K | V rows; while position p is computed from one, the
-//     rows of p+1 are copied into the other.
-//   Backward: buffer A holds K | V, buffer B Q | dO. The lane-per-query half (dQ) reads
-//     A while the Q, dO rows of the same position are copied into B; the lane-per-key
-//     half (dK, dV) reads B while the K, V rows of the next position are copied into A.
-//     D_i = <dO_i, O_i> and LSE_i are formed in the dQ half (no preparation pass, no
-//     workspace) and handed to the dK/dV half through LDS.
+//     rows of p+1 are copied into the other. Wave j owns query block j.
+//   Backward: the four row tiles Q | K | V | dO of one position at once (156 KiB at 144
+//     frames: no second buffer fits). D_i = <dO_i, O_i> (no preparation pass, no
+//     workspace), LSE_i and the valid-key bits are formed first; waves 0-4 then form
+//     dK, dV of one key block each and waves 5-7 dQ of the query blocks; the results
+//     leave as whole rows through the tiles.
 // Rows sit in LDS in the permuted order of the fused joint backward (frame 16g + 4m + i
 // in row 16g + 4i + m) with a 16-byte pad chunk per row, so that the transposing reads of
 // four consecutive frames hit distinct banks; reads past the last frame are clamped to it
