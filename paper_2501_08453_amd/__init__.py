@@ -472,30 +472,93 @@ def temporal_bwd(q, k, v, o, lse, dout, desc, key_mask=None, ws=None):
     return dq, dk, dv
 
 
-def _autograd_function():
+_AUTOGRAD = {}
+
+
+def _autograd_functions():
+    """The autograd wrappers (made once, on first use, so that importing the package does
+    not need torch)."""
+    if _AUTOGRAD:
+        return _AUTOGRAD
     import torch
 
-    class JointAttention(torch.autograd.Function):
-        """Autograd wrapper: forward returns O; LSE is kept for backward."""
+    def branch_fwd(branch, q, k, v, desc, text_len, key_mask):
+        if branch == "joint":
+            return fwd(q, k, v, desc, text_len, key_mask)
+        if branch == "spatial":
+            return spatial_fwd(q, k, v, desc, text_len, key_mask)
+        return temporal_fwd(q, k, v, desc, key_mask)  # no text keys in this branch
+
+    def branch_bwd(branch, q, k, v, o, lse, do, desc, text_len, key_mask):
+        if branch == "joint":
+            return bwd(q, k, v, o, lse, do, desc, text_len, key_mask)
+        if branch == "spatial":
+            return spatial_bwd(q, k, v, o, lse, do, desc, text_len, key_mask)
+        return temporal_bwd(q, k, v, o, lse, do, desc, key_mask)
+
+    class BranchAttention(torch.autograd.Function):
+        """One attention branch ("joint", "spatial" or "temporal"): forward returns O;
+        LSE is kept for backward."""
 
         @staticmethod
-        def forward(ctx, q, k, v, desc, text_len=None, key_mask=None):
-            o, lse = fwd(q, k, v, desc, text_len, key_mask)
+        def forward(ctx, q, k, v, desc, branch, text_len=None, key_mask=None):
+            o, lse = branch_fwd(branch, q, k, v, desc, text_len, key_mask)
             ctx.save_for_backward(q, k, v, o, lse)
-            ctx.desc = desc
-            ctx.text_len = text_len
-            ctx.key_mask = key_mask
+            ctx.desc, ctx.branch, ctx.text_len, ctx.key_mask = desc, branch, text_len, key_mask
             return o
 
         @staticmethod
         def backward(ctx, do):
             q, k, v, o, lse = ctx.saved_tensors
-            dq, dk, dv = bwd(q, k, v, o, lse, do.contiguous(), ctx.desc, ctx.text_len, ctx.key_mask)
-            return dq, dk, dv, None, None, None
+            dq, dk, dv = branch_bwd(ctx.branch, q, k, v, o, lse, do.contiguous(), ctx.desc, ctx.text_len,
+                                    ctx.key_mask)
+            return dq, dk, dv, None, None, None, None
 
-    return JointAttention
+    class ParallelBlockAttention(torch.autograd.Function):
+        """The three branches of the parallel block (Sec. III-B) on one set of q, k, v,
+        summed: forward returns joint + spatial + temporal (the sum fused into the temporal
+        forward); backward hands the same output gradient to every branch and adds their
+        input gradients with the branch-sum kernel (fp32, one rounding)."""
+
+        @staticmethod
+        def forward(ctx, q, k, v, desc, text_len=None, key_mask=None):
+            o_j, l_j = fwd(q, k, v, desc, text_len, key_mask)
+            o_s, l_s = spatial_fwd(q, k, v, desc, text_len, key_mask)
+            o_t, l_t, out = temporal_fwd_sum(q, k, v, desc, o_joint=o_j, o_spatial=o_s, key_mask=key_mask)
+            ctx.save_for_backward(q, k, v, o_j, l_j, o_s, l_s, o_t, l_t)
+            ctx.desc, ctx.text_len, ctx.key_mask = desc, text_len, key_mask
+            return out
+
+        @staticmethod
+        def backward(ctx, do):
+            q, k, v, o_j, l_j, o_s, l_s, o_t, l_t = ctx.saved_tensors
+            do = do.contiguous()
+            desc, tl, km = ctx.desc, ctx.text_len, ctx.key_mask
+            gj = bwd(q, k, v, o_j, l_j, do, desc, tl, km)
+            gs = spatial_bwd(q, k, v, o_s, l_s, do, desc, tl, km)
+            gt = temporal_bwd(q, k, v, o_t, l_t, do, desc, km)
+            grads = tuple(branch_sum(desc, gj[i], gs[i], gt[i], out=gj[i]) for i in range(3))
+            return grads + (None, None, None)
+
+    _AUTOGRAD.update(branch=BranchAttention, block=ParallelBlockAttention)
+    return _AUTOGRAD
 
 
 def joint_attention(q, k, v, desc, text_len=None, key_mask=None):
     """Differentiable joint attention (bf16 in, bf16 out)."""
-    return _autograd_function().apply(q, k, v, desc, text_len, key_mask)
+    return _autograd_functions()["branch"].apply(q, k, v, desc, "joint", text_len, key_mask)
+
+
+def spatial_attention(q, k, v, desc, text_len=None, key_mask=None):
+    """Differentiable spatial-branch attention (bf16 in, bf16 out; text rows of O are 0)."""
+    return _autograd_functions()["branch"].apply(q, k, v, desc, "spatial", text_len, key_mask)
+
+
+def temporal_attention(q, k, v, desc, key_mask=None):
+    """Differentiable temporal-branch attention (bf16 in, bf16 out; text rows of O are 0)."""
+    return _autograd_functions()["branch"].apply(q, k, v, desc, "temporal", None, key_mask)
+
+
+def parallel_block_attention(q, k, v, desc, text_len=None, key_mask=None):
+    """Differentiable sum of the joint, spatial and temporal branches on shared q, k, v."""
+    return _autograd_functions()["block"].apply(q, k, v, desc, text_len, key_mask)

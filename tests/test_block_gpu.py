@@ -18,7 +18,7 @@ import oracle.ref_attention as ora
 import oracle.ref_block as obl
 import oracle.ref_branches as orb
 import workloads as W
-from parity_util import assert_close, bf16_values, log, to_gpu_bf16
+from parity_util import MAX_ABS, assert_close, bf16_values, log, to_gpu_bf16
 
 pytestmark = pytest.mark.gpu
 
@@ -202,3 +202,72 @@ def test_block_sum_long_workload_sampled():
         got.append(bf16_values(out[0, :, h].index_select(0, rows_t)))
         log("   head", h, "oracle done")
     assert_close("sum", np.concatenate(got), np.concatenate(ref))
+
+
+def test_autograd_wrappers():
+    """The differentiable wrappers give what the direct calls give, bit for bit (the
+    deterministic backward, so that no dQ is summed by atomics): each branch alone, and the
+    block, whose output is the fused sum and whose input gradients are the branch sums of
+    the three branches' gradients. The block's are also compared with the block oracle: a
+    gradient is then bf16(g_joint + g_spatial + g_temporal) of three bf16 results, so its
+    max-abs bound is the sum of the three results' own bounds plus half a bf16 spacing of
+    the sum (mean-rel keeps its bar)."""
+    import torch
+    import paper_2501_08453_amd as vc
+    w = W.custom(1, 2, 128, 24, 40, 3, 4, name="autograd", ragged_text=True)  # long-clip temporal
+    x = W.make_inputs(w, seed=77)
+    q, k, v, do = (to_gpu_bf16(x[n]) for n in ("q", "k", "v", "do"))
+    tl = x["text_len"]
+    tl_d = torch.from_numpy(tl).to("cuda")
+    km_np = W.random_key_mask(w, seed=5, keep=0.9)
+    km = torch.from_numpy(km_np).to("cuda")
+    desc = vc.desc_for(w, deterministic=True)
+
+    def run(f, *extra):
+        leaves = [t.clone().requires_grad_(True) for t in (q, k, v)]
+        out = f(*leaves, desc, *extra)
+        out.backward(do)
+        torch.cuda.synchronize()
+        return out.detach(), [t.grad for t in leaves]
+
+    direct = {
+        "joint": (vc.joint_attention, (tl_d, km), lambda: vc.fwd(q, k, v, desc, tl_d, km),
+                  lambda o, l: vc.bwd(q, k, v, o, l, do, desc, tl_d, km)),
+        "spatial": (vc.spatial_attention, (tl_d, km), lambda: vc.spatial_fwd(q, k, v, desc, tl_d, km),
+                    lambda o, l: vc.spatial_bwd(q, k, v, o, l, do, desc, tl_d, km)),
+        "temporal": (vc.temporal_attention, (km,), lambda: vc.temporal_fwd(q, k, v, desc, km),
+                     lambda o, l: vc.temporal_bwd(q, k, v, o, l, do, desc, km)),
+    }
+    grads = {}
+    for name, (wrap, extra, f, b) in direct.items():
+        out, g = run(wrap, *extra)
+        o_d, l_d = f()
+        g_d = b(o_d, l_d)
+        torch.cuda.synchronize()
+        assert torch.equal(out, o_d), name
+        for t, r, n in zip(g, g_d, ("dq", "dk", "dv")):
+            assert torch.equal(t, r), (name, n)
+        grads[name] = g_d
+        log("   wrapper", name, "equals the direct calls")
+
+    out, g = run(vc.parallel_block_attention, tl_d, km)
+    o_j, _ = vc.fwd(q, k, v, desc, tl_d, km)
+    o_s, _ = vc.spatial_fwd(q, k, v, desc, tl_d, km)
+    _, _, out_d = vc.temporal_fwd_sum(q, k, v, desc, o_joint=o_j, o_spatial=o_s, key_mask=km)
+    torch.cuda.synchronize()
+    assert torch.equal(out, out_d)
+    for i, n in enumerate(("dq", "dk", "dv")):
+        s = vc.branch_sum(desc, *(grads[b][i] for b in ("joint", "spatial", "temporal")))
+        torch.cuda.synchronize()
+        assert torch.equal(g[i], s), n
+    hq, hk, hv, hdo = (bf16_values(t) for t in (q, k, v, do))
+    inputs = {n: (hq, hk, hv) for n in obl.BRANCHES}
+    T, F = w.text_slot, w.frames
+    ref_out, br = obl.block_forward(inputs, T, F, tl, km_np)
+    ref = obl.block_backward(inputs, hdo, T, F, tl, km_np, branches=br)
+    assert_close("block out", bf16_values(out), ref_out)
+    for i, n in enumerate(("dQ", "dK", "dV")):
+        total = sum(ref[b][i] for b in obl.BRANCHES)
+        bound = sum(max(MAX_ABS, float(_bf16_spacing(np.max(np.abs(ref[b][i]))))) for b in obl.BRANCHES)
+        bound += 0.5 * float(_bf16_spacing(np.max(np.abs(total))))
+        assert_close("block " + n, bf16_values(g[i]), total, max_abs=bound)
